@@ -1,0 +1,282 @@
+/*
+ * oracle.c -- plain, slow, obviously correct CPU scorer for regression-tree ensembles.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the bench's CPU-baseline leg
+ * load this library. It shares no code, header, table or helper with the GPU library; it
+ * reads the caller's flat creation-order arrays directly and never a packed layout.
+ *
+ * What it computes (Section 3 of the paper, first paragraphs): a tree is walked from its
+ * root; at an internal node holding feature id f and threshold theta the walk goes left when
+ * x[f] < theta and right otherwise, until it reaches a leaf. The feature vector is a dense
+ * float array indexed by feature id (Section 3, dense-vector assumption). An ensemble's score
+ * is the sum over its trees of the reached leaves' values (Section 5.3: an outer loop over the
+ * trees). Scores are summed in double precision in tree order.
+ *
+ * rule 0 (paper): right iff x[f] >= theta.   rule 1: right iff x[f] > theta.
+ * Under IEEE comparison a NaN feature value is never >= (nor >) a threshold, so it goes left.
+ *
+ * Three independent walks reach the leaf:
+ *   walk 0 -- branching walk over explicit left/right links (the Struct form, Section 3);
+ *   walk 1 -- predicated walk: the comparison result, 0 or 1, indexes the pair
+ *             {left, right} (the branch-free step of the Pred form, Section 3, with explicit
+ *             children);
+ *   oracle_score_padded -- the literal Pred form: the tree is padded with dummy nodes to a
+ *             complete tree of its depth d, laid out breadth-first (children of i at 2i+1 and
+ *             2i+2), and walked with exactly d steps i = 2i + 1 + bit. A dummy node's two
+ *             subtrees both end at the original leaf it replaces, so padding does not change
+ *             the prediction (Section 3, end of Pred; Section 6 on unbalanced trees).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_E_MODEL 1 /* a child id out of range or a walk longer than the tree */
+#define ORACLE_E_ARG 2
+#define ORACLE_E_NOMEM 3
+
+static int goes_right(float x, float theta, int rule)
+{
+    if (rule == 0)
+        return x >= theta;
+    return x > theta;
+}
+
+/* Branching (walk 0) or predicated (walk 1) walk of one tree for one document. Returns the
+ * tree-local leaf id, or -1 when the tree is malformed. *steps receives the number of internal
+ * nodes visited (the comparisons made). */
+static int32_t walk_tree(int64_t n_nodes, const int32_t *feature, const float *threshold,
+                         const int32_t *left, const int32_t *right, const float *x,
+                         int32_t n_features, int rule, int walk, int64_t *steps)
+{
+    int64_t n = 0;
+    int64_t k = 0;
+    while (feature[n] >= 0) {
+        int32_t f = feature[n];
+        if (f >= n_features || k >= n_nodes)
+            return -1;
+        int32_t next;
+        if (walk == 0) {
+            if (goes_right(x[f], threshold[n], rule))
+                next = right[n];
+            else
+                next = left[n];
+        } else {
+            int32_t kids[2];
+            kids[0] = left[n];
+            kids[1] = right[n];
+            next = kids[goes_right(x[f], threshold[n], rule)];
+        }
+        if (next < 0 || next >= n_nodes)
+            return -1;
+        n = next;
+        k++;
+    }
+    *steps = k;
+    return (int32_t)n;
+}
+
+/*
+ * Score n_docs documents (row-major X[n_docs][n_features]) with the ensemble.
+ *   scores   [n_docs] doubles, or NULL
+ *   leaf_ids [n_docs][n_trees] tree-local leaf ids, or NULL
+ *   visits   total number of internal nodes visited over all (document, tree) pairs, or NULL
+ * Returns ORACLE_OK or an error code.
+ */
+int oracle_score(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                 const float *threshold, const int32_t *left, const int32_t *right,
+                 const float *value, const float *X, int64_t n_docs, int32_t n_features,
+                 int32_t rule, int32_t walk, int32_t n_threads, double *scores,
+                 int32_t *leaf_ids, int64_t *visits)
+{
+    if (n_trees < 0 || n_docs < 0 || n_features < 0 || (n_trees > 0 && !tree_offsets))
+        return ORACLE_E_ARG;
+    int err = ORACLE_OK;
+    int64_t total_steps = 0;
+#ifdef _OPENMP
+    if (n_threads > 0)
+        omp_set_num_threads(n_threads);
+#endif
+#pragma omp parallel for schedule(dynamic, 16) reduction(+ : total_steps)
+    for (int64_t d = 0; d < n_docs; d++) {
+        const float *x = X + d * (int64_t)n_features;
+        double s = 0.0;
+        for (int32_t t = 0; t < n_trees; t++) {
+            int64_t a = tree_offsets[t];
+            int64_t nn = tree_offsets[t + 1] - a;
+            int64_t steps = 0;
+            int32_t leaf = -1;
+            if (nn > 0)
+                leaf = walk_tree(nn, feature + a, threshold + a, left + a, right + a, x, n_features,
+                                 rule, walk, &steps);
+            if (leaf < 0) {
+#pragma omp atomic write
+                err = ORACLE_E_MODEL;
+                continue;
+            }
+            s += (double)value[a + leaf];
+            total_steps += steps;
+            if (leaf_ids)
+                leaf_ids[d * (int64_t)n_trees + t] = leaf;
+        }
+        if (scores)
+            scores[d] = s;
+    }
+    if (visits)
+        *visits = total_steps;
+    return err;
+}
+
+/* Depth (edges on the longest root-to-leaf path) of a tree, or -1 if malformed. */
+static int32_t tree_depth(int64_t n_nodes, const int32_t *feature, const int32_t *left,
+                          const int32_t *right)
+{
+    /* iterative DFS with an explicit stack of (node, depth) */
+    int64_t *stack = (int64_t *)malloc(sizeof(int64_t) * 2 * (size_t)(n_nodes + 1));
+    if (!stack)
+        return -1;
+    int64_t top = 0, visited = 0;
+    int32_t best = 0;
+    stack[0] = 0;
+    stack[1] = 0;
+    top = 1;
+    while (top > 0) {
+        top--;
+        int64_t n = stack[2 * top], dep = stack[2 * top + 1];
+        if (++visited > n_nodes || n < 0 || n >= n_nodes) {
+            free(stack);
+            return -1;
+        }
+        if (dep > best)
+            best = (int32_t)dep;
+        if (feature[n] >= 0) {
+            stack[2 * top] = left[n];
+            stack[2 * top + 1] = dep + 1;
+            top++;
+            stack[2 * top] = right[n];
+            stack[2 * top + 1] = dep + 1;
+            top++;
+        }
+    }
+    free(stack);
+    return best;
+}
+
+/* Fill the padded breadth-first arrays of a complete tree of depth `depth`: slot `slot` at
+ * level `level` holds original node `node`. A leaf met above the last level becomes a dummy
+ * node (feature 0, threshold 0) whose two subtrees both carry that leaf. */
+static void pad_fill(int64_t slot, int32_t node, int32_t level, int32_t depth,
+                     const int32_t *feature, const float *threshold, const int32_t *left,
+                     const int32_t *right, int32_t *pfid, float *pthr, int32_t *pleaf)
+{
+    int64_t n_internal = ((int64_t)1 << depth) - 1;
+    if (level == depth) {
+        pleaf[slot - n_internal] = node;
+        return;
+    }
+    if (feature[node] >= 0) {
+        pfid[slot] = feature[node];
+        pthr[slot] = threshold[node];
+        pad_fill(2 * slot + 1, left[node], level + 1, depth, feature, threshold, left, right, pfid,
+                 pthr, pleaf);
+        pad_fill(2 * slot + 2, right[node], level + 1, depth, feature, threshold, left, right, pfid,
+                 pthr, pleaf);
+    } else {
+        pfid[slot] = 0;
+        pthr[slot] = 0.0f;
+        pad_fill(2 * slot + 1, node, level + 1, depth, feature, threshold, left, right, pfid, pthr,
+                 pleaf);
+        pad_fill(2 * slot + 2, node, level + 1, depth, feature, threshold, left, right, pfid, pthr,
+                 pleaf);
+    }
+}
+
+/*
+ * Same outputs as oracle_score, reached by the literal padded Pred walk. Trees deeper than
+ * max_depth (at most 24) are rejected with ORACLE_E_ARG, since the padded array has 2^(d+1)-1
+ * slots. Needs n_features >= 1 when any tree is padded (dummy nodes read feature 0).
+ */
+int oracle_score_padded(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                        const float *threshold, const int32_t *left, const int32_t *right,
+                        const float *value, const float *X, int64_t n_docs, int32_t n_features,
+                        int32_t rule, int32_t max_depth, double *scores, int32_t *leaf_ids)
+{
+    if (n_trees < 0 || n_docs < 0 || max_depth > 24)
+        return ORACLE_E_ARG;
+    int32_t **pfid = (int32_t **)calloc((size_t)n_trees + 1, sizeof(int32_t *));
+    float **pthr = (float **)calloc((size_t)n_trees + 1, sizeof(float *));
+    int32_t **pleaf = (int32_t **)calloc((size_t)n_trees + 1, sizeof(int32_t *));
+    int32_t *depth = (int32_t *)calloc((size_t)n_trees + 1, sizeof(int32_t));
+    int err = ORACLE_OK;
+    if (!pfid || !pthr || !pleaf || !depth)
+        err = ORACLE_E_NOMEM;
+    for (int32_t t = 0; t < n_trees && err == ORACLE_OK; t++) {
+        int64_t a = tree_offsets[t];
+        int64_t nn = tree_offsets[t + 1] - a;
+        int32_t d = nn > 0 ? tree_depth(nn, feature + a, left + a, right + a) : -1;
+        if (d < 0) {
+            err = ORACLE_E_MODEL;
+            break;
+        }
+        if (d > max_depth || (d > 0 && n_features < 1)) {
+            err = ORACLE_E_ARG;
+            break;
+        }
+        depth[t] = d;
+        int64_t n_int = ((int64_t)1 << d) - 1;
+        pfid[t] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_int + 1));
+        pthr[t] = (float *)malloc(sizeof(float) * (size_t)(n_int + 1));
+        pleaf[t] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n_int + 1));
+        if (!pfid[t] || !pthr[t] || !pleaf[t]) {
+            err = ORACLE_E_NOMEM;
+            break;
+        }
+        pad_fill(0, 0, 0, d, feature + a, threshold + a, left + a, right + a, pfid[t], pthr[t],
+                 pleaf[t]);
+    }
+    if (err == ORACLE_OK) {
+        for (int64_t doc = 0; doc < n_docs; doc++) {
+            const float *x = X + doc * (int64_t)n_features;
+            double s = 0.0;
+            for (int32_t t = 0; t < n_trees; t++) {
+                int64_t i = 0;
+                for (int32_t k = 0; k < depth[t]; k++)
+                    i = (i << 1) + 1 + goes_right(x[pfid[t][i]], pthr[t][i], rule);
+                int32_t leaf = pleaf[t][i - (((int64_t)1 << depth[t]) - 1)];
+                s += (double)value[tree_offsets[t] + leaf];
+                if (leaf_ids)
+                    leaf_ids[doc * (int64_t)n_trees + t] = leaf;
+            }
+            if (scores)
+                scores[doc] = s;
+        }
+    }
+    for (int32_t t = 0; t < n_trees; t++) {
+        if (pfid)
+            free(pfid[t]);
+        if (pthr)
+            free(pthr[t]);
+        if (pleaf)
+            free(pleaf[t]);
+    }
+    free(pfid);
+    free(pthr);
+    free(pleaf);
+    free(depth);
+    return err;
+}
+
+/* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
+int oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

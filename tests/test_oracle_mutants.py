@@ -1,0 +1,63 @@
+"""Mutation check of the oracle pins: each plausible mistake is planted in a *copy* of
+oracle.c (never in the GPU library), the copy is built, and the pin suite must fail on it.
+This shows that a dropped term, a flipped comparison, a swapped child, a wrong index or a
+lower-precision sum in the oracle would not go unnoticed."""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+# (name, text in oracle.c, replacement, which occurrence: 0 = first only, None = all)
+MUTANTS = [
+    ("tie_rule_flipped", "return x >= theta;", "return x > theta;", None),
+    ("strict_rule_flipped", "return x > theta;", "return x >= theta;", None),
+    ("branch_right_goes_left", "next = right[n];", "next = left[n];", None),
+    ("pred_right_child_is_left", "kids[1] = right[n];", "kids[1] = left[n];", None),
+    ("first_tree_dropped", "for (int32_t t = 0; t < n_trees; t++) {\n            int64_t a = tree_offsets[t];",
+     "for (int32_t t = 1; t < n_trees; t++) {\n            int64_t a = tree_offsets[t];", 0),
+    ("float_accumulator", "double s = 0.0;", "float s = 0.0f;", None),
+    ("feature_index_off_by_one", "goes_right(x[f], threshold[n], rule)", "goes_right(x[f > 0 ? f - 1 : f], threshold[n], rule)", None),
+    ("leaf_value_index_shifted", "s += (double)value[a + leaf];", "s += (double)value[a + leaf - (leaf > 1)];", None),
+    ("padded_walk_mirrored", "i = (i << 1) + 1 + goes_right(", "i = (i << 1) + 2 - goes_right(", None),
+    ("padded_dummy_loses_leaf", "pad_fill(2 * slot + 2, node, level + 1,", "pad_fill(2 * slot + 2, 0, level + 1,", None),
+    ("visit_count_doubled", "        k++;\n", "        k += 2;\n", None),
+    ("threshold_of_wrong_node", "goes_right(x[f], threshold[n], rule)", "goes_right(x[f], threshold[n > 0 ? n - 1 : n], rule)", None),
+]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,old,new,occ", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new, occ):
+    src = open(oracle.SRC).read()
+    assert old in src, f"mutation site for {name} vanished from oracle.c; update the mutant list"
+    mutated = src.replace(old, new, 1) if occ == 0 else src.replace(old, new)
+    assert mutated != src
+    csrc = tmp_path / "oracle_mutant.c"
+    csrc.write_text(mutated)
+    lib = str(tmp_path / "liboracle_mutant.so")
+    oracle.build(out=lib, src=str(csrc), extra=("-Wno-error",))
+    env = dict(os.environ, ORACLE_LIB=lib)
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
+
+
+@pytest.mark.slow
+def test_unmutated_copy_passes(tmp_path):
+    # control: the same build-and-run route with the source unchanged must pass, so a failure
+    # above is the mutation's doing and not the harness's
+    lib = str(tmp_path / "liboracle_copy.so")
+    oracle.build(out=lib)
+    env = dict(os.environ, ORACLE_LIB=lib)
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode == 0, r.stdout[-3000:]
