@@ -1,0 +1,130 @@
+/*
+ * tree_ens.h -- C ABI of the MI355X (gfx950) tree-ensemble scorer.
+ *
+ * The operation (paper, Section 3 and Section 5.3): a model is an ensemble of binary
+ * regression trees. Each internal node holds a feature id f and a threshold theta; a document's
+ * walk goes left when x[f] < theta and right otherwise (the Pred form writes the test as
+ * x[f] >= theta), until it reaches a leaf, which holds a regression value. A document is a
+ * dense float vector indexed by feature id (Section 3). The ensemble score of a document is the
+ * sum of the reached leaves' values over all trees (Section 5.3: an outer loop over the trees).
+ *
+ * No HIP or framework header is needed to include this file. Device pointers are plain
+ * pointers into memory of the device that was current when the model was created (for example
+ * a torch tensor's data_ptr()). Streams are passed as void* and are hipStream_t values
+ * (0 = the null stream).
+ *
+ * Every function returns TREE_ENS_OK (0) or a negative status; on failure
+ * tree_ens_last_error() returns a message for the calling thread. No function throws.
+ */
+#ifndef TREE_ENS_H
+#define TREE_ENS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tree_ens tree_ens_t;
+
+/* status codes */
+#define TREE_ENS_OK 0
+#define TREE_ENS_E_ARG (-1)    /* a null pointer where one is required, a negative count, a
+                                  misaligned pointer, or unknown flag bits */
+#define TREE_ENS_E_MODEL (-2)  /* the flat arrays do not describe an ensemble of trees (see
+                                  tree_ens_create), or a tree is too large for one LDS tile */
+#define TREE_ENS_E_SHAPE (-3)  /* the documents carry fewer features than the model reads */
+#define TREE_ENS_E_DEVICE (-4) /* a HIP call failed (no device, launch or copy error) */
+#define TREE_ENS_E_NOMEM (-5)  /* host or device allocation failed */
+
+/* create-time flags */
+#define TREE_ENS_RIGHT_IF_GE 0u /* right iff x[f] >= theta: the paper's rule (default) */
+#define TREE_ENS_RIGHT_IF_GT 1u /* right iff x[f] >  theta: the other tie convention */
+
+/*
+ * tree_ens_create -- validate an ensemble given as flat host arrays, pack it for the GPU and
+ * upload it to the current device (the model representation of Section 3: per node a feature
+ * id and a threshold, explicit left/right links as in the Struct and Struct+ forms, and leaf
+ * values).
+ *
+ *   out           receives the handle; set to NULL on failure.
+ *   n_trees       number of trees, >= 0 (0 gives all-zero scores).
+ *   tree_offsets  [n_trees+1] int64: tree t owns flat nodes [tree_offsets[t], tree_offsets[t+1]);
+ *                 tree_offsets[0] == 0, every tree has at least one node.
+ *   feature       [n_nodes] int32: feature id (>= 0) of an internal node, -1 for a leaf.
+ *   threshold     [n_nodes] float: threshold of an internal node (NaN rejected); ignored for
+ *                 leaves.
+ *   left, right   [n_nodes] int32: tree-local child ids of an internal node; ignored for leaves.
+ *                 Node 0 of every tree is its root.
+ *   value         [n_nodes] float: leaf values; ignored for internal nodes.
+ *   flags         TREE_ENS_RIGHT_IF_GE or TREE_ENS_RIGHT_IF_GT.
+ *
+ * All arrays are host memory, read during the call only; the caller keeps ownership. Node ids
+ * need not be in any particular order. TREE_ENS_E_MODEL is returned when a child id is out of
+ * range or names the root, a node has two parents, a node is unreachable from the root, a
+ * threshold is NaN, a feature id is below -1, a tree has more nodes than one LDS tile holds
+ * (reported in the message), or a feature id exceeds the LDS document-tile limit. Validation
+ * happens before any HIP call, so model errors are reported on a host without a GPU. The
+ * handle owns the device copy and is immutable; it may be used from several streams at once.
+ */
+int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offsets,
+                    const int32_t *feature, const float *threshold, const int32_t *left,
+                    const int32_t *right, const float *value, uint32_t flags);
+
+/*
+ * tree_ens_predict -- score n_docs documents (the ensemble sum of Section 5.3).
+ *
+ *   h           a handle from tree_ens_create.
+ *   stream      hipStream_t the work is enqueued on (0 = null stream). The call returns without
+ *               waiting; scores are valid once the stream reaches this point, and X must stay
+ *               unchanged until then.
+ *   X           device, row-major float [n_docs][n_features], 4-byte aligned (rows contiguous,
+ *               row stride n_features).
+ *   n_docs      >= 0; 0 returns TREE_ENS_OK without a launch.
+ *   n_features  row length; must be >= 1 + the largest feature id of the model (else
+ *               TREE_ENS_E_SHAPE). Columns beyond the ones the model reads are never read.
+ *   scores      device, float [n_docs]: the sum of the reached leaf values, accumulated in
+ *               double precision and rounded once to float.
+ *
+ * Kernel faults surface at the caller's next synchronisation with the stream. Small batches
+ * use a stream-ordered scratch allocation (hipMallocAsync / hipFreeAsync on `stream`).
+ */
+int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                     int32_t n_features, float *scores);
+
+/*
+ * tree_ens_predict_leaves -- the leaf each (document, tree) pair reaches, by the same walk.
+ *
+ *   leaf_ids  device, int32 [n_docs][n_trees] row-major: the tree-local id, in the caller's
+ *             input numbering, of the leaf that document d reaches in tree t.
+ * Other arguments and behaviour as tree_ens_predict.
+ */
+int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                            int32_t n_features, int32_t *leaf_ids);
+
+/*
+ * tree_ens_info -- facts about a packed model; every output pointer may be NULL.
+ *   n_trees        number of trees.
+ *   min_features   1 + the largest feature id any node reads (0 if there is none).
+ *   max_depth      edges on the longest root-to-leaf path over all trees.
+ *   packed_bytes   bytes of node records on the device.
+ *   n_tiles        LDS tiles the trees are streamed in for a large batch.
+ *   docs_per_block documents a workgroup stages in LDS (a power of two from 8 to 64).
+ */
+int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features,
+                  int32_t *max_depth, int64_t *packed_bytes, int32_t *n_tiles,
+                  int32_t *docs_per_block);
+
+/* tree_ens_destroy -- free the handle and its device memory. NULL is accepted. The caller must
+ * ensure no enqueued predict that uses h is still pending. */
+void tree_ens_destroy(tree_ens_t *h);
+
+/* tree_ens_last_error -- message for the last failure on the calling thread ("" if none). The
+ * pointer stays valid until the next call into the library on this thread. */
+const char *tree_ens_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREE_ENS_H */

@@ -1,0 +1,239 @@
+"""ctypes binding of ``libtreeens.so``: the C ABI of ``include/tree_ens.h`` under the same
+names, plus a small ``TreeEnsemble`` owner class. Argument marshalling only -- every step of
+scoring runs in the HIP kernels; torch supplies device memory and the current stream.
+
+The library is loaded from this package's directory and never built here: if it is missing the
+first call raises ``TreeEnsLibraryMissing`` (build it with ``__graft_entry__.build()``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libtreeens.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "tree_ens.h")
+
+TREE_ENS_OK = 0
+TREE_ENS_E_ARG = -1
+TREE_ENS_E_MODEL = -2
+TREE_ENS_E_SHAPE = -3
+TREE_ENS_E_DEVICE = -4
+TREE_ENS_E_NOMEM = -5
+TREE_ENS_RIGHT_IF_GE = 0
+TREE_ENS_RIGHT_IF_GT = 1
+
+_CODE_NAMES = {0: "OK", -1: "E_ARG", -2: "E_MODEL", -3: "E_SHAPE", -4: "E_DEVICE", -5: "E_NOMEM"}
+
+
+class TreeEnsLibraryMissing(RuntimeError):
+    pass
+
+
+class TreeEnsError(RuntimeError):
+    def __init__(self, code: int, where: str, message: str):
+        super().__init__(f"{where}: {_CODE_NAMES.get(code, code)} ({code}): {message}")
+        self.code = code
+        self.message = message
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load (once) and return the HIP library; raise if it has not been built."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    # torch ships its own HIP runtime under the same soname (libamdhip64.so.7) as the system
+    # one this library links against. Importing torch first makes the loader resolve this
+    # library's dependency to the runtime torch already uses, so the process has one HIP
+    # runtime and torch's streams and allocations are valid here.
+    import torch  # noqa: F401
+    if not os.path.exists(path):
+        raise TreeEnsLibraryMissing(
+            f"{path} is missing: the gfx950 HIP library must be built (__graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    P, i32, i64, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+    lib.tree_ens_create.restype = ctypes.c_int
+    lib.tree_ens_create.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, P, P, u32]
+    lib.tree_ens_predict.restype = ctypes.c_int
+    lib.tree_ens_predict.argtypes = [P, P, P, i64, i32, P]
+    lib.tree_ens_predict_leaves.restype = ctypes.c_int
+    lib.tree_ens_predict_leaves.argtypes = [P, P, P, i64, i32, P]
+    lib.tree_ens_info.restype = ctypes.c_int
+    lib.tree_ens_info.argtypes = [P, P, P, P, P, P, P]
+    lib.tree_ens_destroy.restype = None
+    lib.tree_ens_destroy.argtypes = [P]
+    lib.tree_ens_last_error.restype = ctypes.c_char_p
+    lib.tree_ens_last_error.argtypes = []
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def header_functions(header: str = HEADER) -> list[str]:
+    """Names of the functions ``include/tree_ens.h`` declares."""
+    text = open(header).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tree_ens_[a-z_]+)\s*\(", text)))
+
+
+def tree_ens_last_error() -> str:
+    return load_library().tree_ens_last_error().decode()
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != TREE_ENS_OK:
+        raise TreeEnsError(rc, where, tree_ens_last_error())
+
+
+def _arr(a, dtype):
+    return np.ascontiguousarray(np.asarray(a), dtype=dtype)
+
+
+def tree_ens_create(tree_offsets, feature, threshold, left, right, value,
+                    flags: int = TREE_ENS_RIGHT_IF_GE) -> ctypes.c_void_p:
+    """Validate, pack and upload an ensemble given as flat creation-order arrays (host)."""
+    lib = load_library()
+    off = _arr(tree_offsets, np.int64)
+    fe, th = _arr(feature, np.int32), _arr(threshold, np.float32)
+    le, ri, va = _arr(left, np.int32), _arr(right, np.int32), _arr(value, np.float32)
+    n_trees = int(off.shape[0]) - 1
+    if n_trees < 0:
+        raise ValueError("tree_offsets needs n_trees + 1 entries")
+    n = int(off[-1]) if n_trees > 0 else 0
+    for name, a in (("feature", fe), ("threshold", th), ("left", le), ("right", ri), ("value", va)):
+        if a.shape[0] < n:
+            raise ValueError(f"{name} has {a.shape[0]} entries; tree_offsets asks for {n}")
+    h = ctypes.c_void_p()
+
+    def ptr(a):
+        return a.ctypes.data if a.size else None
+
+    rc = lib.tree_ens_create(ctypes.byref(h), n_trees, ptr(off), ptr(fe), ptr(th), ptr(le), ptr(ri),
+                             ptr(va), int(flags))
+    _check(rc, "tree_ens_create")
+    return h
+
+
+def _stream_of(t, stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream(t.device).cuda_stream
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+def _check_docs(X):
+    import torch
+    if not isinstance(X, torch.Tensor) or X.device.type != "cuda":
+        raise TypeError("X must be a CUDA (HIP) torch tensor")
+    if X.dtype != torch.float32 or X.dim() != 2 or not X.is_contiguous():
+        raise TypeError("X must be a contiguous float32 [n_docs, n_features] tensor")
+
+
+def tree_ens_predict(h, X, scores=None, stream=None):
+    """Scores of the documents ``X`` (device float32 [n_docs, n_features]) as float32 [n_docs],
+    enqueued on ``stream`` (default: torch's current stream for X's device)."""
+    import torch
+    _check_docs(X)
+    n_docs, n_feat = X.shape
+    if scores is None:
+        scores = torch.empty(n_docs, dtype=torch.float32, device=X.device)
+    elif scores.dtype != torch.float32 or scores.numel() < n_docs or not scores.is_contiguous() \
+            or scores.device != X.device:
+        raise TypeError("scores must be a contiguous float32 tensor of n_docs entries on X's device")
+    rc = load_library().tree_ens_predict(h, _stream_of(X, stream), X.data_ptr() if n_docs else None,
+                                         n_docs, n_feat, scores.data_ptr() if n_docs else None)
+    _check(rc, "tree_ens_predict")
+    return scores
+
+
+def tree_ens_predict_leaves(h, X, leaf_ids=None, stream=None):
+    """Leaf reached per (document, tree), int32 [n_docs, n_trees], tree-local input node ids."""
+    import torch
+    _check_docs(X)
+    n_docs, n_feat = X.shape
+    n_trees = tree_ens_info(h)["n_trees"]
+    if leaf_ids is None:
+        leaf_ids = torch.empty((n_docs, n_trees), dtype=torch.int32, device=X.device)
+    elif leaf_ids.dtype != torch.int32 or leaf_ids.numel() < n_docs * n_trees or \
+            not leaf_ids.is_contiguous() or leaf_ids.device != X.device:
+        raise TypeError("leaf_ids must be a contiguous int32 tensor of n_docs*n_trees entries")
+    rc = load_library().tree_ens_predict_leaves(h, _stream_of(X, stream), X.data_ptr() if n_docs else None,
+                                                n_docs, n_feat,
+                                                leaf_ids.data_ptr() if n_docs * n_trees else None)
+    _check(rc, "tree_ens_predict_leaves")
+    return leaf_ids
+
+
+def tree_ens_info(h) -> dict:
+    lib = load_library()
+    nt, mf, md, nt2, dpb = (ctypes.c_int32() for _ in range(5))
+    pb = ctypes.c_int64()
+    rc = lib.tree_ens_info(h, ctypes.byref(nt), ctypes.byref(mf), ctypes.byref(md), ctypes.byref(pb),
+                           ctypes.byref(nt2), ctypes.byref(dpb))
+    _check(rc, "tree_ens_info")
+    return {"n_trees": nt.value, "min_features": mf.value, "max_depth": md.value,
+            "packed_bytes": pb.value, "n_tiles": nt2.value, "docs_per_block": dpb.value}
+
+
+def tree_ens_destroy(h) -> None:
+    if h is not None:
+        load_library().tree_ens_destroy(h)
+
+
+class TreeEnsemble:
+    """Owner of a packed model on the current device.
+
+    ``TreeEnsemble.from_arrays(tree_offsets, feature, threshold, left, right, value, flags)``
+    or ``TreeEnsemble.from_ensemble(ens)`` for any object with those attributes."""
+
+    def __init__(self, handle):
+        self._h = handle
+
+    @classmethod
+    def from_arrays(cls, tree_offsets, feature, threshold, left, right, value,
+                    flags: int = TREE_ENS_RIGHT_IF_GE) -> "TreeEnsemble":
+        return cls(tree_ens_create(tree_offsets, feature, threshold, left, right, value, flags))
+
+    @classmethod
+    def from_ensemble(cls, ens, flags: int = TREE_ENS_RIGHT_IF_GE) -> "TreeEnsemble":
+        return cls.from_arrays(ens.tree_offsets, ens.feature, ens.threshold, ens.left, ens.right,
+                               ens.value, flags)
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("model was destroyed")
+        return self._h
+
+    def predict(self, X, out=None, stream=None):
+        return tree_ens_predict(self.handle, X, out, stream)
+
+    def predict_leaves(self, X, out=None, stream=None):
+        return tree_ens_predict_leaves(self.handle, X, out, stream)
+
+    def info(self) -> dict:
+        return tree_ens_info(self.handle)
+
+    def close(self) -> None:
+        if self._h is not None:
+            tree_ens_destroy(self._h)
+            self._h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

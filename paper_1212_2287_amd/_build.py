@@ -1,0 +1,47 @@
+"""Build of the HIP library ``libtreeens.so`` (gfx950), in-tree next to this file."""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG, "libtreeens.so")
+
+# Device code: gfx950 only, IEEE single-precision denormals kept (the strict tie rule stores
+# the float after 0.0, a subnormal), packed-fp32 instructions disabled.
+HIP_FLAGS = [
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+    "-fno-gpu-flush-denormals-to-zero",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-command-line-argument",
+]
+
+
+def _hipcc() -> str:
+    for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found; the gfx950 library cannot be built")
+
+
+def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
+    """Compile the packer (host C++) and the kernels + C ABI (HIP) into one shared library."""
+    tmp = out + ".tmp"
+    obj = out + ".pack.o"
+    run = (lambda c: subprocess.run(c, check=True)) if verbose else \
+        (lambda c: subprocess.run(c, check=True, stdout=subprocess.DEVNULL))
+    run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", "-c",
+         os.path.join(CSRC, "pack.cpp"), "-o", obj])
+    run([_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC, "-shared",
+         os.path.join(CSRC, "tree_ens.hip"), "-x", "none", obj, "-o", tmp])
+    os.replace(tmp, out)
+    os.remove(obj)
+    return out
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

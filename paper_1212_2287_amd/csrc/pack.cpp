@@ -1,0 +1,262 @@
+// pack.cpp -- validation, breadth-first re-layout and LDS tile planning (host only).
+#include "pack.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+
+namespace treeens {
+
+namespace {
+
+uint32_t float_bits(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, sizeof u);
+    return u;
+}
+
+// Under the strict rule (right iff x > theta) store the next float above theta: no float lies
+// strictly between theta and its successor, so x > theta <=> x >= successor for every non-NaN
+// x. +inf has no successor; x > +inf never holds, which a NaN threshold reproduces under >=.
+float strict_to_inclusive(float theta) {
+    if (std::isinf(theta) && theta > 0)
+        return std::nanf("");
+    return std::nextafter(theta, INFINITY);
+}
+
+LdsPlan plan_lds(int32_t n_cols) {
+    LdsPlan p{};
+    const int64_t cols = int64_t(n_cols) + 1; // + the NaN column the leaves read
+    for (int dl = 64; dl >= 8; dl /= 2) {
+        if (cols * dl * 4 <= kXsMaxBytes) {
+            p.docs_per_block = dl;
+            break;
+        }
+    }
+    if (p.docs_per_block == 0)
+        return p;
+    p.xs_bytes = int32_t(cols * p.docs_per_block * 4);
+    const int reserve = 64; // the all-zero record used by padding walkers, plus slack
+    if (p.xs_bytes <= kTwoWgXsBytes) {
+        p.lds_bytes = kLdsPerCu / 2;
+        p.wg_threads = 512;
+    } else {
+        p.lds_bytes = kLdsPerCu;
+        p.wg_threads = 1024;
+    }
+    p.tile_bytes = (p.lds_bytes - p.xs_bytes - reserve) & ~15;
+    return p;
+}
+
+} // namespace
+
+int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+               const float *threshold, const int32_t *left, const int32_t *right,
+               const float *value, uint32_t flags, Packed &out, std::string &err) {
+    if (n_trees < 0) {
+        err = "n_trees must be >= 0";
+        return kErrArg;
+    }
+    if ((flags & ~1u) != 0) {
+        err = "unknown flag bits";
+        return kErrArg;
+    }
+    const bool strict = (flags & 1u) != 0;
+    if (n_trees > 0 && !tree_offsets) {
+        err = "tree_offsets is NULL";
+        return kErrArg;
+    }
+    if (n_trees > 0 && tree_offsets[0] != 0) {
+        err = "tree_offsets[0] must be 0";
+        return kErrModel;
+    }
+    int64_t n_nodes = n_trees > 0 ? tree_offsets[n_trees] : 0;
+    for (int32_t t = 0; t < n_trees; t++) {
+        if (tree_offsets[t + 1] - tree_offsets[t] < 1) {
+            err = "tree " + std::to_string(t) + " has no node (tree_offsets must increase)";
+            return kErrModel;
+        }
+    }
+    if (n_nodes > 0 && (!feature || !threshold || !left || !right || !value)) {
+        err = "a node array is NULL";
+        return kErrArg;
+    }
+    if (n_nodes >= (int64_t(1) << 32)) {
+        err = "more than 2^32 nodes";
+        return kErrModel;
+    }
+
+    // ---- pass 1: per-tree validation, depth, largest feature id ------------------------
+    int32_t max_fid = -1;
+    std::vector<int32_t> depth_of(size_t(n_trees), 0);
+    std::vector<int32_t> parents, level, order;
+    for (int32_t t = 0; t < n_trees; t++) {
+        const int64_t a = tree_offsets[t];
+        const int64_t n = tree_offsets[t + 1] - a;
+        const std::string where = "tree " + std::to_string(t) + ": ";
+        if (n > 65536) {
+            err = where + "more than 65536 nodes";
+            return kErrModel;
+        }
+        parents.assign(size_t(n), 0);
+        for (int64_t i = 0; i < n; i++) {
+            const int32_t f = feature[a + i];
+            if (f < -1) {
+                err = where + "node " + std::to_string(i) + " has feature id " + std::to_string(f);
+                return kErrModel;
+            }
+            if (f < 0)
+                continue;
+            if (std::isnan(threshold[a + i])) {
+                err = where + "node " + std::to_string(i) + " has a NaN threshold";
+                return kErrModel;
+            }
+            const int32_t l = left[a + i], r = right[a + i];
+            if (l <= 0 || l >= n || r <= 0 || r >= n) {
+                err = where + "node " + std::to_string(i) +
+                      " has a child id out of range or naming the root";
+                return kErrModel;
+            }
+            if (l == r) {
+                err = where + "node " + std::to_string(i) + " has the same left and right child";
+                return kErrModel;
+            }
+            parents[size_t(l)]++;
+            parents[size_t(r)]++;
+            max_fid = std::max(max_fid, f);
+        }
+        for (int64_t i = 1; i < n; i++) {
+            if (parents[size_t(i)] != 1) {
+                err = where + "node " + std::to_string(i) +
+                      (parents[size_t(i)] == 0 ? " is unreachable (no parent)" : " has two parents");
+                return kErrModel;
+            }
+        }
+        // breadth-first from the root: with one parent per non-root node, every node is reached
+        // exactly once unless part of the tree hangs in a cycle away from the root
+        level.assign(size_t(n), 0);
+        order.clear();
+        order.push_back(0);
+        int32_t dmax = 0;
+        for (size_t q = 0; q < order.size(); q++) {
+            const int32_t i = order[q];
+            if (feature[a + i] >= 0) {
+                for (int32_t c : {left[a + i], right[a + i]}) {
+                    level[size_t(c)] = level[size_t(i)] + 1;
+                    dmax = std::max(dmax, level[size_t(c)]);
+                    order.push_back(c);
+                }
+            }
+            if (int64_t(order.size()) > n)
+                break;
+        }
+        if (int64_t(order.size()) != n) {
+            err = where + "some nodes are not reachable from the root (a cycle)";
+            return kErrModel;
+        }
+        depth_of[size_t(t)] = dmax;
+    }
+
+    const int32_t n_cols = max_fid + 1;
+    LdsPlan plan = plan_lds(n_cols);
+    if (plan.docs_per_block == 0) {
+        err = "feature id " + std::to_string(max_fid) + " is beyond the LDS document-tile limit (" +
+              std::to_string(kXsMaxBytes / (8 * 4) - 2) + ")";
+        return kErrModel;
+    }
+    const int64_t max_nodes_per_tree = plan.tile_bytes / int64_t(sizeof(NodeRec));
+    for (int32_t t = 0; t < n_trees; t++) {
+        const int64_t n = tree_offsets[t + 1] - tree_offsets[t];
+        if (n > max_nodes_per_tree) {
+            err = "tree " + std::to_string(t) + " has " + std::to_string(n) +
+                  " nodes; one LDS tile holds at most " + std::to_string(max_nodes_per_tree) +
+                  " at this feature count";
+            return kErrModel;
+        }
+    }
+
+    // ---- pass 2: order trees by depth (deepest first), re-lay each out breadth-first --------
+    Packed p;
+    p.n_trees = n_trees;
+    p.n_cols = n_cols;
+    p.plan = plan;
+    p.tree_orig.resize(size_t(n_trees));
+    std::iota(p.tree_orig.begin(), p.tree_orig.end(), 0);
+    std::stable_sort(p.tree_orig.begin(), p.tree_orig.end(),
+                     [&](int32_t x, int32_t y) { return depth_of[size_t(x)] > depth_of[size_t(y)]; });
+    p.nodes.reserve(size_t(n_nodes));
+    p.orig_id.reserve(size_t(n_nodes));
+    p.tree_node_off.resize(size_t(n_trees) + 1, 0);
+    p.tree_depth.resize(size_t(n_trees), 0);
+    std::vector<int32_t> new_id;
+    for (int32_t pt = 0; pt < n_trees; pt++) {
+        const int32_t t = p.tree_orig[size_t(pt)];
+        const int64_t a = tree_offsets[t];
+        const int64_t n = tree_offsets[t + 1] - a;
+        // breadth-first numbering in which the two children of a node take adjacent slots
+        order.clear();
+        order.push_back(0);
+        new_id.assign(size_t(n), -1);
+        new_id[0] = 0;
+        int32_t next = 1;
+        for (size_t q = 0; q < order.size(); q++) {
+            const int32_t i = order[q];
+            if (feature[a + i] >= 0) {
+                new_id[size_t(left[a + i])] = next;
+                new_id[size_t(right[a + i])] = next + 1;
+                next += 2;
+                order.push_back(left[a + i]);
+                order.push_back(right[a + i]);
+            }
+        }
+        const size_t base = p.nodes.size();
+        p.tree_node_off[size_t(pt)] = uint32_t(base);
+        p.nodes.resize(base + size_t(n));
+        p.orig_id.resize(base + size_t(n));
+        for (int64_t i = 0; i < n; i++) {
+            const int32_t ni = new_id[size_t(i)];
+            NodeRec &r = p.nodes[base + size_t(ni)];
+            p.orig_id[base + size_t(ni)] = int32_t(i);
+            if (feature[a + i] >= 0) {
+                const float th = strict ? strict_to_inclusive(threshold[a + i]) : threshold[a + i];
+                r.thr_bits = float_bits(th);
+                r.w = (uint32_t(new_id[size_t(left[a + i])]) << 16) | uint32_t(feature[a + i] + 1);
+            } else {
+                r.thr_bits = float_bits(value[a + i]);
+                r.w = uint32_t(ni) << 16;
+            }
+        }
+        p.tree_depth[size_t(pt)] = uint32_t(depth_of[size_t(t)]);
+        p.max_depth = std::max(p.max_depth, depth_of[size_t(t)]);
+    }
+    p.tree_node_off[size_t(n_trees)] = uint32_t(p.nodes.size());
+
+    // ---- pass 3: tilings at budget / 2^k -------------------------------------------------
+    for (int k = 0; k < kTileLevels; k++) {
+        p.level_begin[k] = int32_t(p.tiles.size());
+        const int64_t budget = std::max<int64_t>(plan.tile_bytes >> k, 1);
+        int32_t tb = 0;
+        while (tb < n_trees) {
+            int32_t te = tb;
+            int64_t bytes = 0;
+            int32_t dmax = 0;
+            while (te < n_trees) {
+                const int64_t tbytes =
+                    int64_t(p.tree_node_off[size_t(te) + 1] - p.tree_node_off[size_t(te)]) * 8;
+                if (te > tb && bytes + tbytes > budget)
+                    break;
+                bytes += tbytes;
+                dmax = std::max(dmax, int32_t(p.tree_depth[size_t(te)]));
+                te++;
+            }
+            p.tiles.push_back(Tile{tb, te, dmax, int32_t(p.tree_node_off[size_t(tb)])});
+            tb = te;
+        }
+    }
+    p.level_begin[kTileLevels] = int32_t(p.tiles.size());
+    out = std::move(p);
+    return kOk;
+}
+
+} // namespace treeens

@@ -1,0 +1,75 @@
+// pack.hpp -- host-side model packer for the gfx950 tree-ensemble scorer.
+//
+// Turns the caller's flat creation-order arrays into the device layout the kernels walk:
+// one 8-byte record per node, trees re-laid out breadth-first with the two children of a node
+// in adjacent slots (the contiguous Struct+ layout of Section 3, which keeps explicit child
+// links so unbalanced trees pack without empty slots), trees ordered by depth, and a plan of
+// LDS tiles (runs of whole trees that fit the per-workgroup LDS budget).
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace treeens {
+
+// One node record, 8 bytes, as the kernels read it from LDS with one 64-bit load.
+//   internal node: thr = threshold (nudged to the next float up under the strict rule),
+//                  w   = (left child local index << 16) | (feature id + 1)
+//   leaf:          thr = leaf value,
+//                  w   = (own local index << 16) | 0
+// Column 0 of a staged document tile holds NaN for every document, so a leaf compares a NaN
+// with its value, gets "left" and its child index is itself: leaves absorb any further steps.
+// The right child of an internal node is at left + 1.
+struct NodeRec {
+    uint32_t thr_bits;
+    uint32_t w;
+};
+static_assert(sizeof(NodeRec) == 8, "node record must be 8 bytes");
+
+// A run of whole trees [tree_begin, tree_end) (packed order) staged into LDS together.
+struct Tile {
+    int32_t tree_begin;
+    int32_t tree_end;
+    int32_t max_depth;  // deepest tree in the run: the walk's trip count
+    int32_t node_begin; // packed node offset of tree_begin
+};
+
+// Launch plan fixed at create time from the model's feature range.
+struct LdsPlan {
+    int32_t docs_per_block; // documents a workgroup stages (power of two, 8..64)
+    int32_t xs_bytes;       // staged document tile: (n_cols + 1) columns x docs_per_block floats
+    int32_t tile_bytes;     // LDS bytes for node records of one tile
+    int32_t wg_threads;     // workgroup size
+    int32_t lds_bytes;      // total dynamic LDS per workgroup
+};
+
+constexpr int kLdsPerCu = 160 * 1024;  // gfx950 LDS per compute unit
+constexpr int kXsMaxBytes = 96 * 1024; // cap on the staged document tile
+constexpr int kTwoWgXsBytes = 40 * 1024; // tiles up to this size leave room for 2 workgroups/CU
+constexpr int kTileLevels = 5;         // tilings at budget, budget/2, ..., budget/16
+
+struct Packed {
+    int32_t n_trees = 0;
+    int32_t n_cols = 0;    // 1 + largest feature id read (0 if none)
+    int32_t max_depth = 0; // over all trees
+    LdsPlan plan{};
+    std::vector<NodeRec> nodes;          // all trees, packed order
+    std::vector<uint32_t> tree_node_off; // [n_trees + 1] packed node offset of each tree
+    std::vector<uint32_t> tree_depth;    // [n_trees]
+    std::vector<int32_t> tree_orig;      // [n_trees] input index of packed tree t
+    std::vector<int32_t> orig_id;        // [n_nodes] input tree-local id of packed node
+    std::vector<Tile> tiles;             // all tiling levels, concatenated
+    int32_t level_begin[kTileLevels + 1] = {};
+};
+
+// Status codes match the public header.
+constexpr int kOk = 0, kErrArg = -1, kErrModel = -2;
+
+// Validate and pack. Returns kOk or an error code with a message in `err`. Pure host code:
+// no HIP call is made, so every model error is reported without a device.
+int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+               const float *threshold, const int32_t *left, const int32_t *right,
+               const float *value, uint32_t flags, Packed &out, std::string &err);
+
+} // namespace treeens

@@ -1,0 +1,468 @@
+// tree_ens.hip -- gfx950 kernels and the C ABI of the tree-ensemble scorer.
+//
+// Work decomposition (one kernel launch per predict call):
+//   * a workgroup owns a block of DL consecutive documents and stages their features into LDS
+//     once, feature-major ([column][DL] floats, column 0 = NaN, column f+1 = feature f), so a
+//     lane's read of any feature of its own document is a conflict-free LDS access whatever
+//     feature the lane's current node names;
+//   * the trees are streamed through LDS in tiles (runs of whole trees, packed node records);
+//   * lanes are documents; each group of DL lanes (a "walker") walks one tree at a time for its
+//     DL documents, and each lane interleaves K independent trees so that their LDS latencies
+//     overlap (the vectorisation idea of Section 3, VPred, moved from instances to trees);
+//   * each step is the branch-free predicated update of Section 3 (Pred) over explicit,
+//     sibling-adjacent children: idx = left(idx) + (x[fid(idx)] >= theta(idx));
+//   * leaf values are summed per lane in double precision, then reduced across walkers through
+//     LDS in a fixed order and rounded once to float.
+// Small batches split the tiles over a second grid dimension and reduce the per-split partial
+// sums in a second, tiny kernel (fixed order, so results are deterministic).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "pack.hpp"
+#include "tree_ens.h"
+
+#ifndef TREE_ENS_K
+#define TREE_ENS_K 2 // trees interleaved per lane
+#endif
+
+using treeens::NodeRec;
+using treeens::Packed;
+using treeens::Tile;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string &msg) {
+    g_err = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(TREE_ENS_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+constexpr int kNumCus = 256;
+
+// ------------------------------------------------------------------------------------------
+// kernels
+// ------------------------------------------------------------------------------------------
+template <int DL, int K, bool LEAVES>
+__global__ void __launch_bounds__(1024)
+score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
+             const uint2 *__restrict__ nodes, const uint32_t *__restrict__ tree_node_off,
+             const uint32_t *__restrict__ tree_depth, const Tile *__restrict__ tiles,
+             int32_t n_tiles, int32_t n_splits, int32_t xs_bytes, int32_t tile_bytes,
+             double *__restrict__ partials, float *__restrict__ scores,
+             int32_t *__restrict__ leaf_ids, const int32_t *__restrict__ orig_id,
+             const int32_t *__restrict__ tree_orig, int32_t n_trees) {
+    extern __shared__ __align__(16) unsigned char lds[];
+    float *xs = reinterpret_cast<float *>(lds);
+    uint2 *tn = reinterpret_cast<uint2 *>(lds + xs_bytes);
+    const uint32_t zero_rec = uint32_t(xs_bytes + tile_bytes);
+
+    const int tid = threadIdx.x;
+    const int nthr = blockDim.x;
+    const int dl = tid & (DL - 1);
+    const int walker = tid / DL;
+    const int n_walkers = nthr / DL;
+    const int64_t doc0 = int64_t(blockIdx.x) * DL;
+    const int split = blockIdx.y;
+    const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
+    const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
+
+    // stage the document tile: one column per DL consecutive lanes, lane = document
+    const int n_elem = (n_cols + 1) * DL;
+    for (int e = tid; e < n_elem; e += nthr) {
+        const int c = e / DL;
+        const int d = e & (DL - 1);
+        float v = __builtin_nanf("");
+        if (c > 0) {
+            const int64_t doc = doc0 + d;
+            v = doc < n_docs ? X[doc * n_features + (c - 1)] : 0.0f;
+        }
+        xs[e] = v;
+    }
+    if (tid == 0)
+        *reinterpret_cast<uint2 *>(lds + zero_rec) = make_uint2(0u, 0u);
+
+    double acc = 0.0;
+    for (int ti = t_lo; ti < t_hi; ++ti) {
+        const Tile tl = tiles[ti];
+        const int n_rec = int(tree_node_off[tl.tree_end]) - tl.node_begin;
+        __syncthreads(); // previous tile fully consumed (and the document tile written)
+        const uint2 *src = nodes + tl.node_begin;
+        for (int i = tid; i < n_rec; i += nthr)
+            tn[i] = src[i];
+        __syncthreads();
+        const int ntr = tl.tree_end - tl.tree_begin;
+        for (int g = walker * K; g < ntr; g += n_walkers * K) {
+            uint32_t base[K], idx[K];
+            int dmax = 0;
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                idx[i] = 0;
+                if (g + i < ntr) {
+                    const int gt = tl.tree_begin + g + i;
+                    base[i] = uint32_t(xs_bytes) + (tree_node_off[gt] - uint32_t(tl.node_begin)) * 8u;
+                    dmax = max(dmax, int(tree_depth[gt]));
+                } else {
+                    base[i] = zero_rec;
+                }
+            }
+            for (int s = 0; s < dmax; ++s) {
+#pragma unroll
+                for (int i = 0; i < K; ++i) {
+                    const uint2 nd = *reinterpret_cast<const uint2 *>(lds + base[i] + idx[i] * 8u);
+                    const float x = xs[(nd.y & 0xffffu) * DL + dl];
+                    idx[i] = (nd.y >> 16) + (x >= __uint_as_float(nd.x) ? 1u : 0u);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                if constexpr (LEAVES) {
+                    const int64_t doc = doc0 + dl;
+                    if (g + i < ntr && doc < n_docs) {
+                        const int gt = tl.tree_begin + g + i;
+                        leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + idx[i]];
+                    }
+                } else {
+                    const float v = __uint_as_float(
+                        *reinterpret_cast<const uint32_t *>(lds + base[i] + idx[i] * 8u));
+                    acc += double(v);
+                }
+            }
+        }
+    }
+    if constexpr (!LEAVES) {
+        __syncthreads();
+        double *red = reinterpret_cast<double *>(lds + xs_bytes);
+        red[walker * DL + dl] = acc;
+        __syncthreads();
+        if (walker == 0) {
+            double s = 0.0;
+            for (int w = 0; w < n_walkers; ++w)
+                s += red[w * DL + dl];
+            const int64_t doc = doc0 + dl;
+            if (doc < n_docs) {
+                if (n_splits == 1)
+                    scores[doc] = float(s);
+                else
+                    partials[int64_t(split) * n_docs + doc] = s;
+            }
+        }
+    }
+}
+
+__global__ void reduce_partials_kernel(const double *__restrict__ partials, int32_t n_splits,
+                                       int64_t n_docs, float *__restrict__ scores) {
+    const int64_t d = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (d < n_docs) {
+        double s = 0.0;
+        for (int k = 0; k < n_splits; ++k)
+            s += partials[int64_t(k) * n_docs + d];
+        scores[d] = float(s);
+    }
+}
+
+__global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
+    const int64_t d = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (d < n)
+        scores[d] = 0.0f;
+}
+
+using ScoreFn = void (*)(const float *, int64_t, int32_t, int32_t, const uint2 *, const uint32_t *,
+                         const uint32_t *, const Tile *, int32_t, int32_t, int32_t, int32_t,
+                         double *, float *, int32_t *, const int32_t *, const int32_t *, int32_t);
+
+template <bool LEAVES>
+ScoreFn pick_kernel(int dl) {
+    constexpr int K = TREE_ENS_K;
+    switch (dl) {
+    case 64: return score_kernel<64, K, LEAVES>;
+    case 32: return score_kernel<32, K, LEAVES>;
+    case 16: return score_kernel<16, K, LEAVES>;
+    case 8: return score_kernel<8, K, LEAVES>;
+    default: return nullptr;
+    }
+}
+
+} // namespace
+
+// ------------------------------------------------------------------------------------------
+// handle
+// ------------------------------------------------------------------------------------------
+struct tree_ens {
+    int device = 0;
+    int32_t n_trees = 0;
+    int32_t n_cols = 0;
+    int32_t max_depth = 0;
+    int64_t n_nodes = 0;
+    treeens::LdsPlan plan{};
+    int32_t level_begin[treeens::kTileLevels + 1] = {};
+    uint2 *d_nodes = nullptr;
+    uint32_t *d_tree_node_off = nullptr;
+    uint32_t *d_tree_depth = nullptr;
+    int32_t *d_tree_orig = nullptr;
+    int32_t *d_orig_id = nullptr;
+    Tile *d_tiles = nullptr;
+};
+
+namespace {
+
+void free_device(tree_ens *h) {
+    (void)hipFree(h->d_nodes);
+    (void)hipFree(h->d_tree_node_off);
+    (void)hipFree(h->d_tree_depth);
+    (void)hipFree(h->d_tree_orig);
+    (void)hipFree(h->d_orig_id);
+    (void)hipFree(h->d_tiles);
+}
+
+template <typename T>
+hipError_t upload(T **dst, const std::vector<T> &src) {
+    const size_t bytes = std::max<size_t>(src.size() * sizeof(T), sizeof(T));
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(dst), bytes);
+    if (e != hipSuccess)
+        return e;
+    if (!src.empty())
+        e = hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+    return e;
+}
+
+// Split count and tiling level for a batch of n_blocks document blocks: enough workgroups to
+// fill every compute unit twice over, without cutting tiles finer than the finest level.
+void choose_split(const tree_ens *h, int64_t n_blocks, int *level, int *splits) {
+    const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
+    const int64_t target = int64_t(kNumCus) * wg_per_cu * 2;
+    *level = 0;
+    *splits = 1;
+    if (n_blocks >= target)
+        return;
+    const int64_t want = (target + n_blocks - 1) / n_blocks;
+    for (int k = 0; k < treeens::kTileLevels; ++k) {
+        const int nt = h->level_begin[k + 1] - h->level_begin[k];
+        *level = k;
+        *splits = int(std::min<int64_t>(want, nt));
+        if (nt >= want)
+            break;
+    }
+    if (*splits < 1)
+        *splits = 1;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    hipError_t err = hipSuccess;
+    explicit DeviceGuard(int dev) {
+        err = hipGetDevice(&prev);
+        if (err == hipSuccess && prev != dev)
+            err = hipSetDevice(dev);
+        else
+            prev = -1;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0)
+            (void)hipSetDevice(prev);
+    }
+};
+
+int check_predict_args(const tree_ens *h, const float *X, int64_t n_docs, int32_t n_features,
+                       const void *out) {
+    if (!h)
+        return fail(TREE_ENS_E_ARG, "handle is NULL");
+    if (n_docs < 0)
+        return fail(TREE_ENS_E_ARG, "n_docs must be >= 0");
+    if (n_docs == 0)
+        return TREE_ENS_OK;
+    if (!X || !out)
+        return fail(TREE_ENS_E_ARG, "X or the output pointer is NULL");
+    if ((reinterpret_cast<uintptr_t>(X) & 3u) != 0 || (reinterpret_cast<uintptr_t>(out) & 3u) != 0)
+        return fail(TREE_ENS_E_ARG, "X and the output must be 4-byte aligned");
+    if (n_features < h->n_cols)
+        return fail(TREE_ENS_E_SHAPE, "documents carry " + std::to_string(n_features) +
+                                          " features; the model reads feature " +
+                                          std::to_string(h->n_cols - 1));
+    if (n_features < 1)
+        return fail(TREE_ENS_E_SHAPE, "n_features must be >= 1");
+    return TREE_ENS_OK;
+}
+
+template <bool LEAVES>
+int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_t n_docs,
+                   int32_t n_features, float *scores, int32_t *leaf_ids) {
+    const int dl = h->plan.docs_per_block;
+    const int64_t n_blocks = (n_docs + dl - 1) / dl;
+    if (n_blocks > 0x7fffffff)
+        return fail(TREE_ENS_E_ARG, "too many documents for one launch");
+    int level, splits;
+    choose_split(h, n_blocks, &level, &splits);
+    ScoreFn fn = pick_kernel<LEAVES>(dl);
+    if (!fn)
+        return fail(TREE_ENS_E_ARG, "unsupported document block size");
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, h->plan.lds_bytes);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipFuncSetAttribute");
+    double *partials = nullptr;
+    if (!LEAVES && splits > 1) {
+        e = hipMallocAsync(reinterpret_cast<void **>(&partials),
+                           size_t(splits) * size_t(n_docs) * sizeof(double), stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipMallocAsync(partials)");
+    }
+    const Tile *tiles = h->d_tiles + h->level_begin[level];
+    const int n_tiles = h->level_begin[level + 1] - h->level_begin[level];
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(fn, dim3(unsigned(n_blocks), unsigned(splits)), dim3(h->plan.wg_threads),
+                       h->plan.lds_bytes, stream, X, n_docs, n_features, h->n_cols, h->d_nodes,
+                       h->d_tree_node_off, h->d_tree_depth, tiles, n_tiles, splits,
+                       h->plan.xs_bytes, h->plan.tile_bytes, partials, scores, leaf_ids,
+                       h->d_orig_id, h->d_tree_orig, h->n_trees);
+    e = hipGetLastError();
+    if (e == hipSuccess && partials) {
+        const int bs = 256;
+        hipLaunchKernelGGL(reduce_partials_kernel, dim3(unsigned((n_docs + bs - 1) / bs)), dim3(bs),
+                           0, stream, partials, splits, n_docs, scores);
+        e = hipGetLastError();
+    }
+    if (partials) {
+        hipError_t e2 = hipFreeAsync(partials, stream);
+        if (e == hipSuccess)
+            e = e2;
+    }
+    if (e != hipSuccess)
+        return hip_fail(e, "kernel launch");
+    return TREE_ENS_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offsets,
+                    const int32_t *feature, const float *threshold, const int32_t *left,
+                    const int32_t *right, const float *value, uint32_t flags) {
+    g_err.clear();
+    if (!out)
+        return fail(TREE_ENS_E_ARG, "out is NULL");
+    *out = nullptr;
+    Packed p;
+    std::string err;
+    int rc;
+    try {
+        rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value, flags,
+                                 p, err);
+    } catch (const std::bad_alloc &) {
+        return fail(TREE_ENS_E_NOMEM, "host allocation failed while packing");
+    }
+    if (rc != treeens::kOk)
+        return fail(rc, err);
+
+    tree_ens *h = new (std::nothrow) tree_ens();
+    if (!h)
+        return fail(TREE_ENS_E_NOMEM, "host allocation failed");
+    h->n_trees = p.n_trees;
+    h->n_cols = p.n_cols;
+    h->max_depth = p.max_depth;
+    h->n_nodes = int64_t(p.nodes.size());
+    h->plan = p.plan;
+    std::memcpy(h->level_begin, p.level_begin, sizeof h->level_begin);
+    hipError_t e = hipGetDevice(&h->device);
+    std::vector<uint2> nodes(p.nodes.size());
+    if (!p.nodes.empty())
+        std::memcpy(nodes.data(), p.nodes.data(), p.nodes.size() * sizeof(NodeRec));
+    if (e == hipSuccess)
+        e = upload(&h->d_nodes, nodes);
+    if (e == hipSuccess)
+        e = upload(&h->d_tree_node_off, p.tree_node_off);
+    if (e == hipSuccess)
+        e = upload(&h->d_tree_depth, p.tree_depth);
+    if (e == hipSuccess)
+        e = upload(&h->d_tree_orig, p.tree_orig);
+    if (e == hipSuccess)
+        e = upload(&h->d_orig_id, p.orig_id);
+    if (e == hipSuccess)
+        e = upload(&h->d_tiles, p.tiles);
+    if (e != hipSuccess) {
+        free_device(h);
+        delete h;
+        return fail(e == hipErrorOutOfMemory ? TREE_ENS_E_NOMEM : TREE_ENS_E_DEVICE,
+                    std::string("device upload failed: ") + hipGetErrorString(e));
+    }
+    *out = h;
+    return TREE_ENS_OK;
+}
+
+int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                     int32_t n_features, float *scores) {
+    g_err.clear();
+    int rc = check_predict_args(h, X, n_docs, n_features, scores);
+    if (rc != TREE_ENS_OK || n_docs == 0)
+        return rc;
+    DeviceGuard g(h->device);
+    if (g.err != hipSuccess)
+        return hip_fail(g.err, "hipSetDevice");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (h->n_trees == 0) {
+        const int bs = 256;
+        hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n_docs + bs - 1) / bs)), dim3(bs), 0, s,
+                           scores, n_docs);
+        hipError_t e = hipGetLastError();
+        return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "kernel launch");
+    }
+    return launch_predict<false>(h, s, X, n_docs, n_features, scores, nullptr);
+}
+
+int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                            int32_t n_features, int32_t *leaf_ids) {
+    g_err.clear();
+    int rc = check_predict_args(h, X, n_docs, n_features, leaf_ids);
+    if (rc != TREE_ENS_OK || n_docs == 0 || h->n_trees == 0)
+        return rc;
+    DeviceGuard g(h->device);
+    if (g.err != hipSuccess)
+        return hip_fail(g.err, "hipSetDevice");
+    return launch_predict<true>(h, reinterpret_cast<hipStream_t>(stream), X, n_docs, n_features,
+                                nullptr, leaf_ids);
+}
+
+int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features, int32_t *max_depth,
+                  int64_t *packed_bytes, int32_t *n_tiles, int32_t *docs_per_block) {
+    g_err.clear();
+    if (!h)
+        return fail(TREE_ENS_E_ARG, "handle is NULL");
+    if (n_trees)
+        *n_trees = h->n_trees;
+    if (min_features)
+        *min_features = h->n_cols;
+    if (max_depth)
+        *max_depth = h->max_depth;
+    if (packed_bytes)
+        *packed_bytes = h->n_nodes * int64_t(sizeof(NodeRec));
+    if (n_tiles)
+        *n_tiles = h->level_begin[1] - h->level_begin[0];
+    if (docs_per_block)
+        *docs_per_block = h->plan.docs_per_block;
+    return TREE_ENS_OK;
+}
+
+void tree_ens_destroy(tree_ens_t *h) {
+    if (!h)
+        return;
+    DeviceGuard g(h->device);
+    free_device(h);
+    delete h;
+}
+
+const char *tree_ens_last_error(void) { return g_err.c_str(); }
+
+} // extern "C"

@@ -1,0 +1,146 @@
+"""GPU edge cases and properties through the C ABI: batch sizes around the block size, empty
+and single-leaf ensembles, IEEE corner values, both tie rules, slices, determinism, errors."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from _golden import load_hand_ensemble
+from _gpu import assert_leaves_equal, assert_scores_close, dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def T():
+    import paper_1212_2287_amd as T
+    T.load_library()
+    return T
+
+
+def _gpu(T, ens, X, flags=0, leaves=True):
+    import torch
+    with T.TreeEnsemble.from_ensemble(ens, flags) as m:
+        Xd = dev(X)
+        s = m.predict(Xd)
+        ids = m.predict_leaves(Xd) if leaves else None
+        torch.cuda.synchronize()
+        return s.cpu().numpy(), None if ids is None else ids.cpu().numpy()
+
+
+@pytest.mark.parametrize("rule,name", [(0, "ge"), (1, "gt")])
+def test_hand_golden_on_gpu(T, rule, name):
+    ens, X, expects = load_hand_ensemble()
+    s, ids = _gpu(T, ens, X, flags=rule)
+    exp = np.array([e[1] for e in expects[name]], dtype=np.float32)
+    exp_ids = np.array([e[3] for e in expects[name]], dtype=np.int32)
+    assert np.array_equal(s, exp), (s, exp)
+    assert np.array_equal(ids, exp_ids)
+
+
+@pytest.mark.parametrize("n_docs", [1, 7, 63, 64, 65, 127, 4097])
+def test_batch_sizes(T, n_docs):
+    cfg = W.CONFIGS[2]
+    ens = W.make_ensemble(cfg, n_trees=300)
+    X = W.make_docs(cfg, n_docs=n_docs)
+    s, ids = _gpu(T, ens, X)
+    ref, ref_ids, _ = oracle.score(ens, X)
+    assert_scores_close(s, ref, f"{n_docs} docs")
+    assert_leaves_equal(ids, ref_ids, f"{n_docs} docs")
+
+
+def test_zero_docs_and_empty_model(T):
+    import torch
+    ens = W.make_ensemble(W.CONFIGS[1])
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        out = m.predict(torch.empty((0, 136), dtype=torch.float32, device="cuda"))
+        assert out.shape == (0,)
+    empty = W.Ensemble(np.zeros(1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.float32),
+                       np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32), 4)
+    with T.TreeEnsemble.from_ensemble(empty) as m:
+        s = m.predict(dev(np.ones((70, 4), np.float32)))
+        torch.cuda.synchronize()
+        assert np.array_equal(s.cpu().numpy(), np.zeros(70, np.float32))
+        assert m.info()["n_trees"] == 0
+
+
+@pytest.mark.parametrize("rule", [0, 1])
+def test_random_small_ensembles_with_corner_values(T, rule):
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 1.0, np.inf, -np.inf, 1e-45, -1e-45, 3e-39], np.float32)
+    for seed in range(6):
+        ens = W.random_ensemble(seed, n_trees=37, n_features=11, min_leaves=1, max_leaves=24,
+                                thr_values=pool if seed % 2 else None)
+        X = W.random_docs(seed, 300, 11, values=np.concatenate([pool, [np.nan]]).astype(np.float32)
+                          if seed % 2 else None)
+        s, ids = _gpu(T, ens, X, flags=rule)
+        ref, ref_ids, _ = oracle.score(ens, X, rule=rule)
+        assert_leaves_equal(ids, ref_ids, f"seed {seed}")
+        assert_scores_close(s, ref, f"seed {seed}")
+
+
+def test_single_leaf_trees_and_last_feature(T):
+    # depth-0 trees add a constant; a split on the last feature column is read correctly
+    F = 9
+    ens = W.random_ensemble(11, n_trees=50, n_features=F, min_leaves=1, max_leaves=3)
+    fe = ens.feature.copy()
+    fe[fe >= 0] = F - 1
+    ens = W.Ensemble(ens.tree_offsets, fe, ens.threshold, ens.left, ens.right, ens.value, F)
+    X = W.random_docs(12, 500, F)
+    s, ids = _gpu(T, ens, X)
+    ref, ref_ids, _ = oracle.score(ens, X)
+    assert_leaves_equal(ids, ref_ids)
+    assert_scores_close(s, ref)
+
+
+def test_wider_rows_and_slices(T):
+    import torch
+    cfg = W.CONFIGS[2]
+    ens = W.make_ensemble(cfg, n_trees=200)
+    X = W.make_docs(cfg, n_docs=3000)
+    wide = np.concatenate([X, np.full((3000, 21), np.nan, np.float32)], axis=1)  # unused columns
+    ref, ref_ids, _ = oracle.score(ens, X)
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        Wd = dev(wide)
+        s = m.predict(Wd)
+        big = dev(X)
+        part = big[1000:2500]  # a doc-offset slice of a larger tensor
+        s2 = m.predict(part)
+        torch.cuda.synchronize()
+        assert_scores_close(s.cpu().numpy(), ref)
+        assert_scores_close(s2.cpu().numpy(), ref[1000:2500])
+
+
+def test_deterministic(T):
+    import torch
+    cfg = W.CONFIGS[3]
+    ens = W.make_ensemble(cfg, n_trees=500)
+    X = dev(W.make_docs(cfg, n_docs=20000))
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        a = m.predict(X).cpu().numpy()
+        b = m.predict(X).cpu().numpy()
+        c = m.predict(X[:100].contiguous()).cpu().numpy()  # split path
+        d = m.predict(X[:100].contiguous()).cpu().numpy()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert np.array_equal(c.view(np.uint32), d.view(np.uint32))
+
+
+def test_streams_and_errors(T):
+    import torch
+    ens = W.make_ensemble(W.CONFIGS[1])
+    X = W.make_docs(W.CONFIGS[1], n_docs=500)
+    ref, _, _ = oracle.score(ens, X)
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        st = torch.cuda.Stream()
+        Xd = dev(X)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(st):
+            s = m.predict(Xd)
+        st.synchronize()
+        assert_scores_close(s.cpu().numpy(), ref)
+        with pytest.raises(T.TreeEnsError) as ei:
+            m.predict(Xd[:, :50].contiguous())  # model reads features up to 135
+        assert ei.value.code == T.TREE_ENS_E_SHAPE
+        info = m.info()
+        assert info["min_features"] <= 136 and info["n_trees"] == 10
