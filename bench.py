@@ -1,0 +1,305 @@
+#!/usr/bin/env python3
+"""Throughput of tree-ensemble scoring on one MI355X.
+
+A step is one call of tree_ens_predict over the whole workload: stage every document's
+features, walk every (document, tree) pair to its leaf, sum the leaf values, store one score
+per document. The headline workload is the learning-to-rank shaped ensemble (1,000 trees x 32
+leaves, depth <= 16, 136 features) over 100,000 documents, inputs resident in HBM.
+
+Prints ONE JSON line on stdout (progress goes to stderr):
+  value        doc*tree evaluations per second (whole job, one GPU)
+  ns_per_doc   wall time per document
+  latency_100doc_us   one 100-document batch: host wall clock of predict + stream sync
+  roofline     the scoring kernel against the LDS roofline (node bytes)
+  roofline_hbm the same kernel against HBM (feature + score bytes)
+  cpu_baseline the oracle on the host cores, same workload
+  configs_extra the other workload sizes (1M-document ones included), same measurements
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "doc·tree evals/sec; ns/doc at 1k×32-leaf trees; µs per 100-doc batch"
+HEADLINE_CFG = 2
+
+# MI355X figures ("Rooflines"): 256 CUs at 2.4 GHz; LDS read width 256 B/clk/CU;
+# HBM3E 8 TB/s.
+N_CU = 256
+CLOCK_HZ = 2.4e9
+LDS_BYTES_PER_CLK_CU = 256
+LDS_PEAK_GBS = N_CU * CLOCK_HZ * LDS_BYTES_PER_CLK_CU / 1e9  # 157,286 GB/s
+HBM_PEAK_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_1212_2287_amd", "csrc", "tree_ens.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in (KERNEL_SRC, os.path.join(ROOT, "paper_1212_2287_amd", "csrc", "pack.cpp")):
+        with open(p, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def node_depths(ens):
+    """Depth (edges from the root) of every flat node, read off the tree structure."""
+    import numpy as np
+    depth = np.zeros(ens.n_nodes, dtype=np.int32)
+    for t in range(ens.n_trees):
+        a = int(ens.tree_offsets[t])
+        fe, _, le, ri, _ = ens.tree(t)
+        stack = [0]
+        while stack:
+            n = stack.pop()
+            if fe[n] >= 0:
+                depth[a + le[n]] = depth[a + ri[n]] = depth[a + n] + 1
+                stack += [int(le[n]), int(ri[n])]
+    return depth
+
+
+def count_visits(model, ens, Xd, max_docs=None):
+    """Internal nodes visited over all (document, tree) pairs, from the leaves the GPU reaches
+    (leaf depth = comparisons made). With max_docs, counted on a prefix and scaled."""
+    import torch
+    n = Xd.shape[0] if max_docs is None else min(max_docs, Xd.shape[0])
+    depth = torch.from_numpy(node_depths(ens)).to(Xd.device).to(torch.int64)
+    offs = torch.from_numpy(ens.tree_offsets[:-1]).to(Xd.device)
+    total = 0
+    chunk = max(1, 50_000_000 // ens.n_trees)
+    for a in range(0, n, chunk):
+        ids = model.predict_leaves(Xd[a:min(n, a + chunk)].contiguous())
+        total += int(depth[offs[None, :] + ids.to(torch.int64)].sum().item())
+        del ids
+    return total * (Xd.shape[0] / n), n < Xd.shape[0]
+
+
+def time_steps(model, Xd, out, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        model.predict(Xd, out)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(steps):
+        model.predict(Xd, out)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall / steps, ev0.elapsed_time(ev1) / 1e3 / steps
+
+
+def roofline(kernel_s, lds_bytes, hbm_bytes, traffic):
+    return ({"bound": "lds", "achieved": round(lds_bytes / kernel_s / 1e9, 1), "peak": LDS_PEAK_GBS,
+             "unit": "GB/s", "frac": round(lds_bytes / kernel_s / 1e9 / LDS_PEAK_GBS, 4),
+             "traffic": traffic},
+            {"bound": "hbm", "achieved": round(hbm_bytes / kernel_s / 1e9, 1), "peak": HBM_PEAK_GBS,
+             "unit": "GB/s", "frac": round(hbm_bytes / kernel_s / 1e9 / HBM_PEAK_GBS, 4)})
+
+
+def load_traffic(workload: str):
+    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE (scaled by a copy
+    kernel of known size), if taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    ent = rec.get("workloads", {}).get(workload)
+    if not ent or rec.get("kernel_hash") != kernel_hash():
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def measure_config(T, W, cfg_id, steps, warmup, n_docs=None, visits_sample=None):
+    import torch
+    cfg = W.CONFIGS[cfg_id]
+    if n_docs is not None:
+        cfg = W.scaled(cfg, n_docs=n_docs)
+    t0 = time.perf_counter()
+    ens = W.make_ensemble(cfg)
+    X = W.make_docs(cfg)
+    log(f"config {cfg_id} ({cfg.name}): generated {cfg.n_trees} trees, {cfg.n_docs} docs in "
+        f"{time.perf_counter() - t0:.1f}s")
+    model = T.TreeEnsemble.from_ensemble(ens)
+    Xd = torch.from_numpy(X).to("cuda")
+    out = torch.empty(cfg.n_docs, dtype=torch.float32, device="cuda")
+    del X
+    wall_s, kern_s = time_steps(model, Xd, out, steps, warmup)
+    doc_trees = cfg.n_docs * cfg.n_trees
+    visits, sampled = count_visits(model, ens, Xd, visits_sample)
+    lds_bytes = visits * 8 + doc_trees * 4
+    hbm_bytes = cfg.n_docs * cfg.n_features * 4 + cfg.n_docs * 4 + model.info()["packed_bytes"]
+    rl, rl_hbm = roofline(kern_s, lds_bytes, hbm_bytes, load_traffic(cfg.name))
+    rec = {"workload": cfg.name, "n_trees": cfg.n_trees, "n_leaves": cfg.n_leaves,
+           "n_features": cfg.n_features, "n_docs": cfg.n_docs,
+           "value": doc_trees / wall_s, "ms_per_step": wall_s * 1e3, "kernel_ms": kern_s * 1e3,
+           "ns_per_doc": wall_s * 1e9 / cfg.n_docs, "visits": int(visits), "visits_sampled": sampled,
+           "roofline": rl, "roofline_hbm": rl_hbm, "model": model.info()}
+    log(f"config {cfg_id}: {rec['ms_per_step']:.3f} ms/step, {rec['value']:.3e} doc*tree/s, "
+        f"LDS frac {rl['frac']:.3f}")
+    return rec, model, ens, Xd, out
+
+
+def latency_100(model, Xd, reps=300):
+    import torch
+    x = Xd[:100].contiguous()
+    out = torch.empty(100, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(20):
+        model.predict(x, out)
+    torch.cuda.synchronize()
+    walls = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        model.predict(x, out)
+        stream.synchronize()
+        walls.append(time.perf_counter() - t0)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(reps):
+        model.predict(x, out)
+    ev1.record()
+    torch.cuda.synchronize()
+    walls.sort()
+    return {"median_us": statistics.median(walls) * 1e6, "p99_us": walls[int(0.99 * (len(walls) - 1))] * 1e6,
+            "device_us_per_call": ev0.elapsed_time(ev1) * 1e3 / reps, "reps": reps}
+
+
+def cpu_baseline(W, cfg_id, budget_s=10.0):
+    import numpy as np
+    import oracle
+    cfg = W.CONFIGS[cfg_id]
+    ens = W.make_ensemble(cfg)
+    X = W.make_docs(cfg)
+    threads = min(16, len(os.sched_getaffinity(0)))
+    oracle.score(ens, X[:1000], threads=threads, want_leaves=False)
+    runs = []
+    t_start = time.perf_counter()
+    while time.perf_counter() - t_start < budget_s and len(runs) < 50:
+        t0 = time.perf_counter()
+        oracle.score(ens, X, threads=threads, want_leaves=False)
+        runs.append(time.perf_counter() - t0)
+    sec = statistics.median(runs)
+    n1 = min(cfg.n_docs, 10_000)
+    t0 = time.perf_counter()
+    oracle.score(ens, X[:n1], threads=1, want_leaves=False)
+    single = time.perf_counter() - t0
+    return {"value": cfg.n_docs * cfg.n_trees / sec, "unit": "doc·tree/s", "cores": threads, "kind": "oracle",
+            "sample": f"{cfg.name}: all {cfg.n_docs} docs x {cfg.n_trees} trees, {len(runs)} runs "
+                      f"(median), plain C oracle (branching walk, fp64 sum), OpenMP",
+            "ns_per_doc": sec * 1e9 / cfg.n_docs,
+            "single_thread_ns_per_doc_tree": single * 1e9 / (n1 * cfg.n_trees),
+            "cpu_model": _cpu_model()}
+
+
+def pmc_probe(T, W) -> int:
+    """Copy the feature matrix once (reads and writes exactly its bytes: the calibration for the
+    FETCH_SIZE / WRITE_SIZE counters), then score it three times."""
+    import torch
+    cfg = W.CONFIGS[HEADLINE_CFG]
+    ens = W.make_ensemble(cfg)
+    Xd = torch.from_numpy(W.make_docs(cfg)).to("cuda")
+    copy = torch.empty_like(Xd)
+    torch.cuda.synchronize()
+    copy.copy_(Xd)
+    torch.cuda.synchronize()
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        out = torch.empty(cfg.n_docs, dtype=torch.float32, device="cuda")
+        for _ in range(3):
+            m.predict(Xd, out)
+        torch.cuda.synchronize()
+    log(f"pmc probe: copied {Xd.numel() * 4} bytes, scored {cfg.n_docs} docs x3")
+    return 0
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--no-extra", action="store_true", help="only the headline workload")
+    ap.add_argument("--pmc-probe", action="store_true",
+                    help="for rocprofv3 --pmc runs: one device copy of the headline workload's "
+                         "feature matrix (a kernel of known traffic, for calibration) followed by "
+                         "3 predicts; prints nothing else")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this scorer runs on a single MI355X and has no "
+              "multi-GPU path (--gpus must be 1).", file=sys.stderr)
+        return 2
+    import torch
+    import paper_1212_2287_amd as T
+    import workloads as W
+    T.load_library()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+
+    if args.pmc_probe:
+        return pmc_probe(T, W)
+    rec, model, ens, Xd, out = measure_config(T, W, HEADLINE_CFG, args.steps, args.warmup)
+    lat = latency_100(model, Xd)
+    log(f"100-doc batch: median {lat['median_us']:.1f} us, device {lat['device_us_per_call']:.1f} us/call")
+    model.close()
+    del Xd, out
+    torch.cuda.empty_cache()
+
+    extra = {}
+    if not args.no_extra:
+        for c, steps, samp in ((1, 20, None), (3, 10, None), (4, 5, None), (5, 3, 16384)):
+            r, m, _, xd, o = measure_config(T, W, c, steps, 1, visits_sample=samp)
+            r.pop("model", None)
+            extra[W.CONFIGS[c].name] = r
+            m.close()
+            del xd, o
+            torch.cuda.empty_cache()
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(W, HEADLINE_CFG)
+    cfg = W.CONFIGS[HEADLINE_CFG]
+    line = {
+        "metric": METRIC, "value": rec["value"], "unit": "doc·tree/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": rec["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "accumulate": "f64", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.n_trees} trees x {cfg.n_leaves} leaves (depth <= "
+                               f"{cfg.max_depth}), {cfg.n_features} features, {cfg.n_docs} docs",
+                   "n_trees": cfg.n_trees, "n_docs": cfg.n_docs, "n_features": cfg.n_features,
+                   "docs_per_block": rec["model"]["docs_per_block"]},
+        "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"],
+        "latency_100doc_us": lat, "visits": rec["visits"],
+        "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
+        "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

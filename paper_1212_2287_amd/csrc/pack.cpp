@@ -38,12 +38,16 @@ LdsPlan plan_lds(int32_t n_cols) {
         return p;
     p.xs_bytes = int32_t(cols * p.docs_per_block * 4);
     const int reserve = 64; // the all-zero record used by padding walkers, plus slack
+    // 16 waves per workgroup; two workgroups per CU when the document tile is small (32 waves
+    // per CU hide the LDS latency of one walk per lane), else one workgroup whose lanes walk
+    // two trees at once.
+    p.wg_threads = 1024;
     if (p.xs_bytes <= kTwoWgXsBytes) {
         p.lds_bytes = kLdsPerCu / 2;
-        p.wg_threads = 512;
+        p.interleave = 1;
     } else {
         p.lds_bytes = kLdsPerCu;
-        p.wg_threads = 1024;
+        p.interleave = 2;
     }
     p.tile_bytes = (p.lds_bytes - p.xs_bytes - reserve) & ~15;
     return p;
@@ -95,8 +99,8 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         const int64_t a = tree_offsets[t];
         const int64_t n = tree_offsets[t + 1] - a;
         const std::string where = "tree " + std::to_string(t) + ": ";
-        if (n > 65536) {
-            err = where + "more than 65536 nodes";
+        if (n > kMaxTreeNodes) {
+            err = where + "more than " + std::to_string(kMaxTreeNodes) + " nodes";
             return kErrModel;
         }
         parents.assign(size_t(n), 0);
@@ -221,10 +225,11 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             if (feature[a + i] >= 0) {
                 const float th = strict ? strict_to_inclusive(threshold[a + i]) : threshold[a + i];
                 r.thr_bits = float_bits(th);
-                r.w = (uint32_t(new_id[size_t(left[a + i])]) << 16) | uint32_t(feature[a + i] + 1);
+                const uint32_t col = uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) * 4u;
+                r.w = (uint32_t(new_id[size_t(left[a + i])]) << kChildShift) | col;
             } else {
                 r.thr_bits = float_bits(value[a + i]);
-                r.w = uint32_t(ni) << 16;
+                r.w = uint32_t(ni) << kChildShift;
             }
         }
         p.tree_depth[size_t(pt)] = uint32_t(depth_of[size_t(t)]);

@@ -15,17 +15,23 @@ namespace treeens {
 
 // One node record, 8 bytes, as the kernels read it from LDS with one 64-bit load.
 //   internal node: thr = threshold (nudged to the next float up under the strict rule),
-//                  w   = (left child local index << 16) | (feature id + 1)
+//                  w   = (left child local index << kChildShift) | column byte offset
 //   leaf:          thr = leaf value,
-//                  w   = (own local index << 16) | 0
-// Column 0 of a staged document tile holds NaN for every document, so a leaf compares a NaN
-// with its value, gets "left" and its child index is itself: leaves absorb any further steps.
-// The right child of an internal node is at left + 1.
+//                  w   = (own local index << kChildShift) | 0
+// The column byte offset of feature f is (f + 1) * docs_per_block * 4: the offset of f's column
+// in the staged document tile, so a lane's feature address is (w & kColMask) | (lane * 4).
+// Column 0 of the tile holds NaN for every document, so a leaf compares a NaN with its value,
+// gets "left" and its child index is itself: leaves absorb any further steps, and a lane is at
+// a leaf exactly when its record's column offset is 0. The right child of an internal node is
+// at left + 1.
 struct NodeRec {
     uint32_t thr_bits;
     uint32_t w;
 };
 static_assert(sizeof(NodeRec) == 8, "node record must be 8 bytes");
+constexpr int kChildShift = 17;
+constexpr uint32_t kColMask = (1u << kChildShift) - 1; // column offsets < 128 KiB
+constexpr int kMaxTreeNodes = 1 << (32 - kChildShift); // 32768 nodes per tree
 
 // A run of whole trees [tree_begin, tree_end) (packed order) staged into LDS together.
 struct Tile {
@@ -42,6 +48,7 @@ struct LdsPlan {
     int32_t tile_bytes;     // LDS bytes for node records of one tile
     int32_t wg_threads;     // workgroup size
     int32_t lds_bytes;      // total dynamic LDS per workgroup
+    int32_t interleave;     // trees each lane walks at once (K)
 };
 
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950 LDS per compute unit

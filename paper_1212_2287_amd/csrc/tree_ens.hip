@@ -7,10 +7,12 @@
 //     feature the lane's current node names;
 //   * the trees are streamed through LDS in tiles (runs of whole trees, packed node records);
 //   * lanes are documents; each group of DL lanes (a "walker") walks one tree at a time for its
-//     DL documents, and each lane interleaves K independent trees so that their LDS latencies
-//     overlap (the vectorisation idea of Section 3, VPred, moved from instances to trees);
+//     DL documents; with one workgroup per CU each lane interleaves K = 2 independent trees so
+//     that their LDS latencies overlap (the vectorisation idea of Section 3, VPred, applied
+//     to trees instead of instances);
 //   * each step is the branch-free predicated update of Section 3 (Pred) over explicit,
-//     sibling-adjacent children: idx = left(idx) + (x[fid(idx)] >= theta(idx));
+//     sibling-adjacent children: idx = left(idx) + (x[fid(idx)] >= theta(idx)); a wave stops
+//     as soon as all its lanes sit on leaves (trees are unbalanced; most paths are short);
 //   * leaf values are summed per lane in double precision, then reduced across walkers through
 //     LDS in a fixed order and rounded once to float.
 // Small batches split the tiles over a second grid dimension and reduce the per-split partial
@@ -28,10 +30,6 @@
 
 #include "pack.hpp"
 #include "tree_ens.h"
-
-#ifndef TREE_ENS_K
-#define TREE_ENS_K 2 // trees interleaved per lane
-#endif
 
 using treeens::NodeRec;
 using treeens::Packed;
@@ -51,10 +49,19 @@ int hip_fail(hipError_t e, const char *what) {
 }
 
 constexpr int kNumCus = 256;
+constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves)
 
 // ------------------------------------------------------------------------------------------
 // kernels
 // ------------------------------------------------------------------------------------------
+
+// (w & mask) | b in one VALU op. The feature column offset is a multiple of DL * 4 and the lane
+// offset is below DL * 4, so the OR is the sum the address needs.
+__device__ __forceinline__ uint32_t and_or(uint32_t w, uint32_t mask, uint32_t b) {
+    uint32_t r;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(w), "s"(mask), "v"(b));
+    return r;
+}
 template <int DL, int K, bool LEAVES>
 __global__ void __launch_bounds__(1024)
 score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
@@ -64,32 +71,55 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
              double *__restrict__ partials, float *__restrict__ scores,
              int32_t *__restrict__ leaf_ids, const int32_t *__restrict__ orig_id,
              const int32_t *__restrict__ tree_orig, int32_t n_trees) {
-    extern __shared__ __align__(16) unsigned char lds[];
+    (void)tree_depth;
+    // static allocation: the LDS base is address 0, so feature and node addresses need no add
+    constexpr int kLds = K == 1 ? treeens::kLdsPerCu / 2 : treeens::kLdsPerCu;
+    __shared__ __align__(16) unsigned char lds[kLds];
     float *xs = reinterpret_cast<float *>(lds);
     uint2 *tn = reinterpret_cast<uint2 *>(lds + xs_bytes);
     const uint32_t zero_rec = uint32_t(xs_bytes + tile_bytes);
 
     const int tid = threadIdx.x;
-    const int nthr = blockDim.x;
+    const int nthr = kThreads;
     const int dl = tid & (DL - 1);
-    const int walker = tid / DL;
+    // with 64-document blocks a walker is a whole wave: make that visible to the compiler so
+    // the tree loop, the tree offsets and the trip bound live in scalar registers
+    const int walker = DL == 64 ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
     const int n_walkers = nthr / DL;
+    const uint32_t lane_off = uint32_t(dl) * 4u;
+    const uint32_t col_mask = __builtin_amdgcn_readfirstlane(treeens::kColMask);
+    constexpr uint32_t kLeafCol = uint32_t(DL) * 4u; // column offsets below this are the NaN column
     const int64_t doc0 = int64_t(blockIdx.x) * DL;
     const int split = blockIdx.y;
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
     const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
 
-    // stage the document tile: one column per DL consecutive lanes, lane = document
-    const int n_elem = (n_cols + 1) * DL;
-    for (int e = tid; e < n_elem; e += nthr) {
-        const int c = e / DL;
-        const int d = e & (DL - 1);
-        float v = __builtin_nanf("");
-        if (c > 0) {
-            const int64_t doc = doc0 + d;
-            v = doc < n_docs ? X[doc * n_features + (c - 1)] : 0.0f;
+    // stage the document tile: lane = document, so each LDS write is conflict-free. The
+    // workgroup size is a multiple of DL, so a thread's document (and row) is fixed and its
+    // columns step by kThreads / DL; eight columns are loaded before any is written so the
+    // global loads of a pass are in flight together.
+    {
+        constexpr int kColStep = kThreads / DL;
+        constexpr int kUnroll = 8;
+        const int64_t doc = doc0 + dl;
+        const bool live = doc < n_docs;
+        const float *row = X + (live ? doc : 0) * int64_t(n_features);
+        for (int c0 = tid / DL; c0 <= n_cols; c0 += kColStep * kUnroll) {
+            float v[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int c = c0 + u * kColStep;
+                v[u] = __builtin_nanf("");
+                if (c > 0 && c <= n_cols)
+                    v[u] = live ? row[c - 1] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int c = c0 + u * kColStep;
+                if (c <= n_cols)
+                    xs[c * DL + dl] = v[u];
+            }
         }
-        xs[e] = v;
     }
     if (tid == 0)
         *reinterpret_cast<uint2 *>(lds + zero_rec) = make_uint2(0u, 0u);
@@ -105,26 +135,46 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
         __syncthreads();
         const int ntr = tl.tree_end - tl.tree_begin;
         for (int g = walker * K; g < ntr; g += n_walkers * K) {
-            uint32_t base[K], idx[K];
-            int dmax = 0;
+            uint32_t base[K], addr[K];
+            uint2 nd[K];
 #pragma unroll
             for (int i = 0; i < K; ++i) {
-                idx[i] = 0;
-                if (g + i < ntr) {
-                    const int gt = tl.tree_begin + g + i;
-                    base[i] = uint32_t(xs_bytes) + (tree_node_off[gt] - uint32_t(tl.node_begin)) * 8u;
-                    dmax = max(dmax, int(tree_depth[gt]));
-                } else {
-                    base[i] = zero_rec;
-                }
+                base[i] = zero_rec;
+                if (g + i < ntr)
+                    base[i] = uint32_t(xs_bytes) +
+                              (tree_node_off[tl.tree_begin + g + i] - uint32_t(tl.node_begin)) * 8u;
+                // keep the tree base opaque so the step computes base + child * 8 directly
+                // instead of re-associating it into the child index
+                if constexpr (DL == 64)
+                    asm("" : "+s"(base[i]));
+                else
+                    asm("" : "+v"(base[i]));
+                addr[i] = base[i];
+                nd[i] = *reinterpret_cast<const uint2 *>(lds + addr[i]);
             }
-            for (int s = 0; s < dmax; ++s) {
+            // Predicated walk: every lane steps until all lanes of the wave sit on leaves. The
+            // record read that shows a lane is at a leaf already holds the leaf's value. A walk
+            // ends within max_depth steps; the bound only guarantees termination.
+            for (int s = 0; s <= tl.max_depth; ++s) {
+                uint32_t fa[K];
+                bool internal = false;
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
-                    const uint2 nd = *reinterpret_cast<const uint2 *>(lds + base[i] + idx[i] * 8u);
-                    const float x = xs[(nd.y & 0xffffu) * DL + dl];
-                    idx[i] = (nd.y >> 16) + (x >= __uint_as_float(nd.x) ? 1u : 0u);
+                    fa[i] = and_or(nd[i].y, col_mask, lane_off);
+                    internal |= fa[i] >= kLeafCol;
                 }
+                if (!__any(internal))
+                    break;
+#pragma unroll
+                for (int i = 0; i < K; ++i) {
+                    const float x = *reinterpret_cast<const float *>(lds + fa[i]);
+                    const uint32_t child =
+                        (nd[i].y >> treeens::kChildShift) + (x >= __uint_as_float(nd[i].x) ? 1u : 0u);
+                    addr[i] = base[i] + child * 8u;
+                }
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    nd[i] = *reinterpret_cast<const uint2 *>(lds + addr[i]);
             }
 #pragma unroll
             for (int i = 0; i < K; ++i) {
@@ -132,12 +182,11 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
                     const int64_t doc = doc0 + dl;
                     if (g + i < ntr && doc < n_docs) {
                         const int gt = tl.tree_begin + g + i;
-                        leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + idx[i]];
+                        leaf_ids[doc * n_trees + tree_orig[gt]] =
+                            orig_id[tree_node_off[gt] + (addr[i] - base[i]) / 8u];
                     }
                 } else {
-                    const float v = __uint_as_float(
-                        *reinterpret_cast<const uint32_t *>(lds + base[i] + idx[i] * 8u));
-                    acc += double(v);
+                    acc += double(__uint_as_float(nd[i].x)); // the zero record adds 0.0
                 }
             }
         }
@@ -148,29 +197,34 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
         red[walker * DL + dl] = acc;
         __syncthreads();
         if (walker == 0) {
-            double s = 0.0;
+            double sum = 0.0;
             for (int w = 0; w < n_walkers; ++w)
-                s += red[w * DL + dl];
+                sum += red[w * DL + dl];
             const int64_t doc = doc0 + dl;
             if (doc < n_docs) {
                 if (n_splits == 1)
-                    scores[doc] = float(s);
+                    scores[doc] = float(sum);
                 else
-                    partials[int64_t(split) * n_docs + doc] = s;
+                    partials[int64_t(split) * n_docs + doc] = sum;
             }
         }
     }
 }
 
-__global__ void reduce_partials_kernel(const double *__restrict__ partials, int32_t n_splits,
-                                       int64_t n_docs, float *__restrict__ scores) {
-    const int64_t d = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (d < n_docs) {
-        double s = 0.0;
-        for (int k = 0; k < n_splits; ++k)
-            s += partials[int64_t(k) * n_docs + d];
+// One wave per document: lanes take the split partials in a fixed interleave, then a fixed
+// butterfly combines the lanes, so the sum's order (and its rounding) never changes.
+__global__ void __launch_bounds__(64)
+reduce_partials_kernel(const double *__restrict__ partials, int32_t n_splits, int64_t n_docs,
+                       float *__restrict__ scores) {
+    const int64_t d = blockIdx.x;
+    double s = 0.0;
+    for (int k = threadIdx.x; k < n_splits; k += 64)
+        s += partials[int64_t(k) * n_docs + d];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        s += __shfl_xor(s, off);
+    if (threadIdx.x == 0)
         scores[d] = float(s);
-    }
 }
 
 __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
@@ -183,9 +237,8 @@ using ScoreFn = void (*)(const float *, int64_t, int32_t, int32_t, const uint2 *
                          const uint32_t *, const Tile *, int32_t, int32_t, int32_t, int32_t,
                          double *, float *, int32_t *, const int32_t *, const int32_t *, int32_t);
 
-template <bool LEAVES>
-ScoreFn pick_kernel(int dl) {
-    constexpr int K = TREE_ENS_K;
+template <int K, bool LEAVES>
+ScoreFn pick_dl(int dl) {
     switch (dl) {
     case 64: return score_kernel<64, K, LEAVES>;
     case 32: return score_kernel<32, K, LEAVES>;
@@ -193,6 +246,11 @@ ScoreFn pick_kernel(int dl) {
     case 8: return score_kernel<8, K, LEAVES>;
     default: return nullptr;
     }
+}
+
+template <bool LEAVES>
+ScoreFn pick_kernel(int dl, int k) {
+    return k == 2 ? pick_dl<2, LEAVES>(dl) : k == 1 ? pick_dl<1, LEAVES>(dl) : nullptr;
 }
 
 } // namespace
@@ -305,13 +363,10 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     int level, splits;
     choose_split(h, n_blocks, &level, &splits);
-    ScoreFn fn = pick_kernel<LEAVES>(dl);
+    ScoreFn fn = pick_kernel<LEAVES>(dl, h->plan.interleave);
     if (!fn)
         return fail(TREE_ENS_E_ARG, "unsupported document block size");
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, h->plan.lds_bytes);
-    if (e != hipSuccess)
-        return hip_fail(e, "hipFuncSetAttribute");
+    hipError_t e = hipSuccess;
     double *partials = nullptr;
     if (!LEAVES && splits > 1) {
         e = hipMallocAsync(reinterpret_cast<void **>(&partials),
@@ -322,16 +377,15 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const Tile *tiles = h->d_tiles + h->level_begin[level];
     const int n_tiles = h->level_begin[level + 1] - h->level_begin[level];
     (void)hipGetLastError();
-    hipLaunchKernelGGL(fn, dim3(unsigned(n_blocks), unsigned(splits)), dim3(h->plan.wg_threads),
-                       h->plan.lds_bytes, stream, X, n_docs, n_features, h->n_cols, h->d_nodes,
+    hipLaunchKernelGGL(fn, dim3(unsigned(n_blocks), unsigned(splits)), dim3(kThreads), 0,
+                       stream, X, n_docs, n_features, h->n_cols, h->d_nodes,
                        h->d_tree_node_off, h->d_tree_depth, tiles, n_tiles, splits,
                        h->plan.xs_bytes, h->plan.tile_bytes, partials, scores, leaf_ids,
                        h->d_orig_id, h->d_tree_orig, h->n_trees);
     e = hipGetLastError();
     if (e == hipSuccess && partials) {
-        const int bs = 256;
-        hipLaunchKernelGGL(reduce_partials_kernel, dim3(unsigned((n_docs + bs - 1) / bs)), dim3(bs),
-                           0, stream, partials, splits, n_docs, scores);
+        hipLaunchKernelGGL(reduce_partials_kernel, dim3(unsigned(n_docs)), dim3(64), 0, stream,
+                           partials, splits, n_docs, scores);
         e = hipGetLastError();
     }
     if (partials) {
