@@ -34,7 +34,7 @@ def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
     obj = out + ".pack.o"
     run = (lambda c: subprocess.run(c, check=True)) if verbose else \
         (lambda c: subprocess.run(c, check=True, stdout=subprocess.DEVNULL))
-    run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", "-c",
+    run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", *[f"-D{d}" for d in defines], "-c",
          os.path.join(CSRC, "pack.cpp"), "-o", obj])
     run([_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC, "-shared",
          os.path.join(CSRC, "tree_ens.hip"), "-x", "none", obj, "-o", tmp])

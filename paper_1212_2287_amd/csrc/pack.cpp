@@ -25,7 +25,8 @@ float strict_to_inclusive(float theta) {
     return std::nextafter(theta, INFINITY);
 }
 
-LdsPlan plan_lds(int32_t n_cols) {
+// avg_tree_bytes: mean packed size of a tree, to pick how many trees a lane walks at once.
+LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes) {
     LdsPlan p{};
     const int64_t cols = int64_t(n_cols) + 1; // + the NaN column the leaves read
     for (int dl = 64; dl >= 8; dl /= 2) {
@@ -37,19 +38,20 @@ LdsPlan plan_lds(int32_t n_cols) {
     if (p.docs_per_block == 0)
         return p;
     p.xs_bytes = int32_t(cols * p.docs_per_block * 4);
-    const int reserve = 64; // the all-zero record used by padding walkers, plus slack
-    // 16 waves per workgroup; two workgroups per CU when the document tile is small (32 waves
-    // per CU hide the LDS latency of one walk per lane), else one workgroup whose lanes walk
-    // two trees at once.
+    const int reserve = kMetaBytes + 64; // tree-offset table, the all-zero record, slack
+    // 16 waves per workgroup; two workgroups per CU when the document tile is small
     p.wg_threads = 1024;
-    if (p.xs_bytes <= kTwoWgXsBytes) {
-        p.lds_bytes = kLdsPerCu / 2;
-        p.interleave = 1;
-    } else {
-        p.lds_bytes = kLdsPerCu;
-        p.interleave = 2;
-    }
-    p.tile_bytes = (p.lds_bytes - p.xs_bytes - reserve) & ~15;
+    p.lds_bytes = p.xs_bytes <= kTwoWgXsBytes ? kLdsPerCu / 2 : kLdsPerCu;
+    const int prefetch = p.lds_bytes == kLdsPerCu / 2 ? kPrefetchHalf : kPrefetchFull;
+    p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve, prefetch * 1024 * 8) & ~15;
+    // Interleave K trees per lane (latency hiding) only when a tile holds at least K rounds of
+    // walker groups; otherwise most walkers would sit idle.
+    const double fit = avg_tree_bytes > 0 ? p.tile_bytes / avg_tree_bytes : 1e9;
+    const int walkers = 1024 / p.docs_per_block;
+    p.interleave = fit >= 4.0 * walkers ? 4 : fit >= 2.0 * walkers ? 2 : 1;
+#ifdef TREE_ENS_INTERLEAVE // measurement builds only: force the trees-per-lane interleave
+    p.interleave = TREE_ENS_INTERLEAVE;
+#endif
     return p;
 }
 
@@ -163,13 +165,18 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     }
 
     const int32_t n_cols = max_fid + 1;
-    LdsPlan plan = plan_lds(n_cols);
+    LdsPlan plan = plan_lds(n_cols, n_trees > 0 ? 8.0 * double(n_nodes) / n_trees : 0.0);
     if (plan.docs_per_block == 0) {
         err = "feature id " + std::to_string(max_fid) + " is beyond the LDS document-tile limit (" +
               std::to_string(kXsMaxBytes / (8 * 4) - 2) + ")";
         return kErrModel;
     }
     const int64_t max_nodes_per_tree = plan.tile_bytes / int64_t(sizeof(NodeRec));
+    int64_t largest_tree = 0;
+    for (int32_t t = 0; t < n_trees; t++)
+        largest_tree = std::max<int64_t>(largest_tree, tree_offsets[t + 1] - tree_offsets[t]);
+    // the narrow format needs column offsets below 64 KiB and child indices below 2^16
+    plan.narrow = (plan.xs_bytes <= 65536 && largest_tree <= kNarrowMaxTreeNodes) ? 1 : 0;
     for (int32_t t = 0; t < n_trees; t++) {
         const int64_t n = tree_offsets[t + 1] - tree_offsets[t];
         if (n > max_nodes_per_tree) {
@@ -194,6 +201,9 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     p.tree_node_off.resize(size_t(n_trees) + 1, 0);
     p.tree_depth.resize(size_t(n_trees), 0);
     std::vector<int32_t> new_id;
+    auto link = [&](uint32_t child) {
+        return plan.narrow ? child << 16 : child << kWideChildShift;
+    };
     for (int32_t pt = 0; pt < n_trees; pt++) {
         const int32_t t = p.tree_orig[size_t(pt)];
         const int64_t a = tree_offsets[t];
@@ -226,10 +236,10 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                 const float th = strict ? strict_to_inclusive(threshold[a + i]) : threshold[a + i];
                 r.thr_bits = float_bits(th);
                 const uint32_t col = uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) * 4u;
-                r.w = (uint32_t(new_id[size_t(left[a + i])]) << kChildShift) | col;
+                r.w = link(uint32_t(new_id[size_t(left[a + i])])) | col;
             } else {
                 r.thr_bits = float_bits(value[a + i]);
-                r.w = uint32_t(ni) << kChildShift;
+                r.w = link(uint32_t(ni));
             }
         }
         p.tree_depth[size_t(pt)] = uint32_t(depth_of[size_t(t)]);
@@ -238,24 +248,36 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     p.tree_node_off[size_t(n_trees)] = uint32_t(p.nodes.size());
 
     // ---- pass 3: tilings at budget / 2^k -------------------------------------------------
+    // A tile is a run of whole trees within the byte budget. When more than one round of
+    // walker groups fits, the run is cut to a whole number of rounds (walkers x interleave
+    // trees), so that statically assigned groups finish together.
+    const int32_t round = (1024 / plan.docs_per_block) * plan.interleave;
     for (int k = 0; k < kTileLevels; k++) {
         p.level_begin[k] = int32_t(p.tiles.size());
         const int64_t budget = std::max<int64_t>(plan.tile_bytes >> k, 1);
         int32_t tb = 0;
         while (tb < n_trees) {
-            int32_t te = tb;
-            int64_t bytes = 0;
-            int32_t dmax = 0;
-            while (te < n_trees) {
-                const int64_t tbytes =
-                    int64_t(p.tree_node_off[size_t(te) + 1] - p.tree_node_off[size_t(te)]) * 8;
-                if (te > tb && bytes + tbytes > budget)
+            int32_t fit = 0;
+            for (int64_t bytes = 0; tb + fit < n_trees && fit < kMaxTileTrees; fit++) {
+                const int64_t nn = int64_t(p.tree_node_off[size_t(tb + fit) + 1] -
+                                           p.tree_node_off[size_t(tb + fit)]);
+                if (fit > 0 && bytes + nn * 8 > budget)
                     break;
-                bytes += tbytes;
-                dmax = std::max(dmax, int32_t(p.tree_depth[size_t(te)]));
+                bytes += nn * 8;
+            }
+            const int32_t limit = (fit > round && tb + fit < n_trees) ? fit / round * round : fit;
+            int32_t te = tb;
+            int32_t dmax = 0;
+            int32_t complete = -2; // -2: no tree yet
+            while (te < tb + limit) {
+                const int64_t nn = int64_t(p.tree_node_off[size_t(te) + 1] - p.tree_node_off[size_t(te)]);
+                const int32_t d = int32_t(p.tree_depth[size_t(te)]);
+                dmax = std::max(dmax, d);
+                const bool full = nn == (int64_t(2) << d) - 1; // complete binary tree of depth d
+                complete = (complete == -2 || complete == d) && full ? d : -1;
                 te++;
             }
-            p.tiles.push_back(Tile{tb, te, dmax, int32_t(p.tree_node_off[size_t(tb)])});
+            p.tiles.push_back(Tile{tb, te, dmax, int32_t(p.tree_node_off[size_t(tb)]), complete});
             tb = te;
         }
     }

@@ -13,33 +13,39 @@
 
 namespace treeens {
 
-// One node record, 8 bytes, as the kernels read it from LDS with one 64-bit load.
-//   internal node: thr = threshold (nudged to the next float up under the strict rule),
-//                  w   = (left child local index << kChildShift) | column byte offset
-//   leaf:          thr = leaf value,
-//                  w   = (own local index << kChildShift) | 0
+// One node record, 8 bytes: {thr, w}.
+//   internal node: thr = threshold (nudged to the next float up under the strict rule)
+//   leaf:          thr = leaf value
+// w packs the feature column and the child link in one of two formats:
+//   narrow: w = (left child index << 16) | column byte offset             (column < 64 KiB)
+//   wide:   w = (left child index << kWideChildShift) | column byte offset (column < 128 KiB)
+// The child link is tree-relative; the right child follows the left one. A leaf links to
+// itself and has column offset 0.
 // The column byte offset of feature f is (f + 1) * docs_per_block * 4: the offset of f's column
-// in the staged document tile, so a lane's feature address is (w & kColMask) | (lane * 4).
+// in the staged document tile, so a lane's feature address is (w & column mask) | (lane * 4).
 // Column 0 of the tile holds NaN for every document, so a leaf compares a NaN with its value,
-// gets "left" and its child index is itself: leaves absorb any further steps, and a lane is at
-// a leaf exactly when its record's column offset is 0. The right child of an internal node is
-// at left + 1.
+// gets "left" and its link is itself: leaves absorb any further steps, and a lane is at a leaf
+// exactly when its record's column offset is 0.
 struct NodeRec {
     uint32_t thr_bits;
     uint32_t w;
 };
 static_assert(sizeof(NodeRec) == 8, "node record must be 8 bytes");
-constexpr int kChildShift = 17;
-constexpr uint32_t kColMask = (1u << kChildShift) - 1; // column offsets < 128 KiB
-constexpr int kMaxTreeNodes = 1 << (32 - kChildShift); // 32768 nodes per tree
+constexpr int kWideChildShift = 17;
+constexpr uint32_t kNarrowColMask = 0xffffu;
+constexpr uint32_t kWideColMask = (1u << kWideChildShift) - 1; // column offsets < 128 KiB
+constexpr int kMaxTreeNodes = 1 << (32 - kWideChildShift);    // 32768 nodes per tree
+constexpr int kNarrowMaxTreeNodes = 1 << 16;                    // 16-bit child index
 
 // A run of whole trees [tree_begin, tree_end) (packed order) staged into LDS together.
 struct Tile {
     int32_t tree_begin;
     int32_t tree_end;
-    int32_t max_depth;  // deepest tree in the run: the walk's trip count
-    int32_t node_begin; // packed node offset of tree_begin
+    int32_t max_depth;      // deepest tree in the run: bounds the walk's trip count
+    int32_t node_begin;     // packed node offset of tree_begin
+    int32_t complete_depth; // d if every tree of the run is complete of depth d, else -1
 };
+constexpr int kMaxTileTrees = 1024; // one LDS offset slot per tree of a tile
 
 // Launch plan fixed at create time from the model's feature range.
 struct LdsPlan {
@@ -49,9 +55,15 @@ struct LdsPlan {
     int32_t wg_threads;     // workgroup size
     int32_t lds_bytes;      // total dynamic LDS per workgroup
     int32_t interleave;     // trees each lane walks at once (K)
+    int32_t narrow;         // 1: narrow record format (see NodeRec), 0: wide
 };
 
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950 LDS per compute unit
+constexpr int kMetaBytes = kMaxTileTrees * 4; // per-tile table of tree offsets in LDS
+// The kernels prefetch a whole tile into registers (1,024 threads x kPrefetch records): at most
+// 6 records per thread when two workgroups share a CU (64 VGPRs each), 16 when one owns it.
+constexpr int kPrefetchHalf = 6;
+constexpr int kPrefetchFull = 16;
 constexpr int kXsMaxBytes = 96 * 1024; // cap on the staged document tile
 constexpr int kTwoWgXsBytes = 40 * 1024; // tiles up to this size leave room for 2 workgroups/CU
 constexpr int kTileLevels = 5;         // tilings at budget, budget/2, ..., budget/16

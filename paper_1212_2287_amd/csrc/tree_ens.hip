@@ -62,37 +62,80 @@ __device__ __forceinline__ uint32_t and_or(uint32_t w, uint32_t mask, uint32_t b
     asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(w), "s"(mask), "v"(b));
     return r;
 }
-template <int DL, int K, bool LEAVES>
-__global__ void __launch_bounds__(1024)
+// Child index of a narrow record plus the comparison bit, in two VALU ops: the compare writes
+// VCC and an SDWA add-with-carry adds it to the high half-word of w. The s_nop covers the
+// VALU-writes-VCC / VALU-reads-carry hazard (two wait states, as the compiler itself emits).
+__device__ __forceinline__ uint32_t narrow_child(uint32_t w, float x, float thr) {
+    uint32_t r;
+    asm("v_cmp_ge_f32 vcc, %1, %2\n\t"
+        "s_nop 1\n\t"
+        "v_addc_co_u32_sdwa %0, vcc, %3, 0, vcc dst_sel:DWORD dst_unused:UNUSED_PAD "
+        "src0_sel:WORD_1 src1_sel:DWORD"
+        : "=v"(r)
+        : "v"(x), "v"(thr), "v"(w)
+        : "vcc");
+    return r;
+}
+
+template <int DL, int K, bool HALF, bool NARROW, bool LEAVES>
+__global__ void __launch_bounds__(kThreads, HALF ? 8 : 4) // min waves per SIMD: 2 or 1 workgroups per CU
 score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
              const uint2 *__restrict__ nodes, const uint32_t *__restrict__ tree_node_off,
-             const uint32_t *__restrict__ tree_depth, const Tile *__restrict__ tiles,
-             int32_t n_tiles, int32_t n_splits, int32_t xs_bytes, int32_t tile_bytes,
-             double *__restrict__ partials, float *__restrict__ scores,
+             const Tile *__restrict__ tiles, int32_t n_tiles, int32_t n_splits, int32_t xs_bytes,
+             int32_t tile_bytes, double *__restrict__ partials, float *__restrict__ scores,
              int32_t *__restrict__ leaf_ids, const int32_t *__restrict__ orig_id,
              const int32_t *__restrict__ tree_orig, int32_t n_trees) {
-    (void)tree_depth;
-    // static allocation: the LDS base is address 0, so feature and node addresses need no add
-    constexpr int kLds = K == 1 ? treeens::kLdsPerCu / 2 : treeens::kLdsPerCu;
+    // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
+    // HALF = half a CU's LDS, so that two workgroups share a CU. Layout:
+    //   [0, xs_bytes)                      document tile, [(n_cols + 1) x DL] floats
+    //   [xs_bytes, +tile_bytes)            node records of the current tile
+    //   [meta_off, +kMetaBytes)            tile-relative record offset of each tree of the tile
+    //   zero_rec (8 bytes)                 all-zero record: a leaf of value 0 for idle slots
+    constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 : treeens::kLdsPerCu;
     __shared__ __align__(16) unsigned char lds[kLds];
-    float *xs = reinterpret_cast<float *>(lds);
+    constexpr int kPre = HALF ? treeens::kPrefetchHalf : treeens::kPrefetchFull; // records per thread
+    constexpr bool kUniform = DL == 64; // a walker is a whole wave: tree bases are scalar
+    const uint32_t meta_off = uint32_t(xs_bytes + tile_bytes);
+    const uint32_t zero_rec = meta_off + uint32_t(treeens::kMetaBytes);
+    uint32_t *meta = reinterpret_cast<uint32_t *>(lds + meta_off);
     uint2 *tn = reinterpret_cast<uint2 *>(lds + xs_bytes);
-    const uint32_t zero_rec = uint32_t(xs_bytes + tile_bytes);
+    float *xs = reinterpret_cast<float *>(lds);
 
     const int tid = threadIdx.x;
     const int nthr = kThreads;
     const int dl = tid & (DL - 1);
     // with 64-document blocks a walker is a whole wave: make that visible to the compiler so
-    // the tree loop, the tree offsets and the trip bound live in scalar registers
-    const int walker = DL == 64 ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
+    // the group loop and the tree bases live in scalar registers
+    const int walker = kUniform ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
     const int n_walkers = nthr / DL;
     const uint32_t lane_off = uint32_t(dl) * 4u;
-    const uint32_t col_mask = __builtin_amdgcn_readfirstlane(treeens::kColMask);
+    const uint32_t col_mask =
+        __builtin_amdgcn_readfirstlane(NARROW ? treeens::kNarrowColMask : treeens::kWideColMask);
     constexpr uint32_t kLeafCol = uint32_t(DL) * 4u; // column offsets below this are the NaN column
     const int64_t doc0 = int64_t(blockIdx.x) * DL;
     const int split = blockIdx.y;
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
     const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
+
+    // The next tile's records and tree offsets are loaded into registers while the current
+    // tile is walked, so the global-memory latency of a tile load is hidden.
+    uint2 pre[kPre];
+    uint32_t pre_meta = 0;
+    auto fetch = [&](int ti) {
+        const Tile tl = tiles[ti];
+        const int n_rec = int(tree_node_off[tl.tree_end]) - tl.node_begin;
+        const uint2 *src = nodes + tl.node_begin;
+#pragma unroll
+        for (int j = 0; j < kPre; ++j) {
+            const int i = tid + j * kThreads;
+            if (i < n_rec)
+                pre[j] = src[i];
+        }
+        if (!kUniform && tid < tl.tree_end - tl.tree_begin)
+            pre_meta = tree_node_off[tl.tree_begin + tid] - uint32_t(tl.node_begin);
+    };
+    if (t_lo < t_hi)
+        fetch(t_lo);
 
     // stage the document tile: lane = document, so each LDS write is conflict-free. The
     // workgroup size is a multiple of DL, so a thread's document (and row) is fixed and its
@@ -128,65 +171,105 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
     for (int ti = t_lo; ti < t_hi; ++ti) {
         const Tile tl = tiles[ti];
         const int n_rec = int(tree_node_off[tl.tree_end]) - tl.node_begin;
-        __syncthreads(); // previous tile fully consumed (and the document tile written)
-        const uint2 *src = nodes + tl.node_begin;
-        for (int i = tid; i < n_rec; i += nthr)
-            tn[i] = src[i];
-        __syncthreads();
         const int ntr = tl.tree_end - tl.tree_begin;
-        for (int g = walker * K; g < ntr; g += n_walkers * K) {
-            uint32_t base[K], addr[K];
+        __syncthreads(); // the previous tile is fully walked (and the document tile written)
+#pragma unroll
+        for (int j = 0; j < kPre; ++j) {
+            const int i = tid + j * kThreads;
+            if (i < n_rec)
+                tn[i] = pre[j];
+        }
+        if (!kUniform && tid < ntr)
+            meta[tid] = pre_meta;
+        __syncthreads();
+        if (ti + 1 < t_hi)
+            fetch(ti + 1);
+
+        // Walker w takes groups w, w + n_walkers, ... of K consecutive trees (the packer sizes
+        // tiles to a multiple of n_walkers * K trees where it can).
+        const int n_groups = (ntr + K - 1) / K;
+        auto tree_base = [&](int t) -> uint32_t {
+            if (t >= ntr)
+                return zero_rec;
+            if constexpr (kUniform)
+                return uint32_t(xs_bytes) +
+                       (tree_node_off[tl.tree_begin + t] - uint32_t(tl.node_begin)) * 8u;
+            else
+                return uint32_t(xs_bytes) + meta[t] * 8u;
+        };
+        for (int g = walker; g < n_groups; g += n_walkers) {
+            uint32_t base[K];
             uint2 nd[K];
 #pragma unroll
             for (int i = 0; i < K; ++i) {
-                base[i] = zero_rec;
-                if (g + i < ntr)
-                    base[i] = uint32_t(xs_bytes) +
-                              (tree_node_off[tl.tree_begin + g + i] - uint32_t(tl.node_begin)) * 8u;
-                // keep the tree base opaque so the step computes base + child * 8 directly
-                // instead of re-associating it into the child index
-                if constexpr (DL == 64)
-                    asm("" : "+s"(base[i]));
+                base[i] = tree_base(g * K + i);
+                if constexpr (kUniform)
+                    asm("" : "+s"(base[i])); // opaque: keep base + offset as one add
                 else
                     asm("" : "+v"(base[i]));
-                addr[i] = base[i];
-                nd[i] = *reinterpret_cast<const uint2 *>(lds + addr[i]);
+                nd[i] = *reinterpret_cast<const uint2 *>(lds + base[i]);
             }
-            // Predicated walk: every lane steps until all lanes of the wave sit on leaves. The
-            // record read that shows a lane is at a leaf already holds the leaf's value. A walk
-            // ends within max_depth steps; the bound only guarantees termination.
-            for (int s = 0; s <= tl.max_depth; ++s) {
-                uint32_t fa[K];
-                bool internal = false;
+            // One predicated step from the feature addresses fa: read the feature, compare,
+            // child index + bit (the right child follows the left one), read that record.
+            uint32_t fa[K];
+            auto feature_addresses = [&]() {
 #pragma unroll
-                for (int i = 0; i < K; ++i) {
+                for (int i = 0; i < K; ++i)
                     fa[i] = and_or(nd[i].y, col_mask, lane_off);
-                    internal |= fa[i] >= kLeafCol;
-                }
-                if (!__any(internal))
-                    break;
+            };
+            auto step = [&]() {
+                uint32_t addr[K];
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
                     const float x = *reinterpret_cast<const float *>(lds + fa[i]);
-                    const uint32_t child =
-                        (nd[i].y >> treeens::kChildShift) + (x >= __uint_as_float(nd[i].x) ? 1u : 0u);
+                    uint32_t child;
+                    if constexpr (NARROW)
+                        child = narrow_child(nd[i].y, x, __uint_as_float(nd[i].x));
+                    else
+                        child = (nd[i].y >> treeens::kWideChildShift) +
+                                (x >= __uint_as_float(nd[i].x) ? 1u : 0u);
                     addr[i] = base[i] + child * 8u;
                 }
 #pragma unroll
                 for (int i = 0; i < K; ++i)
                     nd[i] = *reinterpret_cast<const uint2 *>(lds + addr[i]);
+            };
+            if (tl.complete_depth >= 0) {
+                // every path has the same length: no leaf test needed
+                for (int s = 0; s < tl.complete_depth; ++s) {
+                    feature_addresses();
+                    step();
+                }
+            } else {
+                // every lane steps until all lanes of the wave sit on leaves (a leaf's feature
+                // address is the NaN column, below kLeafCol); the record that shows a lane is
+                // at a leaf holds the leaf's value. Every path of a validated tree reaches a
+                // leaf within the tile's max_depth steps and leaves link to themselves, so the
+                // exit is always taken.
+                for (;;) {
+                    feature_addresses();
+                    bool internal = false;
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        internal |= fa[i] >= kLeafCol;
+                    if (!__any(internal))
+                        break;
+                    step();
+                }
             }
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 if constexpr (LEAVES) {
+                    // a leaf's link is its own position in the tree
                     const int64_t doc = doc0 + dl;
-                    if (g + i < ntr && doc < n_docs) {
-                        const int gt = tl.tree_begin + g + i;
-                        leaf_ids[doc * n_trees + tree_orig[gt]] =
-                            orig_id[tree_node_off[gt] + (addr[i] - base[i]) / 8u];
+                    const int t = g * K + i;
+                    if (t < ntr && doc < n_docs) {
+                        const int gt = tl.tree_begin + t;
+                        const uint32_t self = nd[i].y >> (NARROW ? 16 : treeens::kWideChildShift);
+                        leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
                     }
                 } else {
-                    acc += double(__uint_as_float(nd[i].x)); // the zero record adds 0.0
+                    acc += double(__uint_as_float(nd[i].x)); // idle slots read the zero record
                 }
             }
         }
@@ -234,23 +317,37 @@ __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
 }
 
 using ScoreFn = void (*)(const float *, int64_t, int32_t, int32_t, const uint2 *, const uint32_t *,
-                         const uint32_t *, const Tile *, int32_t, int32_t, int32_t, int32_t,
-                         double *, float *, int32_t *, const int32_t *, const int32_t *, int32_t);
+                         const Tile *, int32_t, int32_t, int32_t, int32_t, double *, float *,
+                         int32_t *, const int32_t *, const int32_t *, int32_t);
 
-template <int K, bool LEAVES>
-ScoreFn pick_dl(int dl) {
-    switch (dl) {
-    case 64: return score_kernel<64, K, LEAVES>;
-    case 32: return score_kernel<32, K, LEAVES>;
-    case 16: return score_kernel<16, K, LEAVES>;
-    case 8: return score_kernel<8, K, LEAVES>;
+template <int DL, bool HALF, bool NARROW, bool LEAVES>
+ScoreFn pick_k(int k) {
+    switch (k) {
+    case 1: return score_kernel<DL, 1, HALF, NARROW, LEAVES>;
+    case 2: return score_kernel<DL, 2, HALF, NARROW, LEAVES>;
+    case 4: return score_kernel<DL, 4, HALF, NARROW, LEAVES>;
+    default: return nullptr;
+    }
+}
+
+template <bool NARROW, bool LEAVES>
+ScoreFn pick_dl(const treeens::LdsPlan &p) {
+    if (p.lds_bytes == treeens::kLdsPerCu / 2) // two workgroups per CU: only 64-doc blocks fit
+        return p.docs_per_block == 64 ? pick_k<64, true, NARROW, LEAVES>(p.interleave) : nullptr;
+    switch (p.docs_per_block) {
+    case 64: return pick_k<64, false, NARROW, LEAVES>(p.interleave);
+    case 32: return pick_k<32, false, NARROW, LEAVES>(p.interleave);
+    case 16: return pick_k<16, false, NARROW, LEAVES>(p.interleave);
+    case 8: return pick_k<8, false, NARROW, LEAVES>(p.interleave);
     default: return nullptr;
     }
 }
 
 template <bool LEAVES>
-ScoreFn pick_kernel(int dl, int k) {
-    return k == 2 ? pick_dl<2, LEAVES>(dl) : k == 1 ? pick_dl<1, LEAVES>(dl) : nullptr;
+ScoreFn pick_kernel(const treeens::LdsPlan &p) {
+    if (p.lds_bytes != treeens::kLdsPerCu / 2 && p.lds_bytes != treeens::kLdsPerCu)
+        return nullptr;
+    return p.narrow ? pick_dl<true, LEAVES>(p) : pick_dl<false, LEAVES>(p);
 }
 
 } // namespace
@@ -363,7 +460,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     int level, splits;
     choose_split(h, n_blocks, &level, &splits);
-    ScoreFn fn = pick_kernel<LEAVES>(dl, h->plan.interleave);
+    ScoreFn fn = pick_kernel<LEAVES>(h->plan);
     if (!fn)
         return fail(TREE_ENS_E_ARG, "unsupported document block size");
     hipError_t e = hipSuccess;
@@ -379,7 +476,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     (void)hipGetLastError();
     hipLaunchKernelGGL(fn, dim3(unsigned(n_blocks), unsigned(splits)), dim3(kThreads), 0,
                        stream, X, n_docs, n_features, h->n_cols, h->d_nodes,
-                       h->d_tree_node_off, h->d_tree_depth, tiles, n_tiles, splits,
+                       h->d_tree_node_off, tiles, n_tiles, splits,
                        h->plan.xs_bytes, h->plan.tile_bytes, partials, scores, leaf_ids,
                        h->d_orig_id, h->d_tree_orig, h->n_trees);
     e = hipGetLastError();
