@@ -257,6 +257,7 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
                     step();
                 }
             }
+            float group_sum = 0.0f; // K leaf values: exact enough in float, one double add
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 if constexpr (LEAVES) {
@@ -269,9 +270,11 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
                         leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
                     }
                 } else {
-                    acc += double(__uint_as_float(nd[i].x)); // idle slots read the zero record
+                    group_sum += __uint_as_float(nd[i].x); // idle slots read the zero record
                 }
             }
+            if constexpr (!LEAVES)
+                acc += double(group_sum);
         }
     }
     if constexpr (!LEAVES) {
@@ -294,11 +297,23 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
     }
 }
 
-// One wave per document: lanes take the split partials in a fixed interleave, then a fixed
-// butterfly combines the lanes, so the sum's order (and its rounding) never changes.
+// Sum of the split partials of each document in a fixed order (so the rounding never
+// changes). Few splits: one thread per document, in split order. Many splits (small batches):
+// one wave per document, lanes interleave the splits, then a fixed butterfly.
+__global__ void reduce_partials_thread_kernel(const double *__restrict__ partials, int32_t n_splits,
+                                              int64_t n_docs, float *__restrict__ scores) {
+    const int64_t d = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (d < n_docs) {
+        double s = 0.0;
+        for (int k = 0; k < n_splits; ++k)
+            s += partials[int64_t(k) * n_docs + d];
+        scores[d] = float(s);
+    }
+}
+
 __global__ void __launch_bounds__(64)
-reduce_partials_kernel(const double *__restrict__ partials, int32_t n_splits, int64_t n_docs,
-                       float *__restrict__ scores) {
+reduce_partials_wave_kernel(const double *__restrict__ partials, int32_t n_splits, int64_t n_docs,
+                            float *__restrict__ scores) {
     const int64_t d = blockIdx.x;
     double s = 0.0;
     for (int k = threadIdx.x; k < n_splits; k += 64)
@@ -393,25 +408,39 @@ hipError_t upload(T **dst, const std::vector<T> &src) {
     return e;
 }
 
-// Split count and tiling level for a batch of n_blocks document blocks: enough workgroups to
-// fill every compute unit twice over, without cutting tiles finer than the finest level.
+// Split count and tiling level for a batch of n_blocks document blocks. Each (block, split)
+// workgroup walks a contiguous share of the tiles. The estimated makespan, in units of one
+// block walking all trees, is
+//     ceil(n_blocks * splits / resident workgroups) * (largest share + per-workgroup cost)
+//     + (splits > 1 ? cost of the partial-sum reduction : 0):
+// splitting fills the last round of workgroups (a batch of 1,563 blocks on 512 resident
+// workgroups would otherwise run a fourth round at 5% occupancy) and spreads small batches
+// over the whole GPU.
 void choose_split(const tree_ens *h, int64_t n_blocks, int *level, int *splits) {
+    constexpr double kItemCost = 0.2;    // staging, prologue and restaging of one workgroup (measured)
+    constexpr double kReduceCost = 0.05; // the second kernel
     const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
-    const int64_t target = int64_t(kNumCus) * wg_per_cu * 2;
+    const int64_t slots = int64_t(kNumCus) * wg_per_cu;
+    double best = 1e300;
     *level = 0;
     *splits = 1;
-    if (n_blocks >= target)
-        return;
-    const int64_t want = (target + n_blocks - 1) / n_blocks;
     for (int k = 0; k < treeens::kTileLevels; ++k) {
         const int nt = h->level_begin[k + 1] - h->level_begin[k];
-        *level = k;
-        *splits = int(std::min<int64_t>(want, nt));
-        if (nt >= want)
-            break;
+        for (int sp = 1; sp <= std::min(nt, 1024); ++sp) {
+            const int64_t rounds = (n_blocks * sp + slots - 1) / slots;
+            const double share = double((nt + sp - 1) / sp) / nt;
+            const double cost = double(rounds) * (share + kItemCost) + (sp > 1 ? kReduceCost : 0.0);
+            if (cost < best - 1e-9) {
+                best = cost;
+                *level = k;
+                *splits = sp;
+            }
+        }
     }
-    if (*splits < 1)
-        *splits = 1;
+#ifdef TREE_ENS_FORCE_SPLITS // measurement builds only
+    *level = 0;
+    *splits = std::min(TREE_ENS_FORCE_SPLITS, h->level_begin[1] - h->level_begin[0]);
+#endif
 }
 
 struct DeviceGuard {
@@ -481,8 +510,12 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                        h->d_orig_id, h->d_tree_orig, h->n_trees);
     e = hipGetLastError();
     if (e == hipSuccess && partials) {
-        hipLaunchKernelGGL(reduce_partials_kernel, dim3(unsigned(n_docs)), dim3(64), 0, stream,
-                           partials, splits, n_docs, scores);
+        if (splits <= 64)
+            hipLaunchKernelGGL(reduce_partials_thread_kernel, dim3(unsigned((n_docs + 255) / 256)),
+                               dim3(256), 0, stream, partials, splits, n_docs, scores);
+        else
+            hipLaunchKernelGGL(reduce_partials_wave_kernel, dim3(unsigned(n_docs)), dim3(64), 0,
+                               stream, partials, splits, n_docs, scores);
         e = hipGetLastError();
     }
     if (partials) {
