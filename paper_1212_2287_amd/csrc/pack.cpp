@@ -26,22 +26,25 @@ float strict_to_inclusive(float theta) {
 }
 
 // avg_tree_bytes: mean packed size of a tree, to pick how many trees a lane walks at once.
-LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes) {
+// elem_bytes: 4 for float features, 2 for codes.
+LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
     LdsPlan p{};
-    const int64_t cols = int64_t(n_cols) + 1; // + the NaN column the leaves read
+    p.elem_bytes = elem_bytes;
+    p.coded = elem_bytes == 2;
+    const int64_t cols = int64_t(n_cols) + 1; // + the NaN (or zero-code) column the leaves read
     for (int dl = 64; dl >= 8; dl /= 2) {
-        if (cols * dl * 4 <= kXsMaxBytes) {
+        if (cols * dl * elem_bytes <= kXsMaxBytes) {
             p.docs_per_block = dl;
             break;
         }
     }
     if (p.docs_per_block == 0)
         return p;
-    p.xs_bytes = int32_t(cols * p.docs_per_block * 4);
+    p.xs_bytes = int32_t(cols * p.docs_per_block * elem_bytes);
     const int reserve = kMetaBytes + 64; // tree-offset table, the all-zero record, slack
     // 16 waves per workgroup; two workgroups per CU when the document tile is small
     p.wg_threads = 1024;
-    p.lds_bytes = p.xs_bytes <= kTwoWgXsBytes ? kLdsPerCu / 2 : kLdsPerCu;
+    p.lds_bytes = (p.xs_bytes <= kTwoWgXsBytes && !p.coded) ? kLdsPerCu / 2 : kLdsPerCu;
     const int prefetch = p.lds_bytes == kLdsPerCu / 2 ? kPrefetchHalf : kPrefetchFull;
     p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve, prefetch * 1024 * 8) & ~15;
     // Interleave K trees per lane (latency hiding) only when a tile holds at least K rounds of
@@ -165,7 +168,42 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     }
 
     const int32_t n_cols = max_fid + 1;
-    LdsPlan plan = plan_lds(n_cols, n_trees > 0 ? 8.0 * double(n_nodes) / n_trees : 0.0);
+    const double avg_tree_bytes = n_trees > 0 ? 8.0 * double(n_nodes) / n_trees : 0.0;
+    LdsPlan plan = plan_lds(n_cols, avg_tree_bytes, 4);
+
+    // ---- coded features: per-feature sorted distinct thresholds -----------------------------
+    // Used when float features would leave fewer than 64 documents per block and every
+    // feature's thresholds fit one coding workgroup and 16-bit codes.
+    std::vector<std::vector<float>> thr_of;
+    // Coding pays when float documents leave too few per block for the model's trees: when a
+    // float tile cannot hold one tree for each walker, most walkers would idle.
+    bool coded = plan.docs_per_block > 0 && plan.docs_per_block < 64 &&
+                 avg_tree_bytes * (1024 / plan.docs_per_block) > plan.tile_bytes;
+#ifdef TREE_ENS_CODED // measurement builds only: force the choice
+    coded = TREE_ENS_CODED != 0;
+#endif
+    auto canon = [&](float th) {
+        float v = strict ? strict_to_inclusive(th) : th;
+        return v == 0.0f ? 0.0f : v; // fold -0.0 into +0.0 (equal under every comparison)
+    };
+    if (coded) {
+        thr_of.assign(size_t(n_cols), {});
+        for (int64_t i = 0; i < n_nodes && coded; i++) {
+            if (feature[i] < 0)
+                continue;
+            const float v = canon(threshold[i]);
+            if (!std::isnan(v))
+                thr_of[size_t(feature[i])].push_back(v);
+        }
+        for (auto &tv : thr_of) {
+            std::sort(tv.begin(), tv.end());
+            tv.erase(std::unique(tv.begin(), tv.end()), tv.end());
+            if (tv.size() > kMaxCode || tv.size() > size_t(kCodeTableFloats))
+                coded = false;
+        }
+        if (coded)
+            plan = plan_lds(n_cols, avg_tree_bytes, 2);
+    }
     if (plan.docs_per_block == 0) {
         err = "feature id " + std::to_string(max_fid) + " is beyond the LDS document-tile limit (" +
               std::to_string(kXsMaxBytes / (8 * 4) - 2) + ")";
@@ -235,10 +273,20 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             if (feature[a + i] >= 0) {
                 const float th = strict ? strict_to_inclusive(threshold[a + i]) : threshold[a + i];
                 r.thr_bits = float_bits(th);
-                const uint32_t col = uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) * 4u;
+                if (plan.coded) {
+                    const float v = canon(threshold[a + i]);
+                    const auto &tv = thr_of[size_t(feature[a + i])];
+                    r.thr_bits = std::isnan(v) ? 0xFFFFu
+                                               : uint32_t(std::lower_bound(tv.begin(), tv.end(), v) -
+                                                          tv.begin()) + 1u;
+                }
+                const uint32_t col = uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) *
+                                     uint32_t(plan.elem_bytes);
                 r.w = link(uint32_t(new_id[size_t(left[a + i])])) | col;
             } else {
                 r.thr_bits = float_bits(value[a + i]);
+                if (plan.coded && r.thr_bits == 0u)
+                    r.thr_bits = 0x80000000u; // +0.0 as -0.0: never 0, so the leaf stays put
                 r.w = link(uint32_t(ni));
             }
         }
@@ -282,6 +330,26 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
     p.level_begin[kTileLevels] = int32_t(p.tiles.size());
+
+    // ---- coded models: threshold table and coding chunks ------------------------------------
+    if (plan.coded) {
+        p.code_table_off.assign(size_t(n_cols) + 1, 0);
+        for (int32_t f = 0; f < n_cols; f++) {
+            p.code_table_off[size_t(f)] = uint32_t(p.code_table.size());
+            p.code_table.insert(p.code_table.end(), thr_of[size_t(f)].begin(), thr_of[size_t(f)].end());
+        }
+        p.code_table_off[size_t(n_cols)] = uint32_t(p.code_table.size());
+        int32_t fb = 0;
+        while (fb < n_cols) {
+            int32_t fe = fb;
+            while (fe < n_cols && fe - fb < kCodeChunkFeatures &&
+                   p.code_table_off[size_t(fe) + 1] - p.code_table_off[size_t(fb)] <= uint32_t(kCodeTableFloats))
+                fe++;
+            p.code_chunks.push_back(CodeChunk{fb, fe, int32_t(p.code_table_off[size_t(fb)]),
+                                              int32_t(p.code_table_off[size_t(fe)])});
+            fb = fe;
+        }
+    }
     out = std::move(p);
     return kOk;
 }

@@ -56,7 +56,26 @@ struct LdsPlan {
     int32_t lds_bytes;      // total dynamic LDS per workgroup
     int32_t interleave;     // trees each lane walks at once (K)
     int32_t narrow;         // 1: narrow record format (see NodeRec), 0: wide
+    int32_t coded;          // 1: documents are staged as 16-bit threshold codes (see below)
+    int32_t elem_bytes;     // bytes per staged feature value: 4 (float) or 2 (code)
 };
+
+// Coded features (exact). For each feature f let T_f be the model's distinct thresholds of f,
+// sorted (after the strict-rule nudge; -0.0 folded into +0.0; NaN thresholds left out), and
+// code_f(x) = |{t in T_f : x >= t}| (0 for a NaN x). Then x >= T_f[k] <=> code_f(x) >= k + 1,
+// so a node on threshold T_f[k] stores k + 1 and compares codes as unsigned integers; a node
+// whose threshold is NaN (never "right") stores 0xFFFF, above every code. A leaf keeps its
+// value's bits in the threshold slot, with +0.0 stored as -0.0 so the bits are never 0: the
+// leaves' code column holds 0, and 0 >= bits is false, so leaves still go "left" to themselves.
+// Coding halves the staged bytes per document; it is used when float features would not fit
+// 64 documents in the LDS document tile.
+struct CodeChunk {
+    int32_t f_begin, f_end;         // features [f_begin, f_end)
+    int32_t table_begin, table_end; // their thresholds in the concatenated table
+};
+constexpr int kCodeTableFloats = 16384;  // LDS thresholds per coding workgroup (64 KiB)
+constexpr int kCodeChunkFeatures = 256;  // features per coding workgroup at most
+constexpr uint32_t kMaxCode = 0xFFFEu;    // codes are 16-bit; 0xFFFF = "never right"
 
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950 LDS per compute unit
 constexpr int kMetaBytes = kMaxTileTrees * 4; // per-tile table of tree offsets in LDS
@@ -80,6 +99,10 @@ struct Packed {
     std::vector<int32_t> orig_id;        // [n_nodes] input tree-local id of packed node
     std::vector<Tile> tiles;             // all tiling levels, concatenated
     int32_t level_begin[kTileLevels + 1] = {};
+    // coded models only
+    std::vector<float> code_table;         // T_0, T_1, ... concatenated
+    std::vector<uint32_t> code_table_off;  // [n_cols + 1] start of T_f in code_table
+    std::vector<CodeChunk> code_chunks;    // features grouped for the coding kernel
 };
 
 // Status codes match the public header.

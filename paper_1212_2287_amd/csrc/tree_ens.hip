@@ -26,6 +26,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "pack.hpp"
@@ -77,17 +78,31 @@ __device__ __forceinline__ uint32_t narrow_child(uint32_t w, float x, float thr)
     return r;
 }
 
-template <int DL, int K, bool HALF, bool NARROW, bool LEAVES>
+// The same for coded documents: unsigned compare of 16-bit codes.
+__device__ __forceinline__ uint32_t narrow_child_coded(uint32_t w, uint32_t code, uint32_t q) {
+    uint32_t r;
+    asm("v_cmp_ge_u32 vcc, %1, %2\n\t"
+        "s_nop 1\n\t"
+        "v_addc_co_u32_sdwa %0, vcc, %3, 0, vcc dst_sel:DWORD dst_unused:UNUSED_PAD "
+        "src0_sel:WORD_1 src1_sel:DWORD"
+        : "=v"(r)
+        : "v"(code), "v"(q), "v"(w)
+        : "vcc");
+    return r;
+}
+
+template <int DL, int K, bool HALF, bool NARROW, bool CODED, bool LEAVES>
 __global__ void __launch_bounds__(kThreads, HALF ? 8 : 4) // min waves per SIMD: 2 or 1 workgroups per CU
-score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
+score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, int32_t n_cols,
              const uint2 *__restrict__ nodes, const uint32_t *__restrict__ tree_node_off,
              const Tile *__restrict__ tiles, int32_t n_tiles, int32_t n_splits, int32_t xs_bytes,
              int32_t tile_bytes, double *__restrict__ partials, float *__restrict__ scores,
              int32_t *__restrict__ leaf_ids, const int32_t *__restrict__ orig_id,
              const int32_t *__restrict__ tree_orig, int32_t n_trees) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
-    // HALF = half a CU's LDS, so that two workgroups share a CU. Layout:
-    //   [0, xs_bytes)                      document tile, [(n_cols + 1) x DL] floats
+    // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
+    // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
+    //   [0, xs_bytes)                      document tile, [(n_cols + 1) x DL] values
     //   [xs_bytes, +tile_bytes)            node records of the current tile
     //   [meta_off, +kMetaBytes)            tile-relative record offset of each tree of the tile
     //   zero_rec (8 bytes)                 all-zero record: a leaf of value 0 for idle slots
@@ -99,7 +114,9 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
     const uint32_t zero_rec = meta_off + uint32_t(treeens::kMetaBytes);
     uint32_t *meta = reinterpret_cast<uint32_t *>(lds + meta_off);
     uint2 *tn = reinterpret_cast<uint2 *>(lds + xs_bytes);
-    float *xs = reinterpret_cast<float *>(lds);
+    using Elem = std::conditional_t<CODED, uint16_t, float>;
+    const Elem *X = reinterpret_cast<const Elem *>(Xv);
+    Elem *xs = reinterpret_cast<Elem *>(lds);
 
     const int tid = threadIdx.x;
     const int nthr = kThreads;
@@ -108,10 +125,11 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
     // the group loop and the tree bases live in scalar registers
     const int walker = kUniform ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
     const int n_walkers = nthr / DL;
-    const uint32_t lane_off = uint32_t(dl) * 4u;
+    const uint32_t lane_off = uint32_t(dl) * uint32_t(sizeof(Elem));
     const uint32_t col_mask =
         __builtin_amdgcn_readfirstlane(NARROW ? treeens::kNarrowColMask : treeens::kWideColMask);
-    constexpr uint32_t kLeafCol = uint32_t(DL) * 4u; // column offsets below this are the NaN column
+    // column offsets below this are column 0 (NaN, or code 0), which only leaves name
+    constexpr uint32_t kLeafCol = uint32_t(DL) * uint32_t(sizeof(Elem));
     const int64_t doc0 = int64_t(blockIdx.x) * DL;
     const int split = blockIdx.y;
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
@@ -146,15 +164,16 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
         constexpr int kUnroll = 8;
         const int64_t doc = doc0 + dl;
         const bool live = doc < n_docs;
-        const float *row = X + (live ? doc : 0) * int64_t(n_features);
+        const Elem *row = X + (live ? doc : 0) * int64_t(n_features);
+        const Elem leaf_col = CODED ? Elem(0) : Elem(__builtin_nanf(""));
         for (int c0 = tid / DL; c0 <= n_cols; c0 += kColStep * kUnroll) {
-            float v[kUnroll];
+            Elem v[kUnroll];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int c = c0 + u * kColStep;
-                v[u] = __builtin_nanf("");
+                v[u] = leaf_col;
                 if (c > 0 && c <= n_cols)
-                    v[u] = live ? row[c - 1] : 0.0f;
+                    v[u] = live ? row[c - 1] : Elem(0);
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -221,13 +240,21 @@ score_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, in
                 uint32_t addr[K];
 #pragma unroll
                 for (int i = 0; i < K; ++i) {
-                    const float x = *reinterpret_cast<const float *>(lds + fa[i]);
                     uint32_t child;
-                    if constexpr (NARROW)
-                        child = narrow_child(nd[i].y, x, __uint_as_float(nd[i].x));
-                    else
-                        child = (nd[i].y >> treeens::kWideChildShift) +
-                                (x >= __uint_as_float(nd[i].x) ? 1u : 0u);
+                    if constexpr (CODED) {
+                        const uint32_t x = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
+                        if constexpr (NARROW)
+                            child = narrow_child_coded(nd[i].y, x, nd[i].x);
+                        else
+                            child = (nd[i].y >> treeens::kWideChildShift) + (x >= nd[i].x ? 1u : 0u);
+                    } else {
+                        const float x = *reinterpret_cast<const float *>(lds + fa[i]);
+                        if constexpr (NARROW)
+                            child = narrow_child(nd[i].y, x, __uint_as_float(nd[i].x));
+                        else
+                            child = (nd[i].y >> treeens::kWideChildShift) +
+                                    (x >= __uint_as_float(nd[i].x) ? 1u : 0u);
+                    }
                     addr[i] = base[i] + child * 8u;
                 }
 #pragma unroll
@@ -331,29 +358,73 @@ __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
         scores[d] = 0.0f;
 }
 
-using ScoreFn = void (*)(const float *, int64_t, int32_t, int32_t, const uint2 *, const uint32_t *,
+// Threshold codes of a block of documents for a chunk of features: code_f(x) is the number of
+// f's sorted distinct thresholds t with x >= t (upper-bound binary search over the chunk's
+// thresholds, staged in LDS; a NaN x compares false everywhere and gets 0). Output rows hold
+// n_cols 16-bit codes.
+constexpr int kCodeThreads = 1024;
+__global__ void __launch_bounds__(kCodeThreads)
+code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
+            int32_t docs_per_wg,
+            const float *__restrict__ table, const uint32_t *__restrict__ table_off,
+            const treeens::CodeChunk *__restrict__ chunks, uint16_t *__restrict__ codes) {
+    __shared__ float tab[treeens::kCodeTableFloats];
+    __shared__ uint32_t toff[treeens::kCodeChunkFeatures + 1];
+    const treeens::CodeChunk ch = chunks[blockIdx.y];
+    const int nf = ch.f_end - ch.f_begin;
+    for (int i = threadIdx.x; i < ch.table_end - ch.table_begin; i += kCodeThreads)
+        tab[i] = table[ch.table_begin + i];
+    for (int j = threadIdx.x; j <= nf; j += kCodeThreads)
+        toff[j] = table_off[ch.f_begin + j] - uint32_t(ch.table_begin);
+    __syncthreads();
+    const int64_t d0 = int64_t(blockIdx.x) * docs_per_wg;
+    const int n = int(min<int64_t>(docs_per_wg, n_docs - d0)) * nf;
+    for (int e = threadIdx.x; e < n; e += kCodeThreads) {
+        const int d = e / nf;
+        const int j = e - d * nf;
+        const int64_t doc = d0 + d;
+        const float x = X[doc * n_features + ch.f_begin + j];
+        const uint32_t first = toff[j];
+        uint32_t lo = first, hi = toff[j + 1];
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (x >= tab[mid])
+                lo = mid + 1;
+            else
+                hi = mid;
+        }
+        codes[doc * n_cols + ch.f_begin + j] = uint16_t(lo - first);
+    }
+}
+
+using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *, const uint32_t *,
                          const Tile *, int32_t, int32_t, int32_t, int32_t, double *, float *,
                          int32_t *, const int32_t *, const int32_t *, int32_t);
 
-template <int DL, bool HALF, bool NARROW, bool LEAVES>
+template <int DL, bool HALF, bool NARROW, bool CODED, bool LEAVES>
 ScoreFn pick_k(int k) {
     switch (k) {
-    case 1: return score_kernel<DL, 1, HALF, NARROW, LEAVES>;
-    case 2: return score_kernel<DL, 2, HALF, NARROW, LEAVES>;
-    case 4: return score_kernel<DL, 4, HALF, NARROW, LEAVES>;
+    case 1: return score_kernel<DL, 1, HALF, NARROW, CODED, LEAVES>;
+    case 2: return score_kernel<DL, 2, HALF, NARROW, CODED, LEAVES>;
+    case 4: return score_kernel<DL, 4, HALF, NARROW, CODED, LEAVES>;
     default: return nullptr;
     }
 }
 
-template <bool NARROW, bool LEAVES>
+template <bool NARROW, bool CODED, bool LEAVES>
 ScoreFn pick_dl(const treeens::LdsPlan &p) {
-    if (p.lds_bytes == treeens::kLdsPerCu / 2) // two workgroups per CU: only 64-doc blocks fit
-        return p.docs_per_block == 64 ? pick_k<64, true, NARROW, LEAVES>(p.interleave) : nullptr;
+    if (p.lds_bytes == treeens::kLdsPerCu / 2) {
+        // two workgroups per CU: only small float tiles of 64-document blocks
+        if constexpr (CODED)
+            return nullptr;
+        else
+            return p.docs_per_block == 64 ? pick_k<64, true, NARROW, false, LEAVES>(p.interleave) : nullptr;
+    }
     switch (p.docs_per_block) {
-    case 64: return pick_k<64, false, NARROW, LEAVES>(p.interleave);
-    case 32: return pick_k<32, false, NARROW, LEAVES>(p.interleave);
-    case 16: return pick_k<16, false, NARROW, LEAVES>(p.interleave);
-    case 8: return pick_k<8, false, NARROW, LEAVES>(p.interleave);
+    case 64: return pick_k<64, false, NARROW, CODED, LEAVES>(p.interleave);
+    case 32: return pick_k<32, false, NARROW, CODED, LEAVES>(p.interleave);
+    case 16: return pick_k<16, false, NARROW, CODED, LEAVES>(p.interleave);
+    case 8: return pick_k<8, false, NARROW, CODED, LEAVES>(p.interleave);
     default: return nullptr;
     }
 }
@@ -362,7 +433,9 @@ template <bool LEAVES>
 ScoreFn pick_kernel(const treeens::LdsPlan &p) {
     if (p.lds_bytes != treeens::kLdsPerCu / 2 && p.lds_bytes != treeens::kLdsPerCu)
         return nullptr;
-    return p.narrow ? pick_dl<true, LEAVES>(p) : pick_dl<false, LEAVES>(p);
+    if (p.coded)
+        return p.narrow ? pick_dl<true, true, LEAVES>(p) : pick_dl<false, true, LEAVES>(p);
+    return p.narrow ? pick_dl<true, false, LEAVES>(p) : pick_dl<false, false, LEAVES>(p);
 }
 
 } // namespace
@@ -384,6 +457,11 @@ struct tree_ens {
     int32_t *d_tree_orig = nullptr;
     int32_t *d_orig_id = nullptr;
     Tile *d_tiles = nullptr;
+    // coded models
+    float *d_code_table = nullptr;
+    uint32_t *d_code_table_off = nullptr;
+    treeens::CodeChunk *d_code_chunks = nullptr;
+    int32_t n_code_chunks = 0;
 };
 
 namespace {
@@ -395,6 +473,9 @@ void free_device(tree_ens *h) {
     (void)hipFree(h->d_tree_orig);
     (void)hipFree(h->d_orig_id);
     (void)hipFree(h->d_tiles);
+    (void)hipFree(h->d_code_table);
+    (void)hipFree(h->d_code_table_off);
+    (void)hipFree(h->d_code_chunks);
 }
 
 template <typename T>
@@ -503,8 +584,33 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const Tile *tiles = h->d_tiles + h->level_begin[level];
     const int n_tiles = h->level_begin[level + 1] - h->level_begin[level];
     (void)hipGetLastError();
+    // coded models: one pass turns the float features into 16-bit threshold codes
+    const void *docs = X;
+    int32_t row_stride = n_features;
+    uint16_t *codes = nullptr;
+    if (h->plan.coded) {
+        e = hipMallocAsync(reinterpret_cast<void **>(&codes),
+                           size_t(n_docs) * size_t(h->n_cols) * sizeof(uint16_t), stream);
+        if (e != hipSuccess) {
+            if (partials)
+                (void)hipFreeAsync(partials, stream);
+            return hip_fail(e, "hipMallocAsync(codes)");
+        }
+        // documents per coding workgroup: enough workgroups to fill the GPU twice over, but
+        // each one long enough to pay for loading its chunk's thresholds into LDS
+        int64_t per_wg = 256;
+        while (per_wg < 4096 && ((n_docs + per_wg - 1) / per_wg) * h->n_code_chunks > 4 * kNumCus)
+            per_wg *= 2;
+        hipLaunchKernelGGL(code_kernel, dim3(unsigned((n_docs + per_wg - 1) / per_wg),
+                                             unsigned(h->n_code_chunks)),
+                           dim3(kCodeThreads), 0, stream, X, n_docs, n_features, h->n_cols,
+                           int32_t(per_wg), h->d_code_table, h->d_code_table_off,
+                           h->d_code_chunks, codes);
+        docs = codes;
+        row_stride = h->n_cols;
+    }
     hipLaunchKernelGGL(fn, dim3(unsigned(n_blocks), unsigned(splits)), dim3(kThreads), 0,
-                       stream, X, n_docs, n_features, h->n_cols, h->d_nodes,
+                       stream, docs, n_docs, row_stride, h->n_cols, h->d_nodes,
                        h->d_tree_node_off, tiles, n_tiles, splits,
                        h->plan.xs_bytes, h->plan.tile_bytes, partials, scores, leaf_ids,
                        h->d_orig_id, h->d_tree_orig, h->n_trees);
@@ -520,6 +626,11 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     }
     if (partials) {
         hipError_t e2 = hipFreeAsync(partials, stream);
+        if (e == hipSuccess)
+            e = e2;
+    }
+    if (codes) {
+        hipError_t e2 = hipFreeAsync(codes, stream);
         if (e == hipSuccess)
             e = e2;
     }
@@ -576,6 +687,14 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
         e = upload(&h->d_orig_id, p.orig_id);
     if (e == hipSuccess)
         e = upload(&h->d_tiles, p.tiles);
+    if (e == hipSuccess && p.plan.coded) {
+        e = upload(&h->d_code_table, p.code_table);
+        if (e == hipSuccess)
+            e = upload(&h->d_code_table_off, p.code_table_off);
+        if (e == hipSuccess)
+            e = upload(&h->d_code_chunks, p.code_chunks);
+        h->n_code_chunks = int32_t(p.code_chunks.size());
+    }
     if (e != hipSuccess) {
         free_device(h);
         delete h;

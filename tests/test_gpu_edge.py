@@ -144,3 +144,48 @@ def test_streams_and_errors(T):
         assert ei.value.code == T.TREE_ENS_E_SHAPE
         info = m.info()
         assert info["min_features"] <= 136 and info["n_trees"] == 10
+
+
+@pytest.mark.parametrize("rule", [0, 1])
+def test_wide_features_coded(T, rule):
+    # 520 features: float documents would not fit 64 per LDS block, so the model is coded
+    # (16-bit threshold ranks). Ties, signed zeros, infinities, subnormals and NaN features
+    # must route exactly as the float comparison does.
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 1.0, np.inf, -np.inf, 1e-45, -1e-45, 3e-39, 7.0], np.float32)
+    F = 520
+    for seed in range(4):
+        ens = W.random_ensemble(100 + seed, n_trees=60, n_features=F, min_leaves=1, max_leaves=40,
+                                thr_values=pool if seed % 2 else None)
+        fe = ens.feature.copy()
+        fe[(fe >= 0) & (np.arange(fe.shape[0]) % 7 == 0)] = F - 1  # some splits on the last feature
+        ens = W.Ensemble(ens.tree_offsets, fe, ens.threshold, ens.left, ens.right, ens.value, F)
+        X = W.random_docs(100 + seed, 700, F, values=np.concatenate([pool, [np.nan]]).astype(np.float32)
+                          if seed % 2 else None)
+        s, ids = _gpu(T, ens, X, flags=rule)
+        ref, ref_ids, _ = oracle.score(ens, X, rule=rule)
+        assert_leaves_equal(ids, ref_ids, f"seed {seed}")
+        assert_scores_close(s, ref, f"seed {seed}")
+        # a leaf value of exactly +0.0 must still be summed correctly (stored as -0.0 when coded)
+        assert np.isfinite(s).all() or np.isnan(X).any()
+
+
+def test_wide_features_float_fallback(T):
+    # one feature carries more distinct thresholds than a coding workgroup holds, so the model
+    # keeps float documents (32 per block) instead of codes
+    F = 450
+    n = 17_000
+    rng = np.random.default_rng(7)
+    thr = np.sort(rng.random(n, dtype=np.float32))
+    fe = np.tile(np.array([F - 1, -1, -1], np.int32), n)
+    th = np.zeros(3 * n, np.float32)
+    th[0::3] = thr
+    le = np.tile(np.array([1, -1, -1], np.int32), n)
+    ri = np.tile(np.array([2, -1, -1], np.int32), n)
+    va = rng.integers(-8, 8, size=3 * n).astype(np.float32) / 8
+    ens = W.Ensemble(np.arange(n + 1, dtype=np.int64) * 3, fe, th, le, ri, va, F)
+    X = W.random_docs(8, 300, F)
+    X[:20, F - 1] = thr[:20]  # exact ties
+    s, ids = _gpu(T, ens, X)
+    ref, ref_ids, _ = oracle.score(ens, X)
+    assert_leaves_equal(ids, ref_ids)
+    assert_scores_close(s, ref)
