@@ -310,10 +310,10 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         red[walker * DL + dl] = acc;
         __syncthreads();
         if (walker == 0) {
+            const int64_t doc = doc0 + dl;
             double sum = 0.0;
             for (int w = 0; w < n_walkers; ++w)
                 sum += red[w * DL + dl];
-            const int64_t doc = doc0 + dl;
             if (doc < n_docs) {
                 if (n_splits == 1)
                     scores[doc] = float(sum);
@@ -462,7 +462,19 @@ struct tree_ens {
     uint32_t *d_code_table_off = nullptr;
     treeens::CodeChunk *d_code_chunks = nullptr;
     int32_t n_code_chunks = 0;
+    // Small batches: partial sums of the tile splits, reused by every call (no allocation per
+    // call). Calls from different streams are ordered with an event, so they never share the
+    // scratch at the same time.
+    double *d_scratch = nullptr;
+    hipEvent_t scratch_done = nullptr;
+    mutable std::mutex scratch_mu;
+    mutable hipStream_t scratch_stream = nullptr;
+    mutable bool scratch_used = false;
 };
+
+namespace {
+constexpr size_t kScratchDoubles = size_t(1) << 17; // 1 MiB of split partials
+} // namespace
 
 namespace {
 
@@ -476,6 +488,9 @@ void free_device(tree_ens *h) {
     (void)hipFree(h->d_code_table);
     (void)hipFree(h->d_code_table_off);
     (void)hipFree(h->d_code_chunks);
+    (void)hipFree(h->d_scratch);
+    if (h->scratch_done)
+        (void)hipEventDestroy(h->scratch_done);
 }
 
 template <typename T>
@@ -575,11 +590,24 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         return fail(TREE_ENS_E_ARG, "unsupported document block size");
     hipError_t e = hipSuccess;
     double *partials = nullptr;
+    bool own_scratch = false; // partials live in the handle's scratch
+    std::unique_lock<std::mutex> scratch_lock;
     if (!LEAVES && splits > 1) {
-        e = hipMallocAsync(reinterpret_cast<void **>(&partials),
-                           size_t(splits) * size_t(n_docs) * sizeof(double), stream);
-        if (e != hipSuccess)
-            return hip_fail(e, "hipMallocAsync(partials)");
+        if (size_t(splits) * size_t(n_docs) <= kScratchDoubles) {
+            scratch_lock = std::unique_lock<std::mutex>(h->scratch_mu);
+            if (h->scratch_used && h->scratch_stream != stream) {
+                e = hipStreamWaitEvent(stream, h->scratch_done, 0);
+                if (e != hipSuccess)
+                    return hip_fail(e, "hipStreamWaitEvent");
+            }
+            partials = h->d_scratch;
+            own_scratch = true;
+        } else {
+            e = hipMallocAsync(reinterpret_cast<void **>(&partials),
+                               size_t(splits) * size_t(n_docs) * sizeof(double), stream);
+            if (e != hipSuccess)
+                return hip_fail(e, "hipMallocAsync(partials)");
+        }
     }
     const Tile *tiles = h->d_tiles + h->level_begin[level];
     const int n_tiles = h->level_begin[level + 1] - h->level_begin[level];
@@ -624,7 +652,13 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                                stream, partials, splits, n_docs, scores);
         e = hipGetLastError();
     }
-    if (partials) {
+    if (own_scratch) {
+        // the next call from another stream waits for this one's reduction
+        if (e == hipSuccess)
+            e = hipEventRecord(h->scratch_done, stream);
+        h->scratch_stream = stream;
+        h->scratch_used = true;
+    } else if (partials) {
         hipError_t e2 = hipFreeAsync(partials, stream);
         if (e == hipSuccess)
             e = e2;
@@ -687,6 +721,10 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
         e = upload(&h->d_orig_id, p.orig_id);
     if (e == hipSuccess)
         e = upload(&h->d_tiles, p.tiles);
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&h->d_scratch), kScratchDoubles * sizeof(double));
+    if (e == hipSuccess)
+        e = hipEventCreateWithFlags(&h->scratch_done, hipEventDisableTiming);
     if (e == hipSuccess && p.plan.coded) {
         e = upload(&h->d_code_table, p.code_table);
         if (e == hipSuccess)
