@@ -41,12 +41,13 @@ LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
     if (p.docs_per_block == 0)
         return p;
     p.xs_bytes = int32_t(cols * p.docs_per_block * elem_bytes);
-    const int reserve = kMetaBytes + 64; // tree-offset table, the all-zero record, slack
+    const int reserve = 64; // the all-zero record, slack
     // 16 waves per workgroup; two workgroups per CU when the document tile is small
     p.wg_threads = 1024;
     p.lds_bytes = (p.xs_bytes <= kTwoWgXsBytes && !p.coded) ? kLdsPerCu / 2 : kLdsPerCu;
     const int prefetch = p.lds_bytes == kLdsPerCu / 2 ? kPrefetchHalf : kPrefetchFull;
     p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve, prefetch * 1024 * 8) & ~15;
+    p.zero_rec = p.xs_bytes + p.tile_bytes;
     // Interleave K trees per lane (latency hiding) only when a tile holds at least K rounds of
     // walker groups; otherwise most walkers would sit idle.
     const double fit = avg_tree_bytes > 0 ? p.tile_bytes / avg_tree_bytes : 1e9;
@@ -209,11 +210,14 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
               std::to_string(kXsMaxBytes / (8 * 4) - 2) + ")";
         return kErrModel;
     }
-    const int64_t max_nodes_per_tree = plan.tile_bytes / int64_t(sizeof(NodeRec));
+    // a one-tree tile holds the fixed header words and the root copies (padded to K records)
+    const int64_t header1 = kHeaderFixedWords / 2 + plan.interleave;
+    const int64_t max_nodes_per_tree = plan.tile_bytes / int64_t(sizeof(NodeRec)) - header1;
     int64_t largest_tree = 0;
     for (int32_t t = 0; t < n_trees; t++)
         largest_tree = std::max<int64_t>(largest_tree, tree_offsets[t + 1] - tree_offsets[t]);
-    // the narrow format needs column offsets below 64 KiB and child indices below 2^16
+    // the narrow format needs column offsets below 64 KiB and links below 2^16 (absolute LDS
+    // record indices are below 160 KiB / 8 = 20480; tree-relative ones below the tree's size)
     plan.narrow = (plan.xs_bytes <= 65536 && largest_tree <= kNarrowMaxTreeNodes) ? 1 : 0;
     for (int32_t t = 0; t < n_trees; t++) {
         const int64_t n = tree_offsets[t + 1] - tree_offsets[t];
@@ -296,22 +300,25 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     p.tree_node_off[size_t(n_trees)] = uint32_t(p.nodes.size());
 
     // ---- pass 3: tilings at budget / 2^k -------------------------------------------------
-    // A tile is a run of whole trees within the byte budget. When more than one round of
-    // walker groups fits, the run is cut to a whole number of rounds (walkers x interleave
-    // trees), so that statically assigned groups finish together.
-    const int32_t round = (1024 / plan.docs_per_block) * plan.interleave;
+    // A tile is a run of whole trees whose image (header + records) fits the byte budget. When
+    // more than one round of walker groups fits, the run is cut to a whole number of rounds
+    // (walkers x interleave trees), so that statically assigned groups finish together.
+    const int32_t K = plan.interleave;
+    const int32_t round = (1024 / plan.docs_per_block) * K;
+    // header records of a tile of n trees: fixed words + root copies padded to K
+    auto header_recs = [&](int32_t n) { return kHeaderFixedWords / 2 + (n + K - 1) / K * K; };
     for (int k = 0; k < kTileLevels; k++) {
         p.level_begin[k] = int32_t(p.tiles.size());
-        const int64_t budget = std::max<int64_t>(plan.tile_bytes >> k, 1);
+        const int64_t budget = std::max<int64_t>(plan.tile_bytes >> k, 16);
         int32_t tb = 0;
         while (tb < n_trees) {
             int32_t fit = 0;
-            for (int64_t bytes = 0; tb + fit < n_trees && fit < kMaxTileTrees; fit++) {
+            for (int64_t recs = 0; tb + fit < n_trees && fit < kMaxTileTrees; fit++) {
                 const int64_t nn = int64_t(p.tree_node_off[size_t(tb + fit) + 1] -
                                            p.tree_node_off[size_t(tb + fit)]);
-                if (fit > 0 && bytes + nn * 8 > budget)
+                if (fit > 0 && (header_recs(fit + 1) + recs + nn) * 8 > budget)
                     break;
-                bytes += nn * 8;
+                recs += nn;
             }
             const int32_t limit = (fit > round && tb + fit < n_trees) ? fit / round * round : fit;
             int32_t te = tb;
@@ -330,6 +337,58 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
     p.level_begin[kTileLevels] = int32_t(p.tiles.size());
+
+    // ---- pass 4: tile images --------------------------------------------------------------
+    // Records keep their column offsets; links become absolute LDS record indices: the slot
+    // starts right after the document tile, the records right after the header.
+    const int shift = plan.narrow ? 16 : kWideChildShift;
+    const uint32_t col_mask = plan.narrow ? kNarrowColMask : kWideColMask;
+    const uint32_t zero_addr = uint32_t(plan.zero_rec);
+    p.tile_recs.resize(p.tiles.size());
+    for (size_t i = 0; i < p.tiles.size(); i++) {
+        const Tile &tl = p.tiles[i];
+        p.tile_recs[i] = uint32_t(header_recs(tl.tree_end - tl.tree_begin)) +
+                         (p.tree_node_off[size_t(tl.tree_end)] - uint32_t(tl.node_begin));
+    }
+    for (int k = 0; k < kTileLevels; k++) {
+        uint32_t slot = 2;
+        for (int32_t i = p.level_begin[k]; i < p.level_begin[k + 1]; i++)
+            slot = std::max(slot, p.tile_recs[size_t(i)]);
+        p.level_slot_recs[k] = int32_t(slot);
+        p.level_image_off[k] = int64_t(p.images.size());
+        const int32_t n_level = p.level_begin[k + 1] - p.level_begin[k];
+        p.images.resize(p.images.size() + size_t(n_level) * slot, NodeRec{0u, 0u});
+        for (int32_t i = 0; i < n_level; i++) {
+            const Tile &tl = p.tiles[size_t(p.level_begin[k] + i)];
+            NodeRec *img = p.images.data() + p.level_image_off[k] + int64_t(i) * slot;
+            const int32_t ntr = tl.tree_end - tl.tree_begin;
+            const int32_t hrecs = header_recs(ntr);
+            const uint32_t rec0 = uint32_t(plan.xs_bytes / 8 + hrecs); // LDS index of record 0
+            img[0] = NodeRec{uint32_t(ntr), uint32_t(tl.complete_depth)};
+            img[1] = NodeRec{uint32_t(tl.tree_begin),
+                             i + 1 < n_level ? p.tile_recs[size_t(p.level_begin[k] + i + 1)] : 0u};
+            const NodeRec zero_leaf{plan.coded ? 0x80000000u : 0u, (zero_addr / 8u) << shift};
+            for (int32_t t = 0; t < hrecs - kHeaderFixedWords / 2; t++) {
+                NodeRec r = zero_leaf;
+                if (t < ntr) {
+                    const uint32_t first = p.tree_node_off[size_t(tl.tree_begin + t)];
+                    const uint32_t tree_rec = rec0 + first - uint32_t(tl.node_begin);
+                    r = p.nodes[first];
+                    r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                }
+                img[kHeaderFixedWords / 2 + t] = r;
+            }
+            for (int32_t t = tl.tree_begin; t < tl.tree_end; t++) {
+                const uint32_t first = p.tree_node_off[size_t(t)];
+                const uint32_t tree_rec = rec0 + first - uint32_t(tl.node_begin);
+                for (uint32_t n = first; n < p.tree_node_off[size_t(t) + 1]; n++) {
+                    NodeRec r = p.nodes[n];
+                    r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                    img[hrecs + int64_t(n - uint32_t(tl.node_begin))] = r;
+                }
+            }
+        }
+    }
 
     // ---- coded models: threshold table and coding chunks ------------------------------------
     if (plan.coded) {

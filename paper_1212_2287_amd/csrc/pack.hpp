@@ -17,15 +17,18 @@ namespace treeens {
 //   internal node: thr = threshold (nudged to the next float up under the strict rule)
 //   leaf:          thr = leaf value
 // w packs the feature column and the child link in one of two formats:
-//   narrow: w = (left child index << 16) | column byte offset             (column < 64 KiB)
-//   wide:   w = (left child index << kWideChildShift) | column byte offset (column < 128 KiB)
-// The child link is tree-relative; the right child follows the left one. A leaf links to
-// itself and has column offset 0.
-// The column byte offset of feature f is (f + 1) * docs_per_block * 4: the offset of f's column
-// in the staged document tile, so a lane's feature address is (w & column mask) | (lane * 4).
-// Column 0 of the tile holds NaN for every document, so a leaf compares a NaN with its value,
-// gets "left" and its link is itself: leaves absorb any further steps, and a lane is at a leaf
-// exactly when its record's column offset is 0.
+//   narrow: w = (left child link << 16) | column byte offset             (column < 64 KiB)
+//   wide:   w = (left child link << kWideChildShift) | column byte offset (column < 128 KiB)
+// In `nodes` the link is tree-relative (the node's index in its tree). In the tile images the
+// kernels walk, it is the child's absolute LDS record index (LDS byte address / 8), so a step
+// needs no per-tree base. The right child follows the left one. A leaf links to itself and has
+// column offset 0.
+// The column byte offset of feature f is (f + 1) * docs_per_block * elem_bytes: the offset of
+// f's column in the staged document tile, so a lane's feature address is
+// (w & column mask) | (lane * elem_bytes).
+// Column 0 of the tile holds NaN (or code 0) for every document, so a leaf compares it with its
+// value, gets "left" and its link is itself: leaves absorb any further steps, and a lane is at a
+// leaf exactly when its record's column offset is 0.
 struct NodeRec {
     uint32_t thr_bits;
     uint32_t w;
@@ -41,17 +44,32 @@ constexpr int kNarrowMaxTreeNodes = 1 << 16;                    // 16-bit child 
 struct Tile {
     int32_t tree_begin;
     int32_t tree_end;
-    int32_t max_depth;      // deepest tree in the run: bounds the walk's trip count
+    int32_t max_depth;      // deepest tree in the run
     int32_t node_begin;     // packed node offset of tree_begin
     int32_t complete_depth; // d if every tree of the run is complete of depth d, else -1
 };
-constexpr int kMaxTileTrees = 1024; // one LDS offset slot per tree of a tile
+constexpr int kMaxTileTrees = 1024;
+
+// Tile image: what one tile's LDS slot holds, laid out in device memory exactly as it is
+// copied (records of 8 bytes):
+//   word 0     number of trees n in the tile
+//   word 1     complete depth d if every tree is complete of depth d, else -1 (as int32)
+//   word 2     packed index of the tile's first tree
+//   word 3     records to copy for the next tile of the same tiling (0 after the last one)
+//   records 2.. a copy of each tree's root record, padded up to a multiple of the interleave K
+//              with the all-zero self-linked leaf (value 0), so a walker reads its K roots with
+//              one or two broadcast reads
+//   then the node records of the n trees, child links as absolute LDS record indices.
+// Images of one tiling sit at a fixed stride (the largest image of that tiling), so the
+// kernel locates tile t without a table.
+constexpr int kHeaderFixedWords = 4;
 
 // Launch plan fixed at create time from the model's feature range.
 struct LdsPlan {
     int32_t docs_per_block; // documents a workgroup stages (power of two, 8..64)
     int32_t xs_bytes;       // staged document tile: (n_cols + 1) columns x docs_per_block floats
-    int32_t tile_bytes;     // LDS bytes for node records of one tile
+    int32_t tile_bytes;     // LDS bytes of a tile slot (header + node records)
+    int32_t zero_rec;       // LDS byte address of the all-zero self-linked leaf (after the slot)
     int32_t wg_threads;     // workgroup size
     int32_t lds_bytes;      // total dynamic LDS per workgroup
     int32_t interleave;     // trees each lane walks at once (K)
@@ -78,7 +96,6 @@ constexpr int kCodeChunkFeatures = 256;  // features per coding workgroup at mos
 constexpr uint32_t kMaxCode = 0xFFFEu;    // codes are 16-bit; 0xFFFF = "never right"
 
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950 LDS per compute unit
-constexpr int kMetaBytes = kMaxTileTrees * 4; // per-tile table of tree offsets in LDS
 // The kernels prefetch a whole tile into registers (1,024 threads x kPrefetch records): at most
 // 6 records per thread when two workgroups share a CU (64 VGPRs each), 16 when one owns it.
 constexpr int kPrefetchHalf = 6;
@@ -99,6 +116,11 @@ struct Packed {
     std::vector<int32_t> orig_id;        // [n_nodes] input tree-local id of packed node
     std::vector<Tile> tiles;             // all tiling levels, concatenated
     int32_t level_begin[kTileLevels + 1] = {};
+    // tile images (see above), all tilings concatenated
+    std::vector<NodeRec> images;
+    int64_t level_image_off[kTileLevels] = {}; // first record of each tiling's images
+    int32_t level_slot_recs[kTileLevels] = {}; // image stride of each tiling, in records
+    std::vector<uint32_t> tile_recs;           // [tiles] records to copy for each tile
     // coded models only
     std::vector<float> code_table;         // T_0, T_1, ... concatenated
     std::vector<uint32_t> code_table_off;  // [n_cols + 1] start of T_f in code_table

@@ -34,7 +34,6 @@
 
 using treeens::NodeRec;
 using treeens::Packed;
-using treeens::Tile;
 
 namespace {
 
@@ -50,6 +49,8 @@ int hip_fail(hipError_t e, const char *what) {
 }
 
 constexpr int kNumCus = 256;
+// s_waitcnt immediate for gfx9: vmcnt(0), expcnt and lgkmcnt left at their maxima (no wait)
+constexpr int kWaitVmcnt0 = 0x0F70;
 constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves)
 
 // ------------------------------------------------------------------------------------------
@@ -63,6 +64,18 @@ __device__ __forceinline__ uint32_t and_or(uint32_t w, uint32_t mask, uint32_t b
     asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(w), "s"(mask), "v"(b));
     return r;
 }
+// One 8-byte node record from LDS, as one ds_read_b64, kept as one 64-bit value (threshold or
+// leaf value in the low half, w in the high half) so that the pair stays in one register pair. A
+// relaxed atomic load cannot be split: plain loads of the record get split by the compiler into
+// two 4-byte reads (the threshold half sunk past the wave-wide leaf test), doubling the LDS
+// reads per step.
+__device__ __forceinline__ uint64_t read_record(const unsigned char *p) {
+    return __hip_atomic_load(reinterpret_cast<const uint64_t *>(p), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ uint32_t rec_thr(uint64_t r) { return uint32_t(r); }
+__device__ __forceinline__ uint32_t rec_w(uint64_t r) { return uint32_t(r >> 32); }
+
 // Child index of a narrow record plus the comparison bit, in two VALU ops: the compare writes
 // VCC and an SDWA add-with-carry adds it to the high half-word of w. The s_nop covers the
 // VALU-writes-VCC / VALU-reads-carry hazard (two wait states, as the compiler itself emits).
@@ -94,26 +107,25 @@ __device__ __forceinline__ uint32_t narrow_child_coded(uint32_t w, uint32_t code
 template <int DL, int K, bool HALF, bool NARROW, bool CODED, bool LEAVES>
 __global__ void __launch_bounds__(kThreads, HALF ? 8 : 4) // min waves per SIMD: 2 or 1 workgroups per CU
 score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, int32_t n_cols,
-             const uint2 *__restrict__ nodes, const uint32_t *__restrict__ tree_node_off,
-             const Tile *__restrict__ tiles, int32_t n_tiles, int32_t n_splits, int32_t xs_bytes,
-             int32_t tile_bytes, double *__restrict__ partials, float *__restrict__ scores,
-             int32_t *__restrict__ leaf_ids, const int32_t *__restrict__ orig_id,
+             const uint2 *__restrict__ images, int32_t slot_recs,
+             const uint32_t *__restrict__ tile_recs, int32_t n_tiles, int32_t head_blocks,
+             int32_t tail_splits,
+             int32_t xs_bytes, int32_t zero_rec, double *__restrict__ partials,
+             float *__restrict__ scores, int32_t *__restrict__ leaf_ids,
+             const int32_t *__restrict__ orig_id, const uint32_t *__restrict__ tree_node_off,
              const int32_t *__restrict__ tree_orig, int32_t n_trees) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
-    //   [0, xs_bytes)                      document tile, [(n_cols + 1) x DL] values
-    //   [xs_bytes, +tile_bytes)            node records of the current tile
-    //   [meta_off, +kMetaBytes)            tile-relative record offset of each tree of the tile
-    //   zero_rec (8 bytes)                 all-zero record: a leaf of value 0 for idle slots
+    //   [0, xs_bytes)            document tile, [(n_cols + 1) x DL] values
+    //   [xs_bytes, zero_rec)     tile slot: the current tile image (header, then node records)
+    //   zero_rec (8 bytes)       all-zero self-linked leaf of value 0, for idle walker slots
     constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 : treeens::kLdsPerCu;
     __shared__ __align__(16) unsigned char lds[kLds];
     constexpr int kPre = HALF ? treeens::kPrefetchHalf : treeens::kPrefetchFull; // records per thread
-    constexpr bool kUniform = DL == 64; // a walker is a whole wave: tree bases are scalar
-    const uint32_t meta_off = uint32_t(xs_bytes + tile_bytes);
-    const uint32_t zero_rec = meta_off + uint32_t(treeens::kMetaBytes);
-    uint32_t *meta = reinterpret_cast<uint32_t *>(lds + meta_off);
-    uint2 *tn = reinterpret_cast<uint2 *>(lds + xs_bytes);
+    constexpr int kShift = NARROW ? 16 : treeens::kWideChildShift;
+    uint2 *slot = reinterpret_cast<uint2 *>(lds + xs_bytes);
+    const uint32_t *hdr = reinterpret_cast<const uint32_t *>(lds + xs_bytes);
     using Elem = std::conditional_t<CODED, uint16_t, float>;
     const Elem *X = reinterpret_cast<const Elem *>(Xv);
     Elem *xs = reinterpret_cast<Elem *>(lds);
@@ -122,187 +134,216 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     const int nthr = kThreads;
     const int dl = tid & (DL - 1);
     // with 64-document blocks a walker is a whole wave: make that visible to the compiler so
-    // the group loop and the tree bases live in scalar registers
-    const int walker = kUniform ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
+    // the group loop is scalar
+    const int walker = DL == 64 ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
     const int n_walkers = nthr / DL;
     const uint32_t lane_off = uint32_t(dl) * uint32_t(sizeof(Elem));
     const uint32_t col_mask =
         __builtin_amdgcn_readfirstlane(NARROW ? treeens::kNarrowColMask : treeens::kWideColMask);
     // column offsets below this are column 0 (NaN, or code 0), which only leaves name
     constexpr uint32_t kLeafCol = uint32_t(DL) * uint32_t(sizeof(Elem));
-    const int64_t doc0 = int64_t(blockIdx.x) * DL;
-    const int split = blockIdx.y;
+    // Workgroups [0, head_blocks) each walk all tiles for one document block; after them, each
+    // remaining block is split over tail_splits workgroups that walk a contiguous share of the
+    // tiles each and leave fp64 partial sums (the tail fills what would be a last, mostly idle
+    // round of workgroups; small batches have no head at all).
+    int64_t block = blockIdx.x;
+    int split = 0, n_splits = 1;
+    if (block >= head_blocks) {
+        const int64_t t = block - head_blocks;
+        block = head_blocks + t / tail_splits;
+        split = int(t % tail_splits);
+        n_splits = tail_splits;
+    }
+    const int64_t doc0 = block * DL;
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
     const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
 
-    // The next tile's records and tree offsets are loaded into registers while the current
-    // tile is walked, so the global-memory latency of a tile load is hidden.
+    // The next tile image is loaded into registers while the current one is walked, so the
+    // global-memory latency of a tile load is hidden. Its size comes from the current tile's
+    // header: the loop issues no scalar memory load (those share a wait counter with LDS reads
+    // and would stall the walk).
     uint2 pre[kPre];
-    uint32_t pre_meta = 0;
-    auto fetch = [&](int ti) {
-        const Tile tl = tiles[ti];
-        const int n_rec = int(tree_node_off[tl.tree_end]) - tl.node_begin;
-        const uint2 *src = nodes + tl.node_begin;
+    auto fetch = [&](int ti, int n_rec) {
+        const uint2 *src = images + int64_t(ti) * slot_recs;
 #pragma unroll
         for (int j = 0; j < kPre; ++j) {
             const int i = tid + j * kThreads;
             if (i < n_rec)
                 pre[j] = src[i];
         }
-        if (!kUniform && tid < tl.tree_end - tl.tree_begin)
-            pre_meta = tree_node_off[tl.tree_begin + tid] - uint32_t(tl.node_begin);
     };
+    int cur_recs = t_lo < t_hi ? int(tile_recs[t_lo]) : 0;
     if (t_lo < t_hi)
-        fetch(t_lo);
+        fetch(t_lo, cur_recs);
 
     // stage the document tile: lane = document, so each LDS write is conflict-free. The
     // workgroup size is a multiple of DL, so a thread's document (and row) is fixed and its
-    // columns step by kThreads / DL; eight columns are loaded before any is written so the
-    // global loads of a pass are in flight together.
+    // columns step by kThreads / DL. Loads are unconditional (clamped to a valid element) so
+    // that the eight of a pass are in flight together before any is written.
     {
         constexpr int kColStep = kThreads / DL;
         constexpr int kUnroll = 8;
         const int64_t doc = doc0 + dl;
         const bool live = doc < n_docs;
-        const Elem *row = X + (live ? doc : 0) * int64_t(n_features);
+        const Elem *row = X + (live ? doc : n_docs - 1) * int64_t(n_features);
         const Elem leaf_col = CODED ? Elem(0) : Elem(__builtin_nanf(""));
+        const int last = n_cols > 0 ? n_cols - 1 : 0;
         for (int c0 = tid / DL; c0 <= n_cols; c0 += kColStep * kUnroll) {
             Elem v[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int c = c0 + u * kColStep;
-                v[u] = leaf_col;
-                if (c > 0 && c <= n_cols)
-                    v[u] = live ? row[c - 1] : Elem(0);
-            }
+            for (int u = 0; u < kUnroll; ++u)
+                v[u] = row[min(max(c0 + u * kColStep - 1, 0), last)];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int c = c0 + u * kColStep;
                 if (c <= n_cols)
-                    xs[c * DL + dl] = v[u];
+                    xs[c * DL + dl] = c == 0 ? leaf_col : (live ? v[u] : Elem(0));
             }
         }
     }
-    if (tid == 0)
-        *reinterpret_cast<uint2 *>(lds + zero_rec) = make_uint2(0u, 0u);
+    if (tid == 0) {
+        // value 0 (as -0.0 for codes, whose leaves never hold zero bits), column 0, self link
+        const uint32_t thr = CODED ? 0x80000000u : 0u;
+        *reinterpret_cast<uint2 *>(lds + zero_rec) = make_uint2(thr, (uint32_t(zero_rec) / 8u) << kShift);
+    }
 
     double acc = 0.0;
     for (int ti = t_lo; ti < t_hi; ++ti) {
-        const Tile tl = tiles[ti];
-        const int n_rec = int(tree_node_off[tl.tree_end]) - tl.node_begin;
-        const int ntr = tl.tree_end - tl.tree_begin;
         __syncthreads(); // the previous tile is fully walked (and the document tile written)
+        // All outstanding global loads (this tile's records, and the document rows before the
+        // first tile) land here, unconditionally: otherwise the compiler cannot prove them
+        // complete on every path and waits for them again inside the walk.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 #pragma unroll
         for (int j = 0; j < kPre; ++j) {
             const int i = tid + j * kThreads;
-            if (i < n_rec)
-                tn[i] = pre[j];
+            if (i < cur_recs)
+                slot[i] = pre[j];
         }
-        if (!kUniform && tid < ntr)
-            meta[tid] = pre_meta;
         __syncthreads();
+        const uint4 h = *reinterpret_cast<const uint4 *>(hdr);
+        const int ntr = __builtin_amdgcn_readfirstlane(int(h.x));
+        const int complete_depth = __builtin_amdgcn_readfirstlane(int(h.y));
+        const int tree_begin = __builtin_amdgcn_readfirstlane(int(h.z));
+        cur_recs = __builtin_amdgcn_readfirstlane(int(h.w));
         if (ti + 1 < t_hi)
-            fetch(ti + 1);
+            fetch(ti + 1, cur_recs);
 
         // Walker w takes groups w, w + n_walkers, ... of K consecutive trees (the packer sizes
-        // tiles to a multiple of n_walkers * K trees where it can).
+        // tiles to a multiple of n_walkers * K trees where it can, and pads the header's root
+        // copies to a multiple of K with the zero record).
         const int n_groups = (ntr + K - 1) / K;
-        auto tree_base = [&](int t) -> uint32_t {
-            if (t >= ntr)
-                return zero_rec;
-            if constexpr (kUniform)
-                return uint32_t(xs_bytes) +
-                       (tree_node_off[tl.tree_begin + t] - uint32_t(tl.node_begin)) * 8u;
-            else
-                return uint32_t(xs_bytes) + meta[t] * 8u;
-        };
-        for (int g = walker; g < n_groups; g += n_walkers) {
-            uint32_t base[K];
-            uint2 nd[K];
-#pragma unroll
-            for (int i = 0; i < K; ++i) {
-                base[i] = tree_base(g * K + i);
-                if constexpr (kUniform)
-                    asm("" : "+s"(base[i])); // opaque: keep base + offset as one add
-                else
-                    asm("" : "+v"(base[i]));
-                nd[i] = *reinterpret_cast<const uint2 *>(lds + base[i]);
-            }
-            // One predicated step from the feature addresses fa: read the feature, compare,
-            // child index + bit (the right child follows the left one), read that record.
-            uint32_t fa[K];
-            auto feature_addresses = [&]() {
+        // records of the tile's trees start after the fixed header words and the root copies
+        const uint32_t rec0 = uint32_t(xs_bytes) / 8u + uint32_t(treeens::kHeaderFixedWords / 2 + n_groups * K);
+        auto walk = [&](auto complete_tag) {
+            constexpr bool kComplete = decltype(complete_tag)::value;
+            for (int g = walker; g < n_groups; g += n_walkers) {
+                // the K root records, copied into the header (broadcast reads)
+                uint64_t nd[K];
+                const unsigned char *rc = lds + xs_bytes + 8 * (treeens::kHeaderFixedWords / 2 + g * K);
 #pragma unroll
                 for (int i = 0; i < K; ++i)
-                    fa[i] = and_or(nd[i].y, col_mask, lane_off);
-            };
-            auto step = [&]() {
-                uint32_t addr[K];
+                    nd[i] = read_record(rc + 8 * i);
+                // One predicated step: feature addresses fa from the records, read the features
+                // xv, compare, child link + bit (the right child follows the left one), read
+                // that record.
+                uint32_t fa[K];
+                std::conditional_t<CODED, uint32_t, float> xv[K];
+                auto read_features = [&]() {
 #pragma unroll
-                for (int i = 0; i < K; ++i) {
-                    uint32_t child;
-                    if constexpr (CODED) {
-                        const uint32_t x = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
-                        if constexpr (NARROW)
-                            child = narrow_child_coded(nd[i].y, x, nd[i].x);
+                    for (int i = 0; i < K; ++i) {
+                        fa[i] = and_or(rec_w(nd[i]), col_mask, lane_off);
+                        if constexpr (CODED)
+                            xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
                         else
-                            child = (nd[i].y >> treeens::kWideChildShift) + (x >= nd[i].x ? 1u : 0u);
-                    } else {
-                        const float x = *reinterpret_cast<const float *>(lds + fa[i]);
-                        if constexpr (NARROW)
-                            child = narrow_child(nd[i].y, x, __uint_as_float(nd[i].x));
-                        else
-                            child = (nd[i].y >> treeens::kWideChildShift) +
-                                    (x >= __uint_as_float(nd[i].x) ? 1u : 0u);
+                            xv[i] = *reinterpret_cast<const float *>(lds + fa[i]);
                     }
-                    addr[i] = base[i] + child * 8u;
-                }
+                };
+                auto descend = [&]() {
+                    uint32_t addr[K];
 #pragma unroll
-                for (int i = 0; i < K; ++i)
-                    nd[i] = *reinterpret_cast<const uint2 *>(lds + addr[i]);
-            };
-            if (tl.complete_depth >= 0) {
-                // every path has the same length: no leaf test needed
-                for (int s = 0; s < tl.complete_depth; ++s) {
-                    feature_addresses();
-                    step();
-                }
-            } else {
-                // every lane steps until all lanes of the wave sit on leaves (a leaf's feature
-                // address is the NaN column, below kLeafCol); the record that shows a lane is
-                // at a leaf holds the leaf's value. Every path of a validated tree reaches a
-                // leaf within the tile's max_depth steps and leaves link to themselves, so the
-                // exit is always taken.
-                for (;;) {
-                    feature_addresses();
-                    bool internal = false;
+                    for (int i = 0; i < K; ++i) {
+                        uint32_t child;
+                        const uint32_t w = rec_w(nd[i]), thr = rec_thr(nd[i]);
+                        if constexpr (CODED) {
+                            if constexpr (NARROW)
+                                child = narrow_child_coded(w, xv[i], thr);
+                            else
+                                child = (w >> kShift) + (xv[i] >= thr ? 1u : 0u);
+                        } else {
+                            if constexpr (NARROW)
+                                child = narrow_child(w, xv[i], __uint_as_float(thr));
+                            else
+                                child = (w >> kShift) + (xv[i] >= __uint_as_float(thr) ? 1u : 0u);
+                        }
+                        addr[i] = child * 8u;
+                    }
 #pragma unroll
                     for (int i = 0; i < K; ++i)
-                        internal |= fa[i] >= kLeafCol;
-                    if (!__any(internal))
-                        break;
-                    step();
-                }
-            }
-            float group_sum = 0.0f; // K leaf values: exact enough in float, one double add
-#pragma unroll
-            for (int i = 0; i < K; ++i) {
-                if constexpr (LEAVES) {
-                    // a leaf's link is its own position in the tree
-                    const int64_t doc = doc0 + dl;
-                    const int t = g * K + i;
-                    if (t < ntr && doc < n_docs) {
-                        const int gt = tl.tree_begin + t;
-                        const uint32_t self = nd[i].y >> (NARROW ? 16 : treeens::kWideChildShift);
-                        leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
+                        nd[i] = read_record(lds + addr[i]);
+                };
+                if constexpr (kComplete) {
+                    // every path has the same length: no leaf test needed
+                    for (int s = 0; s < complete_depth; ++s) {
+                        read_features();
+                        descend();
                     }
                 } else {
-                    group_sum += __uint_as_float(nd[i].x); // idle slots read the zero record
+                    // Every lane steps until all lanes of the wave sit on leaves (a leaf's
+                    // feature address is the NaN column, below kLeafCol); the record that shows
+                    // a lane is at a leaf holds the leaf's value. Every path of a validated tree
+                    // reaches a leaf and leaves link to themselves, so the exit is always taken.
+                    // The next feature reads are issued before the test, so the test overlaps
+                    // their latency (after the last step they read the NaN column: harmless).
+                    auto any_internal = [&]() {
+                        bool internal = false;
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            internal |= fa[i] >= kLeafCol;
+                        return __builtin_amdgcn_ballot_w64(internal) != 0;
+                    };
+                    read_features();
+                    if (any_internal()) {
+                        do {
+                            descend();
+                            read_features();
+                        } while (any_internal());
+                    }
+                    // The exit path "uses" the last feature reads, so the compiler cannot sink
+                    // them below the test (where they would serialise with it again).
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        asm volatile("" ::"v"(xv[i]));
+                }
+                if constexpr (LEAVES) {
+                    const int64_t doc = doc0 + dl;
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        // a leaf's link is its own LDS record index; minus that of its tree's
+                        // root, it is the leaf's position in the tree
+                        const int t = g * K + i;
+                        if (t < ntr && doc < n_docs) {
+                            const int gt = tree_begin + t;
+                            const uint32_t root = rec0 + tree_node_off[gt] - tree_node_off[tree_begin];
+                            const uint32_t self = (rec_w(nd[i]) >> kShift) - root;
+                            leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
+                        }
+                    }
+                } else {
+                    // K leaf values: exact enough in float, one double add (idle slots hold the
+                    // zero record)
+                    float group_sum = __uint_as_float(rec_thr(nd[0]));
+#pragma unroll
+                    for (int i = 1; i < K; ++i)
+                        group_sum += __uint_as_float(rec_thr(nd[i]));
+                    acc += double(group_sum);
                 }
             }
-            if constexpr (!LEAVES)
-                acc += double(group_sum);
-        }
+        };
+        if (complete_depth >= 0)
+            walk(std::true_type{});
+        else
+            walk(std::false_type{});
     }
     if constexpr (!LEAVES) {
         __syncthreads();
@@ -315,10 +356,12 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             for (int w = 0; w < n_walkers; ++w)
                 sum += red[w * DL + dl];
             if (doc < n_docs) {
-                if (n_splits == 1)
+                if (n_splits == 1) {
                     scores[doc] = float(sum);
-                else
-                    partials[int64_t(split) * n_docs + doc] = sum;
+                } else {
+                    const int64_t tail0 = int64_t(head_blocks) * DL;
+                    partials[int64_t(split) * (n_docs - tail0) + (doc - tail0)] = sum;
+                }
             }
         }
     }
@@ -397,9 +440,10 @@ code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int
     }
 }
 
-using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *, const uint32_t *,
-                         const Tile *, int32_t, int32_t, int32_t, int32_t, double *, float *,
-                         int32_t *, const int32_t *, const int32_t *, int32_t);
+using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *, int32_t,
+                         const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
+                         float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
+                         int32_t);
 
 template <int DL, bool HALF, bool NARROW, bool CODED, bool LEAVES>
 ScoreFn pick_k(int k) {
@@ -451,12 +495,14 @@ struct tree_ens {
     int64_t n_nodes = 0;
     treeens::LdsPlan plan{};
     int32_t level_begin[treeens::kTileLevels + 1] = {};
-    uint2 *d_nodes = nullptr;
+    int64_t level_image_off[treeens::kTileLevels] = {};
+    int32_t level_slot_recs[treeens::kTileLevels] = {};
+    uint2 *d_images = nullptr;      // tile images of every tiling
+    uint32_t *d_tile_recs = nullptr; // records of each tile image
+    // leaf-id output: packed tree -> input tree, packed node -> input node id
     uint32_t *d_tree_node_off = nullptr;
-    uint32_t *d_tree_depth = nullptr;
     int32_t *d_tree_orig = nullptr;
     int32_t *d_orig_id = nullptr;
-    Tile *d_tiles = nullptr;
     // coded models
     float *d_code_table = nullptr;
     uint32_t *d_code_table_off = nullptr;
@@ -479,12 +525,11 @@ constexpr size_t kScratchDoubles = size_t(1) << 17; // 1 MiB of split partials
 namespace {
 
 void free_device(tree_ens *h) {
-    (void)hipFree(h->d_nodes);
+    (void)hipFree(h->d_images);
+    (void)hipFree(h->d_tile_recs);
     (void)hipFree(h->d_tree_node_off);
-    (void)hipFree(h->d_tree_depth);
     (void)hipFree(h->d_tree_orig);
     (void)hipFree(h->d_orig_id);
-    (void)hipFree(h->d_tiles);
     (void)hipFree(h->d_code_table);
     (void)hipFree(h->d_code_table_off);
     (void)hipFree(h->d_code_chunks);
@@ -504,39 +549,56 @@ hipError_t upload(T **dst, const std::vector<T> &src) {
     return e;
 }
 
-// Split count and tiling level for a batch of n_blocks document blocks. Each (block, split)
-// workgroup walks a contiguous share of the tiles. The estimated makespan, in units of one
-// block walking all trees, is
-//     ceil(n_blocks * splits / resident workgroups) * (largest share + per-workgroup cost)
-//     + (splits > 1 ? cost of the partial-sum reduction : 0):
-// splitting fills the last round of workgroups (a batch of 1,563 blocks on 512 resident
-// workgroups would otherwise run a fourth round at 5% occupancy) and spreads small batches
-// over the whole GPU.
-void choose_split(const tree_ens *h, int64_t n_blocks, int *level, int *splits) {
+// Launch shape for a batch of n_blocks document blocks: a tiling level, a number of head
+// blocks walked whole by one workgroup each, and the split count of the remaining (tail)
+// blocks, each split over that many workgroups that walk a contiguous share of the tiles. The
+// estimated makespan, in units of one block walking all trees, is
+//     head rounds * (1 + per-workgroup cost)
+//     + ceil(tail blocks * splits / resident workgroups) * (largest share + per-workgroup cost)
+//     + (splits > 1 ? cost of the partial-sum reduction : 0).
+// Candidates: everything split uniformly (no head; small batches spread over the whole GPU),
+// and whole rounds as head with the remainder split to fill the last round (a batch of 1,563
+// blocks on 512 resident workgroups would otherwise run a fourth round at 5% occupancy).
+struct LaunchShape {
+    int level = 0;
+    int64_t head = 0;
+    int splits = 1;
+};
+
+LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
     constexpr double kItemCost = 0.2;    // staging, prologue and restaging of one workgroup (measured)
     constexpr double kReduceCost = 0.05; // the second kernel
     const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
     const int64_t slots = int64_t(kNumCus) * wg_per_cu;
     double best = 1e300;
-    *level = 0;
-    *splits = 1;
+    LaunchShape pick;
+    auto consider = [&](int level, int64_t head, int sp) {
+        const int nt = h->level_begin[level + 1] - h->level_begin[level];
+        const int64_t tail = n_blocks - head;
+        const double share = double((nt + sp - 1) / sp) / nt;
+        const double cost = double(head / slots) * (1.0 + kItemCost) +
+                            double((tail * sp + slots - 1) / slots) * (share + kItemCost) +
+                            (sp > 1 ? kReduceCost : 0.0);
+        if (cost < best - 1e-9) {
+            best = cost;
+            pick = LaunchShape{level, head, sp};
+        }
+    };
     for (int k = 0; k < treeens::kTileLevels; ++k) {
         const int nt = h->level_begin[k + 1] - h->level_begin[k];
-        for (int sp = 1; sp <= std::min(nt, 1024); ++sp) {
-            const int64_t rounds = (n_blocks * sp + slots - 1) / slots;
-            const double share = double((nt + sp - 1) / sp) / nt;
-            const double cost = double(rounds) * (share + kItemCost) + (sp > 1 ? kReduceCost : 0.0);
-            if (cost < best - 1e-9) {
-                best = cost;
-                *level = k;
-                *splits = sp;
-            }
-        }
+        for (int sp = 1; sp <= std::min(nt, 1024); ++sp)
+            consider(k, 0, sp);
+    }
+    const int64_t rem = n_blocks % slots;
+    if (n_blocks > slots && rem > 0) {
+        const int nt = h->level_begin[1] - h->level_begin[0];
+        for (int sp = 2; sp <= std::min<int64_t>(nt, slots / rem); ++sp)
+            consider(0, n_blocks - rem, sp);
     }
 #ifdef TREE_ENS_FORCE_SPLITS // measurement builds only
-    *level = 0;
-    *splits = std::min(TREE_ENS_FORCE_SPLITS, h->level_begin[1] - h->level_begin[0]);
+    pick = LaunchShape{0, 0, std::min(TREE_ENS_FORCE_SPLITS, h->level_begin[1] - h->level_begin[0])};
 #endif
+    return pick;
 }
 
 struct DeviceGuard {
@@ -583,8 +645,12 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const int64_t n_blocks = (n_docs + dl - 1) / dl;
     if (n_blocks > 0x7fffffff)
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
-    int level, splits;
-    choose_split(h, n_blocks, &level, &splits);
+    const LaunchShape shape = choose_launch(h, n_blocks);
+    const int level = shape.level, splits = shape.splits;
+    const int64_t tail_docs = n_docs - shape.head * dl;
+    const int64_t n_wgs = shape.head + (n_blocks - shape.head) * splits;
+    if (n_wgs > 0x7fffffff)
+        return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     ScoreFn fn = pick_kernel<LEAVES>(h->plan);
     if (!fn)
         return fail(TREE_ENS_E_ARG, "unsupported document block size");
@@ -593,7 +659,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     bool own_scratch = false; // partials live in the handle's scratch
     std::unique_lock<std::mutex> scratch_lock;
     if (!LEAVES && splits > 1) {
-        if (size_t(splits) * size_t(n_docs) <= kScratchDoubles) {
+        if (size_t(splits) * size_t(tail_docs) <= kScratchDoubles) {
             scratch_lock = std::unique_lock<std::mutex>(h->scratch_mu);
             if (h->scratch_used && h->scratch_stream != stream) {
                 e = hipStreamWaitEvent(stream, h->scratch_done, 0);
@@ -604,12 +670,13 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
             own_scratch = true;
         } else {
             e = hipMallocAsync(reinterpret_cast<void **>(&partials),
-                               size_t(splits) * size_t(n_docs) * sizeof(double), stream);
+                               size_t(splits) * size_t(tail_docs) * sizeof(double), stream);
             if (e != hipSuccess)
                 return hip_fail(e, "hipMallocAsync(partials)");
         }
     }
-    const Tile *tiles = h->d_tiles + h->level_begin[level];
+    const uint2 *images = h->d_images + h->level_image_off[level];
+    const uint32_t *tile_recs = h->d_tile_recs + h->level_begin[level];
     const int n_tiles = h->level_begin[level + 1] - h->level_begin[level];
     (void)hipGetLastError();
     // coded models: one pass turns the float features into 16-bit threshold codes
@@ -637,19 +704,20 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         docs = codes;
         row_stride = h->n_cols;
     }
-    hipLaunchKernelGGL(fn, dim3(unsigned(n_blocks), unsigned(splits)), dim3(kThreads), 0,
-                       stream, docs, n_docs, row_stride, h->n_cols, h->d_nodes,
-                       h->d_tree_node_off, tiles, n_tiles, splits,
-                       h->plan.xs_bytes, h->plan.tile_bytes, partials, scores, leaf_ids,
-                       h->d_orig_id, h->d_tree_orig, h->n_trees);
+    hipLaunchKernelGGL(fn, dim3(unsigned(n_wgs)), dim3(kThreads), 0, stream, docs, n_docs,
+                       row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs, n_tiles,
+                       int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec, partials,
+                       scores, leaf_ids, h->d_orig_id, h->d_tree_node_off, h->d_tree_orig,
+                       h->n_trees);
     e = hipGetLastError();
     if (e == hipSuccess && partials) {
+        float *tail_scores = scores + shape.head * dl;
         if (splits <= 64)
-            hipLaunchKernelGGL(reduce_partials_thread_kernel, dim3(unsigned((n_docs + 255) / 256)),
-                               dim3(256), 0, stream, partials, splits, n_docs, scores);
+            hipLaunchKernelGGL(reduce_partials_thread_kernel, dim3(unsigned((tail_docs + 255) / 256)),
+                               dim3(256), 0, stream, partials, splits, tail_docs, tail_scores);
         else
-            hipLaunchKernelGGL(reduce_partials_wave_kernel, dim3(unsigned(n_docs)), dim3(64), 0,
-                               stream, partials, splits, n_docs, scores);
+            hipLaunchKernelGGL(reduce_partials_wave_kernel, dim3(unsigned(tail_docs)), dim3(64), 0,
+                               stream, partials, splits, tail_docs, tail_scores);
         e = hipGetLastError();
     }
     if (own_scratch) {
@@ -706,21 +774,21 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
     h->plan = p.plan;
     std::memcpy(h->level_begin, p.level_begin, sizeof h->level_begin);
     hipError_t e = hipGetDevice(&h->device);
-    std::vector<uint2> nodes(p.nodes.size());
-    if (!p.nodes.empty())
-        std::memcpy(nodes.data(), p.nodes.data(), p.nodes.size() * sizeof(NodeRec));
+    std::memcpy(h->level_image_off, p.level_image_off, sizeof h->level_image_off);
+    std::memcpy(h->level_slot_recs, p.level_slot_recs, sizeof h->level_slot_recs);
+    std::vector<uint2> images(p.images.size());
+    if (!p.images.empty())
+        std::memcpy(images.data(), p.images.data(), p.images.size() * sizeof(NodeRec));
     if (e == hipSuccess)
-        e = upload(&h->d_nodes, nodes);
+        e = upload(&h->d_images, images);
+    if (e == hipSuccess)
+        e = upload(&h->d_tile_recs, p.tile_recs);
     if (e == hipSuccess)
         e = upload(&h->d_tree_node_off, p.tree_node_off);
-    if (e == hipSuccess)
-        e = upload(&h->d_tree_depth, p.tree_depth);
     if (e == hipSuccess)
         e = upload(&h->d_tree_orig, p.tree_orig);
     if (e == hipSuccess)
         e = upload(&h->d_orig_id, p.orig_id);
-    if (e == hipSuccess)
-        e = upload(&h->d_tiles, p.tiles);
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&h->d_scratch), kScratchDoubles * sizeof(double));
     if (e == hipSuccess)

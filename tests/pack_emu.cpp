@@ -1,0 +1,213 @@
+// pack_emu.cpp -- host emulation of the scoring kernel's addressing, for CPU tests.
+//
+// Test infrastructure: packs a model with the library's own packer (pack.cpp) and walks every
+// tile image of one tiling the way the kernel does -- LDS byte layout, feature addresses built
+// by OR-ing the column offset with the lane offset, child links as absolute LDS record
+// indices, the all-zero self-linked record for padding slots -- checking that every LDS
+// access stays inside the region it must read. The tests compare the leaf ids it reports with
+// the oracle's, so a packing or addressing mistake shows up on the CPU before any GPU run.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "pack.hpp"
+
+namespace {
+
+std::string g_msg;
+
+int bad(const std::string &m) {
+    g_msg = m;
+    return 1;
+}
+
+float as_float(uint32_t u) {
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// code_f(x) = number of distinct thresholds t of f with x >= t (0 for NaN)
+uint16_t code_of(const treeens::Packed &p, int f, float x) {
+    const float *b = p.code_table.data() + p.code_table_off[size_t(f)];
+    const float *e = p.code_table.data() + p.code_table_off[size_t(f) + 1];
+    uint16_t c = 0;
+    for (const float *t = b; t < e; ++t)
+        if (x >= *t)
+            ++c;
+    return c;
+}
+
+} // namespace
+
+extern "C" {
+
+const char *emu_message(void) { return g_msg.c_str(); }
+
+// Walk all documents through tiling `level`. Outputs leaf ids [n_docs][n_trees] (input node ids)
+// and fp64 scores. Returns 0, or 1 with a message naming the first violated invariant, or a
+// negative packer status.
+int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+             const float *threshold, const int32_t *left, const int32_t *right, const float *value,
+             uint32_t flags, const float *X, int64_t n_docs, int32_t n_features, int32_t level,
+             int32_t *leaf_ids, double *scores, int32_t *plan_out) {
+    treeens::Packed p;
+    std::string err;
+    const int rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value,
+                                       flags, p, err);
+    if (rc != treeens::kOk) {
+        g_msg = err;
+        return rc;
+    }
+    const treeens::LdsPlan &pl = p.plan;
+    if (plan_out) {
+        plan_out[0] = pl.docs_per_block;
+        plan_out[1] = pl.interleave;
+        plan_out[2] = pl.narrow;
+        plan_out[3] = pl.coded;
+        plan_out[4] = p.level_begin[1] - p.level_begin[0];
+        plan_out[5] = pl.lds_bytes;
+    }
+    const int DL = pl.docs_per_block, K = pl.interleave, E = pl.elem_bytes;
+    const int shift = pl.narrow ? 16 : treeens::kWideChildShift;
+    const uint32_t mask = pl.narrow ? treeens::kNarrowColMask : treeens::kWideColMask;
+    const uint32_t xs = uint32_t(pl.xs_bytes), zero = uint32_t(pl.zero_rec);
+    const uint32_t leaf_col = uint32_t(DL * E);
+    if (xs % 16 || zero % 8 || zero + 8 > uint32_t(pl.lds_bytes) || xs + uint32_t(pl.tile_bytes) > zero)
+        return bad("LDS plan regions overlap or exceed the workgroup's LDS");
+    if (int64_t(p.n_cols + 1) * DL * E != pl.xs_bytes)
+        return bad("document tile size does not match the column count");
+    std::vector<uint8_t> lds(size_t(pl.lds_bytes), 0);
+    auto rec_at = [&](uint32_t a) {
+        treeens::NodeRec r;
+        std::memcpy(&r, lds.data() + a, 8);
+        return r;
+    };
+    const int32_t t0 = p.level_begin[level], t1 = p.level_begin[level + 1];
+    const int64_t slot = p.level_slot_recs[level];
+    if (slot * 8 > pl.tile_bytes)
+        return bad("image stride exceeds the LDS slot");
+    std::vector<int32_t> seen(size_t(n_trees), 0);
+    for (int64_t i = 0; i < n_docs * n_trees; i++)
+        leaf_ids[i] = -1;
+    for (int64_t d = 0; d < n_docs; d++)
+        scores[d] = 0.0;
+
+    for (int64_t doc0 = 0; doc0 < n_docs; doc0 += DL) {
+        // document tile: column 0 NaN (or code 0), column f + 1 = feature f, lane = document
+        for (int c = 0; c <= p.n_cols; c++) {
+            for (int dl = 0; dl < DL; dl++) {
+                const int64_t doc = doc0 + dl;
+                uint8_t *dst = lds.data() + (size_t(c) * DL + dl) * E;
+                if (E == 4) {
+                    float v = c == 0 ? NAN : (doc < n_docs ? X[doc * n_features + c - 1] : 0.0f);
+                    std::memcpy(dst, &v, 4);
+                } else {
+                    uint16_t v = c == 0 || doc >= n_docs ? 0 : code_of(p, c - 1, X[doc * n_features + c - 1]);
+                    std::memcpy(dst, &v, 2);
+                }
+            }
+        }
+        const treeens::NodeRec z{pl.coded ? 0x80000000u : 0u, (zero / 8u) << shift};
+        std::memcpy(lds.data() + zero, &z, 8);
+
+        for (int32_t t = t0; t < t1; t++) {
+            const uint32_t recs = p.tile_recs[size_t(t)];
+            if (recs > uint32_t(slot))
+                return bad("tile image longer than its stride");
+            const treeens::NodeRec *img = p.images.data() + p.level_image_off[level] + (t - t0) * slot;
+            std::memcpy(lds.data() + xs, img, size_t(recs) * 8);
+            uint32_t h[4];
+            std::memcpy(h, lds.data() + xs, 16);
+            const int ntr = int(h[0]), complete = int32_t(h[1]), tb = int(h[2]);
+            const uint32_t next = h[3];
+            if (next != (t + 1 < t1 ? p.tile_recs[size_t(t) + 1] : 0u))
+                return bad("header: next tile size is wrong");
+            if (ntr < 1 || tb < 0 || tb + ntr > n_trees)
+                return bad("header: tree range out of bounds");
+            const int padded = (ntr + K - 1) / K * K;
+            const uint32_t hdr_bytes = uint32_t(treeens::kHeaderFixedWords / 2 + padded) * 8u;
+            const uint32_t lo = xs + hdr_bytes, hi = xs + recs * 8u;
+            auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= lo && a + 8 <= hi) || a == zero); };
+            // root copies: records 2.. of the header; padding slots hold the zero record
+            const uint32_t root0 = xs + 8u * uint32_t(treeens::kHeaderFixedWords / 2);
+            for (int s = ntr; s < padded; s++)
+                if (std::memcmp(lds.data() + root0 + 8u * s, lds.data() + zero, 8) != 0)
+                    return bad("header: padding root is not the zero record");
+            const uint32_t rec0 = xs / 8u + hdr_bytes / 8u; // LDS index of the first tree record
+            for (int s = 0; s < ntr; s++) {
+                const int gt = tb + s;
+                const uint32_t root_idx = rec0 + p.tree_node_off[size_t(gt)] - p.tree_node_off[size_t(tb)];
+                if (!valid(root_idx * 8u) || std::memcmp(lds.data() + root_idx * 8u, lds.data() + root0 + 8u * s, 8) != 0)
+                    return bad("root copy does not match the tree's root record");
+                const int64_t tree_n = int64_t(p.tree_node_off[size_t(gt) + 1] - p.tree_node_off[size_t(gt)]);
+                for (int dl = 0; dl < DL && doc0 + dl < n_docs; dl++) {
+                    const int64_t doc = doc0 + dl;
+                    treeens::NodeRec r = rec_at(root0 + 8u * s);
+                    int steps = 0;
+                    for (;;) {
+                        const uint32_t fa = (r.w & mask) | uint32_t(dl * E);
+                        if (fa != (r.w & mask) + uint32_t(dl * E))
+                            return bad("column offset and lane offset overlap");
+                        if (fa + uint32_t(E) > xs)
+                            return bad("feature address outside the document tile");
+                        if (complete >= 0 ? steps == complete : fa < leaf_col)
+                            break;
+                        bool right_side;
+                        if (E == 4) {
+                            float x;
+                            std::memcpy(&x, lds.data() + fa, 4);
+                            right_side = x >= as_float(r.thr_bits);
+                        } else {
+                            uint16_t x;
+                            std::memcpy(&x, lds.data() + fa, 2);
+                            right_side = uint32_t(x) >= r.thr_bits;
+                        }
+                        const uint32_t a = ((r.w >> shift) + (right_side ? 1u : 0u)) * 8u;
+                        if (!valid(a))
+                            return bad("child address outside the tile's records");
+                        r = rec_at(a);
+                        if (++steps > p.max_depth + 1)
+                            return bad("walk longer than the deepest tree");
+                    }
+                    if ((r.w & mask) != 0)
+                        return bad("walk ended on an internal node");
+                    {
+                        // one more step from a leaf must come back to the same record
+                        bool right_side;
+                        if (E == 4) {
+                            float x;
+                            std::memcpy(&x, lds.data() + (r.w & mask) + dl * E, 4);
+                            right_side = x >= as_float(r.thr_bits);
+                        } else {
+                            uint16_t x;
+                            std::memcpy(&x, lds.data() + (r.w & mask) + dl * E, 2);
+                            right_side = uint32_t(x) >= r.thr_bits;
+                        }
+                        const uint32_t a = ((r.w >> shift) + (right_side ? 1u : 0u)) * 8u;
+                        if (!valid(a) || std::memcmp(lds.data() + a, &r, 8) != 0)
+                            return bad("a leaf does not absorb a further step");
+                    }
+                    const int64_t self = int64_t(r.w >> shift) - int64_t(root_idx);
+                    if (self < 0 || self >= tree_n)
+                        return bad("leaf outside its tree");
+                    const int32_t orig_tree = p.tree_orig[size_t(gt)];
+                    leaf_ids[doc * n_trees + orig_tree] = p.orig_id[p.tree_node_off[size_t(gt)] + size_t(self)];
+                    scores[doc] += double(as_float(r.thr_bits));
+                }
+                seen[size_t(p.tree_orig[size_t(gt)])]++;
+            }
+        }
+    }
+    const int64_t blocks = (n_docs + DL - 1) / DL;
+    for (int32_t t = 0; t < n_trees; t++)
+        if (seen[size_t(t)] != blocks)
+            return bad("tree " + std::to_string(t) + " is not walked exactly once per block");
+    return 0;
+}
+
+} // extern "C"

@@ -40,7 +40,9 @@ def test_hand_golden_on_gpu(T, rule, name):
     assert np.array_equal(ids, exp_ids)
 
 
-@pytest.mark.parametrize("n_docs", [1, 7, 63, 64, 65, 127, 4097])
+# 32,773 and 67,331 documents: whole rounds of 64-document blocks on the 512 resident
+# workgroups plus a remainder, whose blocks the launch splits over the tiles (partial sums)
+@pytest.mark.parametrize("n_docs", [1, 7, 63, 64, 65, 127, 4097, 32773, 67331])
 def test_batch_sizes(T, n_docs):
     cfg = W.CONFIGS[2]
     ens = W.make_ensemble(cfg, n_trees=300)

@@ -1,0 +1,95 @@
+"""The packer's tile images, walked on the host exactly as the scoring kernel addresses them
+(``tests/pack_emu.cpp``): every LDS access stays in its region, every tree is walked once per
+document block, leaves absorb further steps, and the leaf each document reaches matches the
+oracle's, at every tiling the launch may pick. This pins the layout before any GPU run."""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from _golden import load_hand_ensemble
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_1212_2287_amd", "csrc")
+LEVELS = 5
+
+
+@pytest.fixture(scope="module")
+def emu(tmp_path_factory):
+    out = str(tmp_path_factory.mktemp("emu") / "libpackemu.so")
+    subprocess.run(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-I", CSRC,
+                    os.path.join(ROOT, "tests", "pack_emu.cpp"), os.path.join(CSRC, "pack.cpp"),
+                    "-o", out], check=True)
+    lib = ctypes.CDLL(out)
+    P = ctypes.c_void_p
+    lib.emu_walk.restype = ctypes.c_int
+    lib.emu_walk.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_uint32, P, ctypes.c_int64,
+                             ctypes.c_int32, ctypes.c_int32, P, P, P]
+    lib.emu_message.restype = ctypes.c_char_p
+    return lib
+
+
+def _walk(lib, ens, X, level, flags=0):
+    arrs = [np.ascontiguousarray(ens.tree_offsets, np.int64), np.ascontiguousarray(ens.feature, np.int32),
+            np.ascontiguousarray(ens.threshold, np.float32), np.ascontiguousarray(ens.left, np.int32),
+            np.ascontiguousarray(ens.right, np.int32), np.ascontiguousarray(ens.value, np.float32)]
+    X = np.ascontiguousarray(X, np.float32)
+    leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
+    scores = np.empty(X.shape[0], np.float64)
+    plan = np.zeros(6, np.int32)
+    rc = lib.emu_walk(ens.n_trees, *[a.ctypes.data for a in arrs], flags, X.ctypes.data, X.shape[0],
+                      X.shape[1], level, leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
+    assert rc == 0, lib.emu_message().decode()
+    return leaves, scores, plan
+
+
+def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
+    ref_scores, ref_leaves, _ = oracle.score(ens, X, rule=flags)
+    plans = []
+    for lv in levels:
+        leaves, scores, plan = _walk(lib, ens, X, lv, flags)
+        np.testing.assert_array_equal(leaves, ref_leaves, err_msg=f"tiling {lv}")
+        np.testing.assert_allclose(scores, ref_scores, rtol=1e-12, atol=1e-12, err_msg=f"tiling {lv}")
+        plans.append(plan)
+    return plans[0]
+
+
+def test_hand_ensemble_both_rules(emu):
+    ens, X, _ = load_hand_ensemble()
+    for flags in (0, 1):
+        _check(emu, ens, X, flags)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_ensembles(emu, seed):
+    rng = np.random.default_rng(seed)
+    n_feat = int(rng.integers(1, 300))
+    ens = W.random_ensemble(seed, n_trees=int(rng.integers(1, 400)), n_features=n_feat,
+                            min_leaves=1, max_leaves=int(rng.integers(2, 200)))
+    X = W.random_docs(seed, n_docs=int(rng.integers(1, 150)), n_features=n_feat)
+    _check(emu, ens, X, flags=seed % 2)
+
+
+@pytest.mark.parametrize("cfg_id,n_trees,n_docs,expect", [
+    (1, None, 200, dict(dl=64, coded=0)),
+    (2, None, 130, dict(dl=64, coded=0)),
+    (3, 300, 70, dict(dl=32, coded=0)),
+    (4, 3000, 70, dict(dl=64, coded=0)),
+    (5, 200, 70, dict(dl=64, coded=1, narrow=0)),
+])
+def test_workload_shapes(emu, cfg_id, n_trees, n_docs, expect):
+    """Prefixes of the benchmark workloads: both record formats, float and coded documents,
+    complete-depth tiles (configuration 4), several interleave factors."""
+    cfg = W.CONFIGS[cfg_id]
+    ens = W.make_ensemble(cfg, n_trees=n_trees)
+    X = W.make_docs(cfg, n_docs=n_docs)
+    plan = _check(emu, ens, X, levels=(0, 4))
+    assert plan[0] == expect["dl"] and plan[3] == expect["coded"], plan
+    if "narrow" in expect:
+        assert plan[2] == expect["narrow"], plan
