@@ -45,7 +45,9 @@ LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
     // 16 waves per workgroup; two workgroups per CU when the document tile is small
     p.wg_threads = 1024;
     p.lds_bytes = (p.xs_bytes <= kTwoWgXsBytes && !p.coded) ? kLdsPerCu / 2 : kLdsPerCu;
-    const int prefetch = p.lds_bytes == kLdsPerCu / 2 ? kPrefetchHalf : kPrefetchFull;
+    // records per thread a tile may take in the registers that prefetch it: all of the
+    // prefetch registers with two workgroups per CU, half of them (two tiles in flight) with one
+    const int prefetch = p.lds_bytes == kLdsPerCu / 2 ? kPrefetchHalf : kPrefetchFull / 2;
     p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve, prefetch * 1024 * 8) & ~15;
     p.zero_rec = p.xs_bytes + p.tile_bytes;
     // Interleave K trees per lane (latency hiding) only when a tile holds at least K rounds of
@@ -389,6 +391,10 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             }
         }
     }
+
+    // The one-workgroup-per-CU kernels copy whole windows of 1,024-record chunks: pad the images
+    // so that the window of the last tile stays inside the buffer.
+    p.images.resize(p.images.size() + size_t(kPrefetchFull / 2) * 1024, NodeRec{0u, 0u});
 
     // ---- coded models: threshold table and coding chunks ------------------------------------
     if (plan.coded) {

@@ -96,8 +96,9 @@ constexpr int kCodeChunkFeatures = 256;  // features per coding workgroup at mos
 constexpr uint32_t kMaxCode = 0xFFFEu;    // codes are 16-bit; 0xFFFF = "never right"
 
 constexpr int kLdsPerCu = 160 * 1024;  // gfx950 LDS per compute unit
-// The kernels prefetch a whole tile into registers (1,024 threads x kPrefetch records): at most
-// 6 records per thread when two workgroups share a CU (64 VGPRs each), 16 when one owns it.
+// The kernels prefetch tiles into registers (1,024 threads x kPrefetch records): at most 6
+// records per thread (one tile) when two workgroups share a CU (64 VGPRs each); 16 when one
+// owns it, as two tiles of up to 8 records per thread each (64 KiB) in flight at once.
 constexpr int kPrefetchHalf = 6;
 constexpr int kPrefetchFull = 16;
 constexpr int kXsMaxBytes = 96 * 1024; // cap on the staged document tile

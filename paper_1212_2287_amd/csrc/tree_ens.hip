@@ -51,6 +51,9 @@ int hip_fail(hipError_t e, const char *what) {
 constexpr int kNumCus = 256;
 // s_waitcnt immediate for gfx9: vmcnt(0), expcnt and lgkmcnt left at their maxima (no wait)
 constexpr int kWaitVmcnt0 = 0x0F70;
+#ifndef TREE_ENS_PREFETCH_DEPTH
+#define TREE_ENS_PREFETCH_DEPTH 2 // tiles in flight with one workgroup per CU
+#endif
 constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves)
 
 // ------------------------------------------------------------------------------------------
@@ -158,23 +161,47 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
     const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
 
-    // The next tile image is loaded into registers while the current one is walked, so the
-    // global-memory latency of a tile load is hidden. Its size comes from the current tile's
-    // header: the loop issues no scalar memory load (those share a wait counter with LDS reads
-    // and would stall the walk).
-    uint2 pre[kPre];
+    // Tile images are loaded into registers while the previous tile is walked, so the
+    // global-memory latency of a tile load is hidden; the tile loop issues no scalar memory load
+    // (those share a wait counter with LDS reads and would stall the walk).
+    //  * HALF (two workgroups per CU, walk-bound): one tile in flight, its exact record count
+    //    taken from the current tile's header.
+    //  * full CU: two tiles in flight (one per register half), each a fixed window of
+    //    kWin x kThreads records (the packer caps these tiles at that size and pads the images),
+    //    loaded unconditionally so that the compiler counts the outstanding loads exactly.
+    constexpr int kWin = treeens::kPrefetchFull / 2;
+    constexpr int kDepth = HALF ? 1 : TREE_ENS_PREFETCH_DEPTH; // tiles in flight
+    constexpr int kPreA = HALF ? kPre : kWin;
+    uint2 pa[kPreA], win[kDepth][HALF ? 1 : kWin];
+    int cur_recs = 0;
+    const int chunks = (slot_recs + kThreads - 1) / kThreads;
     auto fetch = [&](int ti, int n_rec) {
         const uint2 *src = images + int64_t(ti) * slot_recs;
 #pragma unroll
         for (int j = 0; j < kPre; ++j) {
             const int i = tid + j * kThreads;
             if (i < n_rec)
-                pre[j] = src[i];
+                pa[j] = src[i];
         }
     };
-    int cur_recs = t_lo < t_hi ? int(tile_recs[t_lo]) : 0;
-    if (t_lo < t_hi)
-        fetch(t_lo, cur_recs);
+    auto fetch_window = [&](uint2 (&dst)[kWin], int ti) {
+        // unconditional: past the last tile it reloads that tile (exact wait counts)
+        const uint2 *src = images + int64_t(min(ti, t_hi - 1)) * slot_recs + tid;
+#pragma unroll
+        for (int j = 0; j < kWin; ++j)
+            dst[j] = src[(j < chunks ? j : 0) * kThreads];
+    };
+    if constexpr (HALF) {
+        cur_recs = t_lo < t_hi ? int(tile_recs[t_lo]) : 0;
+        if (t_lo < t_hi)
+            fetch(t_lo, cur_recs);
+    } else {
+        if (t_lo < t_hi) {
+#pragma unroll
+            for (int d = 0; d < kDepth; ++d)
+                fetch_window(win[d], t_lo + d);
+        }
+    }
 
     // stage the document tile: lane = document, so each LDS write is conflict-free. The
     // workgroup size is a multiple of DL, so a thread's document (and row) is fixed and its
@@ -208,27 +235,12 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     }
 
     double acc = 0.0;
-    for (int ti = t_lo; ti < t_hi; ++ti) {
-        __syncthreads(); // the previous tile is fully walked (and the document tile written)
-        // All outstanding global loads (this tile's records, and the document rows before the
-        // first tile) land here, unconditionally: otherwise the compiler cannot prove them
-        // complete on every path and waits for them again inside the walk.
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-#pragma unroll
-        for (int j = 0; j < kPre; ++j) {
-            const int i = tid + j * kThreads;
-            if (i < cur_recs)
-                slot[i] = pre[j];
-        }
-        __syncthreads();
+    // Walk the tile image in the LDS slot.
+    auto walk_tile = [&]() {
         const uint4 h = *reinterpret_cast<const uint4 *>(hdr);
         const int ntr = __builtin_amdgcn_readfirstlane(int(h.x));
         const int complete_depth = __builtin_amdgcn_readfirstlane(int(h.y));
         const int tree_begin = __builtin_amdgcn_readfirstlane(int(h.z));
-        cur_recs = __builtin_amdgcn_readfirstlane(int(h.w));
-        if (ti + 1 < t_hi)
-            fetch(ti + 1, cur_recs);
-
         // Walker w takes groups w, w + n_walkers, ... of K consecutive trees (the packer sizes
         // tiles to a multiple of n_walkers * K trees where it can, and pads the header's root
         // copies to a multiple of K with the zero record).
@@ -344,6 +356,46 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             walk(std::true_type{});
         else
             walk(std::false_type{});
+    };
+    if constexpr (HALF) {
+        for (int ti = t_lo; ti < t_hi; ++ti) {
+            __syncthreads(); // the previous tile is fully walked (and the document tile written)
+            // All outstanding global loads (this tile's records, and the document rows before
+            // the first tile) land here, unconditionally: otherwise the compiler cannot prove
+            // them complete on every path and waits for them again inside the walk.
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+#pragma unroll
+            for (int j = 0; j < kPre; ++j) {
+                const int i = tid + j * kThreads;
+                if (i < cur_recs)
+                    slot[i] = pa[j];
+            }
+            __syncthreads();
+            cur_recs = __builtin_amdgcn_readfirstlane(int(hdr[3])); // the next tile's size
+            if (ti + 1 < t_hi)
+                fetch(ti + 1, cur_recs);
+            walk_tile();
+        }
+    } else {
+        // the document rows (loaded after the first two tiles) land before the first barrier
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        auto write_window = [&](const uint2 (&src)[kWin]) {
+#pragma unroll
+            for (int j = 0; j < kWin; ++j)
+                if (j < chunks)
+                    slot[tid + j * kThreads] = src[j];
+        };
+        for (int ti = t_lo; ti < t_hi; ti += kDepth) {
+#pragma unroll
+            for (int d = 0; d < kDepth; ++d) {
+                __syncthreads(); // the previous tile is fully walked (and the document tile written)
+                write_window(win[d]);
+                __syncthreads();
+                fetch_window(win[d], ti + d + kDepth);
+                if (d == 0 || ti + d < t_hi)
+                    walk_tile();
+            }
+        }
     }
     if constexpr (!LEAVES) {
         __syncthreads();

@@ -91,6 +91,18 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
     const int64_t slot = p.level_slot_recs[level];
     if (slot * 8 > pl.tile_bytes)
         return bad("image stride exceeds the LDS slot");
+    // prefetch capacity: one tile in 6 records per thread with two workgroups per CU; windows
+    // of whole 1,024-record chunks, at most 8 per tile, with one
+    if (pl.lds_bytes == treeens::kLdsPerCu) {
+        const int64_t chunks = (slot + 1023) / 1024;
+        if (chunks > treeens::kPrefetchFull / 2 || chunks * 1024 * 8 > pl.tile_bytes)
+            return bad("tile window exceeds the registers or the LDS slot");
+        const int64_t last = p.level_image_off[level] + int64_t(t1 - t0 - 1) * slot;
+        if (t1 > t0 && last + chunks * 1024 > int64_t(p.images.size()))
+            return bad("the last tile's window reads past the images");
+    } else if (slot > int64_t(treeens::kPrefetchHalf) * 1024) {
+        return bad("tile image exceeds the prefetch registers");
+    }
     std::vector<int32_t> seen(size_t(n_trees), 0);
     for (int64_t i = 0; i < n_docs * n_trees; i++)
         leaf_ids[i] = -1;
