@@ -226,6 +226,64 @@ def pmc_probe(T, W) -> int:
     return 0
 
 
+def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) -> int:
+    """Per-launch HBM traffic of the scoring kernel from two rocprofv3 --pmc runs of
+    --pmc-probe (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what the same
+    counter reads for the probe's plain device copy of the feature matrix (a kernel that reads
+    and writes exactly that many bytes). Runs on the host; writes profiles/hbm_traffic.json."""
+    import csv
+    import workloads as W
+    cfg = W.CONFIGS[HEADLINE_CFG]
+    copy_bytes = cfg.n_docs * cfg.n_features * 4
+
+    def per_kernel(path, counter):
+        copies, scores = [], []
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                v = float(r["Counter_Value"])
+                if "copyBuffer" in r["Kernel_Name"]:
+                    copies.append(v)
+                elif "score_kernel" in r["Kernel_Name"]:
+                    scores.append(v)
+        if not copies or not scores:
+            raise SystemExit(f"{path}: no copy or scoring dispatch with {counter}")
+        return max(copies), statistics.mean(scores), len(scores)
+
+    f_copy, f_score, n_f = per_kernel(fetch_csv, "FETCH_SIZE")
+    w_copy, w_score, n_w = per_kernel(write_csv, "WRITE_SIZE")
+    f_factor = copy_bytes / 1024.0 / f_copy
+    w_factor = copy_bytes / 1024.0 / w_copy
+    read_b = f_score * 1024.0 * f_factor
+    write_b = w_score * 1024.0 * w_factor
+    rec = {
+        "kernel_hash": kernel_hash(),
+        "note": (f"HBM bytes per launch of the scoring kernel on {cfg.name} ({cfg.n_docs} docs), mean "
+                 f"of {n_f} (FETCH_SIZE) and {n_w} (WRITE_SIZE) dispatches, each counter scaled by "
+                 f"its reading on a plain device copy of {copy_bytes} bytes (FETCH_SIZE {f_copy:.1f} "
+                 f"KiB, WRITE_SIZE {w_copy:.1f} KiB for {copy_bytes / 1024:.1f} KiB moved)."),
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o fetch -- python -u bench.py --pmc-probe",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o write -- python -u bench.py --pmc-probe",
+            "python bench.py --write-traffic gpurun_out/pmc_fetch/fetch_counter_collection.csv "
+            "gpurun_out/pmc_write/write_counter_collection.csv",
+        ],
+        "calibration": {"fetch_factor": f_factor, "write_factor": w_factor},
+        "workloads": {cfg.name: {
+            "fetch_kib_raw": f_score, "write_kib_raw": w_score,
+            "hbm_read_bytes_per_launch": int(round(read_b)),
+            "hbm_write_bytes_per_launch": int(round(write_b)),
+            "hbm_bytes_per_launch": int(round(read_b + write_b)),
+            "algorithmic_hbm_bytes": cfg.n_docs * cfg.n_features * 4 + cfg.n_docs * 4,
+        }},
+    }
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    log(f"wrote {out_path}: {read_b / 1e6:.1f} MB read + {write_b / 1e6:.2f} MB written per launch")
+    return 0
+
+
 def _cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as fh:
@@ -248,7 +306,12 @@ def main() -> int:
                     help="for rocprofv3 --pmc runs: one device copy of the headline workload's "
                          "feature matrix (a kernel of known traffic, for calibration) followed by "
                          "3 predicts; prints nothing else")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="host only: turn the counter CSVs of the two --pmc-probe runs into "
+                         "profiles/hbm_traffic.json")
     args = ap.parse_args()
+    if args.write_traffic:
+        return write_traffic(*args.write_traffic)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this scorer runs on a single MI355X and has no "

@@ -86,8 +86,13 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
  *   scores      device, float [n_docs]: the sum of the reached leaf values, accumulated in
  *               double precision and rounded once to float.
  *
- * Kernel faults surface at the caller's next synchronisation with the stream. Small batches
- * use a stream-ordered scratch allocation (hipMallocAsync / hipFreeAsync on `stream`).
+ * Kernel faults surface at the caller's next synchronisation with the stream. When the launch
+ * splits document blocks over several workgroups (small batches, and the blocks of a last,
+ * partial round of workgroups) their fp64 partial sums go to a 1 MiB scratch buffer owned by
+ * the handle (calls on different streams are ordered by an event while they share it), or, if
+ * larger, to a stream-ordered allocation (hipMallocAsync / hipFreeAsync on `stream`). Models
+ * with threshold-coded features also take a stream-ordered buffer of n_docs x min_features
+ * 16-bit codes for the duration of the call.
  */
 int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
                      int32_t n_features, float *scores);
@@ -107,7 +112,8 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
  *   n_trees        number of trees.
  *   min_features   1 + the largest feature id any node reads (0 if there is none).
  *   max_depth      edges on the longest root-to-leaf path over all trees.
- *   packed_bytes   bytes of node records on the device.
+ *   packed_bytes   bytes of node records (8 per node); the device also holds the tile images
+ *                  built from them (one set per tiling granularity).
  *   n_tiles        LDS tiles the trees are streamed in for a large batch.
  *   docs_per_block documents a workgroup stages in LDS (a power of two from 8 to 64).
  */

@@ -1,22 +1,24 @@
 // tree_ens.hip -- gfx950 kernels and the C ABI of the tree-ensemble scorer.
 //
-// Work decomposition (one kernel launch per predict call):
+// Work decomposition (one scoring launch per predict call):
 //   * a workgroup owns a block of DL consecutive documents and stages their features into LDS
-//     once, feature-major ([column][DL] floats, column 0 = NaN, column f+1 = feature f), so a
+//     once, feature-major ([column][DL] values, column 0 = NaN, column f+1 = feature f), so a
 //     lane's read of any feature of its own document is a conflict-free LDS access whatever
 //     feature the lane's current node names;
-//   * the trees are streamed through LDS in tiles (runs of whole trees, packed node records);
-//   * lanes are documents; each group of DL lanes (a "walker") walks one tree at a time for its
-//     DL documents; with one workgroup per CU each lane interleaves K = 2 independent trees so
-//     that their LDS latencies overlap (the vectorisation idea of Section 3, VPred, applied
-//     to trees instead of instances);
+//   * the trees are streamed through an LDS slot in tiles: self-describing images (header,
+//     root copies, node records with absolute child links) copied global -> registers -> LDS,
+//     the next one loading while the current one is walked;
+//   * lanes are documents; each group of DL lanes (a "walker", a whole wave when DL = 64) walks
+//     K trees of the tile at a time so that their LDS latencies overlap (the vectorisation
+//     idea of Section 3, VPred, applied to trees instead of instances);
 //   * each step is the branch-free predicated update of Section 3 (Pred) over explicit,
 //     sibling-adjacent children: idx = left(idx) + (x[fid(idx)] >= theta(idx)); a wave stops
 //     as soon as all its lanes sit on leaves (trees are unbalanced; most paths are short);
 //   * leaf values are summed per lane in double precision, then reduced across walkers through
 //     LDS in a fixed order and rounded once to float.
-// Small batches split the tiles over a second grid dimension and reduce the per-split partial
-// sums in a second, tiny kernel (fixed order, so results are deterministic).
+// Blocks of a last, partial round of workgroups (and every block of a small batch) are split
+// over the tiles; the per-split partial sums are reduced by a second, tiny kernel in a fixed
+// order, so results are deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
