@@ -47,10 +47,17 @@ def log(msg: str) -> None:
 
 
 def kernel_hash() -> str:
+    """Hash of the kernel and packer sources with comments and whitespace removed: stored
+    counter results stay valid across comment edits and lapse on any code change."""
+    import re
     h = hashlib.sha256()
-    for p in (KERNEL_SRC, os.path.join(ROOT, "paper_1212_2287_amd", "csrc", "pack.cpp")):
-        with open(p, "rb") as fh:
-            h.update(fh.read())
+    for p in (KERNEL_SRC, os.path.join(ROOT, "paper_1212_2287_amd", "csrc", "pack.cpp"),
+              os.path.join(ROOT, "paper_1212_2287_amd", "csrc", "pack.hpp")):
+        with open(p) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update("".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
