@@ -205,28 +205,60 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         }
     }
 
-    // stage the document tile: lane = document, so each LDS write is conflict-free. The
-    // workgroup size is a multiple of DL, so a thread's document (and row) is fixed and its
-    // columns step by kThreads / DL. Loads are unconditional (clamped to a valid element) so
-    // that the eight of a pass are in flight together before any is written.
+    // Stage the document tile: lane = document, so each LDS write is conflict-free (bank =
+    // lane). The workgroup size is a multiple of DL, so a thread's document (and row) is fixed
+    // and it takes every (kThreads / DL)-th group of columns. When rows are 16-byte aligned a
+    // lane reads 16 bytes of its row at a time (4 floats or 8 codes: a quarter or an eighth of
+    // the strided row reads), else one value. Loads are unconditional (clamped to the row) so
+    // that a pass's loads are in flight together before any is written.
     {
         constexpr int kColStep = kThreads / DL;
         constexpr int kUnroll = 8;
+        constexpr int kVec = 16 / int(sizeof(Elem)); // values per 16-byte load
         const int64_t doc = doc0 + dl;
         const bool live = doc < n_docs;
         const Elem *row = X + (live ? doc : n_docs - 1) * int64_t(n_features);
         const Elem leaf_col = CODED ? Elem(0) : Elem(__builtin_nanf(""));
-        const int last = n_cols > 0 ? n_cols - 1 : 0;
-        for (int c0 = tid / DL; c0 <= n_cols; c0 += kColStep * kUnroll) {
-            Elem v[kUnroll];
+        if (tid < DL)
+            xs[dl] = leaf_col;
+        const bool vec = (n_features % kVec) == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0;
+        if (vec) {
+            const uint4 *row4 = reinterpret_cast<const uint4 *>(row);
+            const int n_groups = (n_cols + kVec - 1) / kVec; // within the row: n_features % kVec == 0
+            const int last = n_groups > 0 ? n_groups - 1 : 0;
+            constexpr int kVecUnroll = 4;
+            for (int q0 = tid / DL; q0 < n_groups; q0 += kColStep * kVecUnroll) {
+                uint4 v[kVecUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                v[u] = row[min(max(c0 + u * kColStep - 1, 0), last)];
+                for (int u = 0; u < kVecUnroll; ++u)
+                    v[u] = row4[min(q0 + u * kColStep, last)];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int c = c0 + u * kColStep;
-                if (c <= n_cols)
-                    xs[c * DL + dl] = c == 0 ? leaf_col : (live ? v[u] : Elem(0));
+                for (int u = 0; u < kVecUnroll; ++u) {
+                    const int q = q0 + u * kColStep;
+                    if (q < n_groups) {
+                        const Elem *e = reinterpret_cast<const Elem *>(&v[u]);
+#pragma unroll
+                        for (int k = 0; k < kVec; ++k) {
+                            const int c = q * kVec + k + 1; // tile column of feature q * kVec + k
+                            if (c <= n_cols)
+                                xs[c * DL + dl] = live ? e[k] : Elem(0);
+                        }
+                    }
+                }
+            }
+        } else {
+            const int last = n_cols > 0 ? n_cols - 1 : 0;
+            for (int c0 = tid / DL + 1; c0 <= n_cols; c0 += kColStep * kUnroll) {
+                Elem v[kUnroll];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+                    v[u] = row[min(c0 + u * kColStep - 1, last)];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const int c = c0 + u * kColStep;
+                    if (c <= n_cols)
+                        xs[c * DL + dl] = live ? v[u] : Elem(0);
+                }
             }
         }
     }
