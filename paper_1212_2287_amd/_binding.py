@@ -124,6 +124,11 @@ def tree_ens_create(tree_offsets, feature, threshold, left, right, value,
 def _stream_of(t, stream) -> Optional[int]:
     import torch
     if stream is None:
+        # the raw handle of torch's current stream on X's device (cheaper than building a
+        # Stream object per call)
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        if raw is not None:
+            return raw(t.device.index)
         return torch.cuda.current_stream(t.device).cuda_stream
     return int(getattr(stream, "cuda_stream", stream))
 

@@ -346,6 +346,15 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     const int shift = plan.narrow ? 16 : kWideChildShift;
     const uint32_t col_mask = plan.narrow ? kNarrowColMask : kWideColMask;
     const uint32_t zero_addr = uint32_t(plan.zero_rec);
+    for (int k = 0; k < kTileLevels; k++) {
+        for (int32_t i = p.level_begin[k]; i < p.level_begin[k + 1]; i++) {
+            const Tile &tl = p.tiles[size_t(i)];
+            const int32_t r = (tl.tree_end - tl.tree_begin + round - 1) / round;
+            p.level_max_rounds[k] = std::max(p.level_max_rounds[k], r);
+            if (k == 0)
+                p.total_rounds += r;
+        }
+    }
     p.tile_recs.resize(p.tiles.size());
     for (size_t i = 0; i < p.tiles.size(); i++) {
         const Tile &tl = p.tiles[i];

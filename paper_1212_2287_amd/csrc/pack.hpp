@@ -122,6 +122,10 @@ struct Packed {
     int64_t level_image_off[kTileLevels] = {}; // first record of each tiling's images
     int32_t level_slot_recs[kTileLevels] = {}; // image stride of each tiling, in records
     std::vector<uint32_t> tile_recs;           // [tiles] records to copy for each tile
+    // walker rounds (groups of walkers x interleave trees) of the fullest tile of each tiling,
+    // and of all tiles of tiling 0: the launch planner's unit of time
+    int32_t level_max_rounds[kTileLevels] = {};
+    int64_t total_rounds = 0;
     // coded models only
     std::vector<float> code_table;         // T_0, T_1, ... concatenated
     std::vector<uint32_t> code_table_off;  // [n_cols + 1] start of T_f in code_table

@@ -460,8 +460,19 @@ __global__ void reduce_partials_thread_kernel(const double *__restrict__ partial
                                               int64_t n_docs, float *__restrict__ scores) {
     const int64_t d = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (d < n_docs) {
+        // eight independent loads in flight, then summed in split order
         double s = 0.0;
-        for (int k = 0; k < n_splits; ++k)
+        int k = 0;
+        for (; k + 8 <= n_splits; k += 8) {
+            double v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                v[u] = partials[int64_t(k + u) * n_docs + d];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                s += v[u];
+        }
+        for (; k < n_splits; ++k)
             s += partials[int64_t(k) * n_docs + d];
         scores[d] = float(s);
     }
@@ -581,6 +592,8 @@ struct tree_ens {
     int64_t n_nodes = 0;
     treeens::LdsPlan plan{};
     int32_t level_begin[treeens::kTileLevels + 1] = {};
+    int32_t level_max_rounds[treeens::kTileLevels] = {}; // walker rounds of the fullest tile
+    int64_t total_rounds = 0;                            // walker rounds of all tiles, tiling 0
     int64_t level_image_off[treeens::kTileLevels] = {};
     int32_t level_slot_recs[treeens::kTileLevels] = {};
     uint2 *d_images = nullptr;      // tile images of every tiling
@@ -602,6 +615,12 @@ struct tree_ens {
     mutable std::mutex scratch_mu;
     mutable hipStream_t scratch_stream = nullptr;
     mutable bool scratch_used = false;
+    // launch shape of the last batch size seen (callers usually repeat one batch size)
+    mutable std::mutex shape_mu;
+    mutable int64_t shape_blocks = -1;
+    mutable int shape_level = 0;
+    mutable int64_t shape_head = 0;
+    mutable int shape_splits = 1;
 };
 
 namespace {
@@ -637,14 +656,19 @@ hipError_t upload(T **dst, const std::vector<T> &src) {
 
 // Launch shape for a batch of n_blocks document blocks: a tiling level, a number of head
 // blocks walked whole by one workgroup each, and the split count of the remaining (tail)
-// blocks, each split over that many workgroups that walk a contiguous share of the tiles. The
-// estimated makespan, in units of one block walking all trees, is
-//     head rounds * (1 + per-workgroup cost)
-//     + ceil(tail blocks * splits / resident workgroups) * (largest share + per-workgroup cost)
-//     + (splits > 1 ? cost of the partial-sum reduction : 0).
-// Candidates: everything split uniformly (no head; small batches spread over the whole GPU),
-// and whole rounds as head with the remainder split to fill the last round (a batch of 1,563
-// blocks on 512 resident workgroups would otherwise run a fourth round at 5% occupancy).
+// blocks, each split over that many workgroups that walk a contiguous share of the tiles. Time
+// is counted in walker rounds (every walker walking one group of K trees: a tile takes as long
+// as its fullest round, so tiles smaller than one round save nothing). With W resident
+// workgroups, the estimated makespan in units of one block walking all trees is
+//     head / W * (1 + c_wg)
+//     + ceil(tail blocks * splits / W) * (share + c_wg)
+//     + (splits > 1 ? c_reduce : 0) + tiny * workgroups,
+// where share = ceil(tiles / splits) * rounds of the fullest tile / rounds of all tiles, c_wg
+// is the per-workgroup cost (staging, prologue, epilogue) and the last term prefers fewer
+// workgroups (fewer partial sums) among equal estimates. Candidates: everything split
+// uniformly (no head; small batches spread over the GPU), and whole rounds of workgroups as
+// head with the remainder split to fill the last round (a batch of 1,563 blocks on 512 resident
+// workgroups would otherwise run a fourth round at 5% occupancy).
 struct LaunchShape {
     int level = 0;
     int64_t head = 0;
@@ -654,17 +678,19 @@ struct LaunchShape {
 LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
     constexpr double kItemCost = 0.2;    // staging, prologue and restaging of one workgroup (measured)
     constexpr double kReduceCost = 0.05; // the second kernel
+    constexpr double kPerWorkgroup = 1e-6;
     const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
     const int64_t slots = int64_t(kNumCus) * wg_per_cu;
+    const double total = double(std::max<int64_t>(h->total_rounds, 1));
     double best = 1e300;
     LaunchShape pick;
     auto consider = [&](int level, int64_t head, int sp) {
         const int nt = h->level_begin[level + 1] - h->level_begin[level];
         const int64_t tail = n_blocks - head;
-        const double share = double((nt + sp - 1) / sp) / nt;
+        const double share = double((nt + sp - 1) / sp) * h->level_max_rounds[level] / total;
         const double cost = double(head / slots) * (1.0 + kItemCost) +
                             double((tail * sp + slots - 1) / slots) * (share + kItemCost) +
-                            (sp > 1 ? kReduceCost : 0.0);
+                            (sp > 1 ? kReduceCost : 0.0) + kPerWorkgroup * double(head + tail * sp);
         if (cost < best - 1e-9) {
             best = cost;
             pick = LaunchShape{level, head, sp};
@@ -731,7 +757,19 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const int64_t n_blocks = (n_docs + dl - 1) / dl;
     if (n_blocks > 0x7fffffff)
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
-    const LaunchShape shape = choose_launch(h, n_blocks);
+    LaunchShape shape;
+    {
+        std::lock_guard<std::mutex> lock(h->shape_mu);
+        if (h->shape_blocks == n_blocks) {
+            shape = LaunchShape{h->shape_level, h->shape_head, h->shape_splits};
+        } else {
+            shape = choose_launch(h, n_blocks);
+            h->shape_blocks = n_blocks;
+            h->shape_level = shape.level;
+            h->shape_head = shape.head;
+            h->shape_splits = shape.splits;
+        }
+    }
     const int level = shape.level, splits = shape.splits;
     const int64_t tail_docs = n_docs - shape.head * dl;
     const int64_t n_wgs = shape.head + (n_blocks - shape.head) * splits;
@@ -861,6 +899,8 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
     std::memcpy(h->level_begin, p.level_begin, sizeof h->level_begin);
     hipError_t e = hipGetDevice(&h->device);
     std::memcpy(h->level_image_off, p.level_image_off, sizeof h->level_image_off);
+    std::memcpy(h->level_max_rounds, p.level_max_rounds, sizeof h->level_max_rounds);
+    h->total_rounds = p.total_rounds;
     std::memcpy(h->level_slot_recs, p.level_slot_recs, sizeof h->level_slot_recs);
     std::vector<uint2> images(p.images.size());
     if (!p.images.empty())
