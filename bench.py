@@ -10,6 +10,7 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   value        doc*tree evaluations per second (whole job, one GPU)
   ns_per_doc   wall time per document
   latency_100doc_us   one 100-document batch: host wall clock of predict + stream sync
+  rerank       per-query top-20 of the headline workload's query groups (Section 6's reranking)
   roofline     the scoring kernel against the LDS roofline (node bytes)
   roofline_hbm the same kernel against HBM (feature + score bytes)
   cpu_baseline the oracle on the host cores, same workload
@@ -186,6 +187,36 @@ def latency_100(model, Xd, reps=300):
             "device_us_per_call": ev0.elapsed_time(ev1) * 1e3 / reps, "reps": reps}
 
 
+def rerank(T, W, model, Xd, cfg, k=20, reps=50):
+    """Section 6's reranking step on the headline workload: every query's candidates (20-200
+    documents) scored and cut to the best k, in one call (tree_ens_predict_topk), and the top-k
+    kernel alone over already computed scores (tree_ens_topk)."""
+    import numpy as np
+    import torch
+    sizes = W.make_query_groups(cfg)
+    off = torch.from_numpy(np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)).to("cuda")
+    scores, idx, vals = model.predict_topk(Xd, off, k)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        T.tree_ens_topk(scores, off, k, idx, vals)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(reps):
+        T.tree_ens_topk(scores, off, k, idx, vals)
+    ev1.record()
+    torch.cuda.synchronize()
+    topk_us = ev0.elapsed_time(ev1) * 1e3 / reps
+    ev0.record()
+    for _ in range(reps):
+        model.predict_topk(Xd, off, k)
+    ev1.record()
+    torch.cuda.synchronize()
+    fused_ms = ev0.elapsed_time(ev1) / reps
+    return {"queries": int(len(sizes)), "k": k, "docs": int(cfg.n_docs),
+            "topk_us": topk_us, "predict_topk_ms": fused_ms,
+            "queries_per_s": len(sizes) / (fused_ms * 1e-3)}
+
+
 def cpu_baseline(W, cfg_id, budget_s=10.0):
     import numpy as np
     import oracle
@@ -337,6 +368,9 @@ def main() -> int:
     rec, model, ens, Xd, out = measure_config(T, W, HEADLINE_CFG, args.steps, args.warmup)
     lat = latency_100(model, Xd)
     log(f"100-doc batch: median {lat['median_us']:.1f} us, device {lat['device_us_per_call']:.1f} us/call")
+    rr = rerank(T, W, model, Xd, W.CONFIGS[HEADLINE_CFG])
+    log(f"rerank top-{rr['k']} of {rr['queries']} queries: top-k kernel {rr['topk_us']:.1f} us, "
+        f"score + top-k {rr['predict_topk_ms']:.3f} ms")
     model.close()
     del Xd, out
     torch.cuda.empty_cache()
@@ -363,7 +397,7 @@ def main() -> int:
                    "n_trees": cfg.n_trees, "n_docs": cfg.n_docs, "n_features": cfg.n_features,
                    "docs_per_block": rec["model"]["docs_per_block"]},
         "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"],
-        "latency_100doc_us": lat, "visits": rec["visits"],
+        "latency_100doc_us": lat, "rerank": rr, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
         "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
     }

@@ -108,6 +108,39 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
                             int32_t n_features, int32_t *leaf_ids);
 
 /*
+ * tree_ens_topk -- per-query top-k reranking of scores (Section 6: a query's candidate
+ * documents, e.g. 200 of them, are scored and reranked into the final list of the best 20).
+ *
+ *   stream        hipStream_t the work is enqueued on (0 = null stream); returns without waiting.
+ *   scores        device, float [n_docs].
+ *   n_docs        >= 0 and <= INT32_MAX (indices are int32).
+ *   group_offsets device, int64 [n_groups+1]: query g owns documents [off[g], off[g+1]).
+ *                 Offsets are clamped into [0, n_docs] and a group ending before it starts is
+ *                 empty, so ill-formed offsets never read outside `scores`.
+ *   n_groups      >= 0; 0 returns TREE_ENS_OK without a launch.
+ *   k             1 <= k <= 1024.
+ *   top_idx       device, int32 [n_groups][k] row-major: the k first documents of each group
+ *                 (absolute document indices). Order: higher score first; equal scores
+ *                 (-0.0 equals +0.0) by increasing document index; NaN scores after every
+ *                 number. Positions past a group's size hold -1.
+ *   top_scores    device, float [n_groups][k], or NULL: the scores of top_idx (NaN past a
+ *                 group's size).
+ * Returns TREE_ENS_E_ARG for a count or k out of range or a NULL required pointer.
+ */
+int tree_ens_topk(void *stream, const float *scores, int64_t n_docs, const int64_t *group_offsets,
+                  int64_t n_groups, int32_t k, int32_t *top_idx, float *top_scores);
+
+/*
+ * tree_ens_predict_topk -- tree_ens_predict into `scores` followed by tree_ens_topk over it,
+ * both enqueued on `stream` (scoring and reranking of query candidates in one call). Arguments
+ * as for those two functions; `scores` is a device buffer of n_docs floats the caller owns
+ * (it receives the scores).
+ */
+int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                          int32_t n_features, const int64_t *group_offsets, int64_t n_groups,
+                          int32_t k, float *scores, int32_t *top_idx, float *top_scores);
+
+/*
  * tree_ens_info -- facts about a packed model; every output pointer may be NULL.
  *   n_trees        number of trees.
  *   min_features   1 + the largest feature id any node reads (0 if there is none).

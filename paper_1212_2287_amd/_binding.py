@@ -65,6 +65,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tree_ens_predict.argtypes = [P, P, P, i64, i32, P]
     lib.tree_ens_predict_leaves.restype = ctypes.c_int
     lib.tree_ens_predict_leaves.argtypes = [P, P, P, i64, i32, P]
+    lib.tree_ens_topk.restype = ctypes.c_int
+    lib.tree_ens_topk.argtypes = [P, P, i64, P, i64, i32, P, P]
+    lib.tree_ens_predict_topk.restype = ctypes.c_int
+    lib.tree_ens_predict_topk.argtypes = [P, P, P, i64, i32, P, i64, i32, P, P, P]
     lib.tree_ens_info.restype = ctypes.c_int
     lib.tree_ens_info.argtypes = [P, P, P, P, P, P, P]
     lib.tree_ens_destroy.restype = None
@@ -176,6 +180,68 @@ def tree_ens_predict_leaves(h, X, leaf_ids=None, stream=None):
     return leaf_ids
 
 
+def _topk_outputs(device, n_groups, k, top_idx, top_scores):
+    import torch
+    if top_idx is None:
+        top_idx = torch.empty((n_groups, k), dtype=torch.int32, device=device)
+    elif top_idx.dtype != torch.int32 or top_idx.numel() < n_groups * k or not top_idx.is_contiguous() \
+            or top_idx.device != device:
+        raise TypeError("top_idx must be a contiguous int32 tensor of n_groups*k entries on the device")
+    if top_scores is None:
+        top_scores = torch.empty((n_groups, k), dtype=torch.float32, device=device)
+    elif top_scores.dtype != torch.float32 or top_scores.numel() < n_groups * k or \
+            not top_scores.is_contiguous() or top_scores.device != device:
+        raise TypeError("top_scores must be a contiguous float32 tensor of n_groups*k entries")
+    return top_idx, top_scores
+
+
+def _check_offsets(group_offsets, device):
+    import torch
+    if not isinstance(group_offsets, torch.Tensor) or group_offsets.dtype != torch.int64 or \
+            group_offsets.dim() != 1 or not group_offsets.is_contiguous() or \
+            group_offsets.device != device or group_offsets.numel() < 1:
+        raise TypeError("group_offsets must be a contiguous int64 [n_groups + 1] tensor on the device")
+    return group_offsets.numel() - 1
+
+
+def tree_ens_topk(scores, group_offsets, k: int, top_idx=None, top_scores=None, stream=None):
+    """Per-group top-k of device float32 ``scores`` over the groups of ``group_offsets`` (device
+    int64 [n_groups + 1]): (top_idx int32 [n_groups, k], top_scores float32 [n_groups, k])."""
+    import torch
+    if not isinstance(scores, torch.Tensor) or scores.device.type != "cuda" or \
+            scores.dtype != torch.float32 or scores.dim() != 1 or not scores.is_contiguous():
+        raise TypeError("scores must be a contiguous float32 CUDA (HIP) vector")
+    n_groups = _check_offsets(group_offsets, scores.device)
+    top_idx, top_scores = _topk_outputs(scores.device, n_groups, k, top_idx, top_scores)
+    rc = load_library().tree_ens_topk(_stream_of(scores, stream), scores.data_ptr() if scores.numel() else None,
+                                      scores.numel(), group_offsets.data_ptr(), n_groups, int(k),
+                                      top_idx.data_ptr() if n_groups else None,
+                                      top_scores.data_ptr() if n_groups else None)
+    _check(rc, "tree_ens_topk")
+    return top_idx, top_scores
+
+
+def tree_ens_predict_topk(h, X, group_offsets, k: int, scores=None, top_idx=None, top_scores=None,
+                          stream=None):
+    """Scores of ``X`` and their per-group top-k in one call: (scores, top_idx, top_scores)."""
+    import torch
+    _check_docs(X)
+    n_docs, n_feat = X.shape
+    if scores is None:
+        scores = torch.empty(n_docs, dtype=torch.float32, device=X.device)
+    elif scores.dtype != torch.float32 or scores.numel() < n_docs or not scores.is_contiguous() \
+            or scores.device != X.device:
+        raise TypeError("scores must be a contiguous float32 tensor of n_docs entries on X's device")
+    n_groups = _check_offsets(group_offsets, X.device)
+    top_idx, top_scores = _topk_outputs(X.device, n_groups, k, top_idx, top_scores)
+    rc = load_library().tree_ens_predict_topk(
+        h, _stream_of(X, stream), X.data_ptr() if n_docs else None, n_docs, n_feat,
+        group_offsets.data_ptr(), n_groups, int(k), scores.data_ptr() if n_docs else None,
+        top_idx.data_ptr() if n_groups else None, top_scores.data_ptr() if n_groups else None)
+    _check(rc, "tree_ens_predict_topk")
+    return scores, top_idx, top_scores
+
+
 def tree_ens_info(h) -> dict:
     lib = load_library()
     nt, mf, md, nt2, dpb = (ctypes.c_int32() for _ in range(5))
@@ -222,6 +288,10 @@ class TreeEnsemble:
 
     def predict_leaves(self, X, out=None, stream=None):
         return tree_ens_predict_leaves(self.handle, X, out, stream)
+
+    def predict_topk(self, X, group_offsets, k: int, stream=None):
+        """(scores, top_idx, top_scores): scores of X and each query group's k best documents."""
+        return tree_ens_predict_topk(self.handle, X, group_offsets, k, stream=stream)
 
     def info(self) -> dict:
         return tree_ens_info(self.handle)

@@ -37,7 +37,8 @@ def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
     run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", *[f"-D{d}" for d in defines], "-c",
          os.path.join(CSRC, "pack.cpp"), "-o", obj])
     run([_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC, "-shared",
-         os.path.join(CSRC, "tree_ens.hip"), "-x", "none", obj, "-o", tmp])
+         os.path.join(CSRC, "tree_ens.hip"), os.path.join(CSRC, "topk.hip"), "-x", "none", obj,
+         "-o", tmp])
     os.replace(tmp, out)
     os.remove(obj)
     return out

@@ -32,6 +32,7 @@
 #include <vector>
 
 #include "pack.hpp"
+#include "status.hpp"
 #include "tree_ens.h"
 
 using treeens::NodeRec;
@@ -581,6 +582,14 @@ ScoreFn pick_kernel(const treeens::LdsPlan &p) {
 
 } // namespace
 
+namespace treeens {
+int set_error(int code, const std::string &message) {
+    g_err = message;
+    return code;
+}
+void clear_error() { g_err.clear(); }
+} // namespace treeens
+
 // ------------------------------------------------------------------------------------------
 // handle
 // ------------------------------------------------------------------------------------------
@@ -968,6 +977,15 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
         return hip_fail(g.err, "hipSetDevice");
     return launch_predict<true>(h, reinterpret_cast<hipStream_t>(stream), X, n_docs, n_features,
                                 nullptr, leaf_ids);
+}
+
+int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                          int32_t n_features, const int64_t *group_offsets, int64_t n_groups,
+                          int32_t k, float *scores, int32_t *top_idx, float *top_scores) {
+    int rc = tree_ens_predict(h, stream, X, n_docs, n_features, scores);
+    if (rc != TREE_ENS_OK)
+        return rc;
+    return tree_ens_topk(stream, scores, n_docs, group_offsets, n_groups, k, top_idx, top_scores);
 }
 
 int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features, int32_t *max_depth,
