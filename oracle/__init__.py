@@ -6,7 +6,8 @@ this package. The GPU library never loads it and shares no code with it.
 * ``liboracle.so`` (built from ``oracle.c`` with plain ``gcc -O2 -fopenmp``): the definition of
   the score written out -- a branching walk, a predicated walk and the literal padded
   breadth-first predicated walk (Section 3 of the paper), leaf values summed in double precision
-  in tree order (Section 5.3).
+  in tree order (Section 5.3); and the feature-access trace, the distinct features each
+  document's walks compare (Section 6, Table 4).
 * ``brute.py``: a path-conjunction brute force for tiny inputs (a document reaches leaf l iff
   every predicate on the root-to-l path holds), summed with ``math.fsum``.
 
@@ -48,6 +49,8 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_score.argtypes = [i32, P, P, P, P, P, P, P, i64, i32, i32, i32, i32, P, P, P]
     lib.oracle_score_padded.restype = ctypes.c_int
     lib.oracle_score_padded.argtypes = [i32, P, P, P, P, P, P, P, i64, i32, i32, i32, P, P]
+    lib.oracle_feature_usage.restype = ctypes.c_int
+    lib.oracle_feature_usage.argtypes = [i32, P, P, P, P, P, P, i64, i32, i32, i32, P, P]
     lib.oracle_max_threads.restype = ctypes.c_int
     lib.oracle_max_threads.argtypes = []
     return lib
@@ -121,6 +124,23 @@ def score_padded(ens, X: np.ndarray, rule: int = RULE_GE, max_depth: int = 20,
     if rc != 0:
         raise OracleError(f"oracle_score_padded failed with code {rc}")
     return scores, leaves
+
+
+def feature_usage(ens, X: np.ndarray, rule: int = RULE_GE, threads: int = 0,
+                  lib: Optional[ctypes.CDLL] = None):
+    """Features examined per document over all trees (Section 6, Table 4): (counts int32
+    [n_docs], masks uint32 [n_docs][(n_features + 31) // 32], bit f % 32 of word f // 32)."""
+    lib = lib or load()
+    off, fe, th, le, ri, _ = _model_arrays(ens)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    n_docs, n_feat = X.shape
+    counts = np.empty(n_docs, dtype=np.int32)
+    masks = np.empty((n_docs, (n_feat + 31) // 32), dtype=np.uint32)
+    rc = lib.oracle_feature_usage(ens.n_trees, _p(off), _p(fe), _p(th), _p(le), _p(ri), _p(X), n_docs,
+                                  n_feat, rule, threads, _p(counts), _p(masks))
+    if rc != 0:
+        raise OracleError(f"oracle_feature_usage failed with code {rc}")
+    return counts, masks
 
 
 def max_threads(lib: Optional[ctypes.CDLL] = None) -> int:

@@ -25,6 +25,10 @@
  *             2i+2), and walked with exactly d steps i = 2i + 1 + bit. A dummy node's two
  *             subtrees both end at the original leaf it replaces, so padding does not change
  *             the prediction (Section 3, end of Pred; Section 6 on unbalanced trees).
+ *
+ * oracle_feature_usage traces the branching walk and records the distinct feature ids each
+ * document's walks compare over the whole ensemble (the fraction of features a prediction
+ * reads, Section 6 and its Table 4).
  */
 #include <math.h>
 #include <stdint.h>
@@ -129,6 +133,77 @@ int oracle_score(int32_t n_trees, const int64_t *tree_offsets, const int32_t *fe
     }
     if (visits)
         *visits = total_steps;
+    return err;
+}
+
+/*
+ * Features examined (Section 6 and its Table 4: the fraction of features a prediction reads).
+ * For each document, the set of distinct feature ids compared at the internal nodes its walks
+ * pass through, over all trees (branching walk, the same rule as oracle_score).
+ *   counts [n_docs] int32: the size of the set, or NULL
+ *   masks  [n_docs][(n_features + 31) / 32] uint32: bit (f % 32) of word f / 32 is set when
+ *          feature f is examined, or NULL
+ * Returns ORACLE_OK or an error code.
+ */
+int oracle_feature_usage(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                         const float *threshold, const int32_t *left, const int32_t *right,
+                         const float *X, int64_t n_docs, int32_t n_features, int32_t rule,
+                         int32_t n_threads, int32_t *counts, uint32_t *masks)
+{
+    if (n_trees < 0 || n_docs < 0 || n_features < 1 || (n_trees > 0 && !tree_offsets))
+        return ORACLE_E_ARG;
+    const int64_t words = ((int64_t)n_features + 31) / 32;
+    int err = ORACLE_OK;
+#ifdef _OPENMP
+    if (n_threads > 0)
+        omp_set_num_threads(n_threads);
+#endif
+#pragma omp parallel
+    {
+        uint32_t *seen = (uint32_t *)calloc((size_t)words, sizeof(uint32_t));
+        if (!seen) {
+#pragma omp atomic write
+            err = ORACLE_E_NOMEM;
+        }
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t d = 0; d < n_docs; d++) {
+            if (!seen)
+                continue;
+            const float *x = X + d * (int64_t)n_features;
+            memset(seen, 0, (size_t)words * sizeof(uint32_t));
+            for (int32_t t = 0; t < n_trees; t++) {
+                const int64_t a = tree_offsets[t];
+                const int64_t nn = tree_offsets[t + 1] - a;
+                int64_t n = 0, k = 0;
+                while (nn > 0 && feature[a + n] >= 0) {
+                    const int32_t f = feature[a + n];
+                    if (f >= n_features || k >= nn) {
+#pragma omp atomic write
+                        err = ORACLE_E_MODEL;
+                        break;
+                    }
+                    seen[f / 32] |= (uint32_t)1 << (f % 32);
+                    n = goes_right(x[f], threshold[a + n], rule) ? right[a + n] : left[a + n];
+                    if (n < 0 || n >= nn) {
+#pragma omp atomic write
+                        err = ORACLE_E_MODEL;
+                        break;
+                    }
+                    k++;
+                }
+            }
+            int32_t c = 0;
+            for (int64_t w = 0; w < words; w++) {
+                for (int b = 0; b < 32; b++)
+                    c += (seen[w] >> b) & 1u;
+                if (masks)
+                    masks[d * words + w] = seen[w];
+            }
+            if (counts)
+                counts[d] = c;
+        }
+        free(seen);
+    }
     return err;
 }
 

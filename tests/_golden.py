@@ -16,10 +16,10 @@ def _f(tok: str) -> float:
 
 def load_hand_ensemble(name: str = "hand_ensemble.txt"):
     """Returns (ensemble, X float32, expects) where expects[rule] = list of
-    (doc, score, visits, [leaf ids])."""
+    (doc, score, visits, [leaf ids]) and expects["usage_" + rule] = list of (doc, [feature ids])."""
     trees: list[dict] = []
     docs: dict[int, list[float]] = {}
-    expects: dict[str, list] = {"ge": [], "gt": []}
+    expects: dict[str, list] = {"ge": [], "gt": [], "usage_ge": [], "usage_gt": []}
     n_features = None
     with open(os.path.join(GOLDEN, name)) as fh:
         for line in fh:
@@ -38,6 +38,8 @@ def load_hand_ensemble(name: str = "hand_ensemble.txt"):
                 docs[int(tok[1])] = [_f(t) for t in tok[2:]]
             elif tok[0] == "expect":
                 expects[tok[1]].append((int(tok[2]), _f(tok[3]), int(tok[4]), [int(t) for t in tok[5:]]))
+            elif tok[0] == "usage":
+                expects["usage_" + tok[1]].append((int(tok[2]), [int(t) for t in tok[3:]]))
             else:
                 raise ValueError(f"bad golden line: {line}")
     feats, thrs, lefts, rights, vals, offs = [], [], [], [], [], [0]

@@ -31,10 +31,30 @@ MUTANTS = [
     ("threshold_of_wrong_node", "goes_right(x[f], threshold[n], rule)", "goes_right(x[f], threshold[n > 0 ? n - 1 : n], rule)", None),
 ]
 
+# mistakes in the feature-access trace, caught by tests/test_oracle_usage.py
+USAGE_MUTANTS = [
+    ("usage_wrong_bit", "seen[f / 32] |= (uint32_t)1 << (f % 32);",
+     "seen[f / 32] |= (uint32_t)1 << ((f + 1) % 32);", None),
+    ("usage_one_word", "seen[f / 32] |= (uint32_t)1 << (f % 32);",
+     "seen[0] |= (uint32_t)1 << (f % 32);", None),
+    ("usage_not_reset_per_doc", "memset(seen, 0, (size_t)words * sizeof(uint32_t));", "", None),
+    ("usage_right_goes_left", "? right[a + n] : left[a + n];", "? left[a + n] : left[a + n];", None),
+    ("usage_rule_ignored", "goes_right(x[f], threshold[a + n], rule)", "goes_right(x[f], threshold[a + n], 0)", None),
+    ("usage_last_tree_dropped", "for (int32_t t = 0; t < n_trees; t++) {\n                const int64_t a",
+     "for (int32_t t = 0; t + 1 < n_trees; t++) {\n                const int64_t a", None),
+    ("usage_count_first_word", "for (int64_t w = 0; w < words; w++) {\n                for (int b = 0;",
+     "for (int64_t w = 0; w < words; w++) {\n                if (w) break;\n                for (int b = 0;", None),
+]
 
-@pytest.mark.slow
-@pytest.mark.parametrize("name,old,new,occ", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_catch_mutant(tmp_path, name, old, new, occ):
+
+def _run_pins(lib, pin_file):
+    env = dict(os.environ, ORACLE_LIB=lib)
+    return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                           os.path.join(ROOT, "tests", pin_file)],
+                          cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+
+
+def _build_mutant(tmp_path, name, old, new, occ):
     src = open(oracle.SRC).read()
     assert old in src, f"mutation site for {name} vanished from oracle.c; update the mutant list"
     mutated = src.replace(old, new, 1) if occ == 0 else src.replace(old, new)
@@ -43,21 +63,29 @@ def test_pins_catch_mutant(tmp_path, name, old, new, occ):
     csrc.write_text(mutated)
     lib = str(tmp_path / "liboracle_mutant.so")
     oracle.build(out=lib, src=str(csrc), extra=("-Wno-error",))
-    env = dict(os.environ, ORACLE_LIB=lib)
-    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
-                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return lib
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,old,new,occ", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new, occ):
+    r = _run_pins(_build_mutant(tmp_path, name, old, new, occ), "test_oracle_pins.py")
     assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
 
 
 @pytest.mark.slow
-def test_unmutated_copy_passes(tmp_path):
+@pytest.mark.parametrize("name,old,new,occ", USAGE_MUTANTS, ids=[m[0] for m in USAGE_MUTANTS])
+def test_usage_pins_catch_mutant(tmp_path, name, old, new, occ):
+    r = _run_pins(_build_mutant(tmp_path, name, old, new, occ), "test_oracle_usage.py")
+    assert r.returncode != 0, f"usage pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("pin_file", ["test_oracle_pins.py", "test_oracle_usage.py"])
+def test_unmutated_copy_passes(tmp_path, pin_file):
     # control: the same build-and-run route with the source unchanged must pass, so a failure
     # above is the mutation's doing and not the harness's
     lib = str(tmp_path / "liboracle_copy.so")
     oracle.build(out=lib)
-    env = dict(os.environ, ORACLE_LIB=lib)
-    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
-                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    r = _run_pins(lib, pin_file)
     assert r.returncode == 0, r.stdout[-3000:]
