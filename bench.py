@@ -217,6 +217,28 @@ def rerank(T, W, model, Xd, cfg, k=20, reps=50):
             "queries_per_s": len(sizes) / (fused_ms * 1e-3)}
 
 
+def feature_usage(model, Xd, cfg, reps=5):
+    """Section 6 / Table 4's measure on a workload: the share of the features each document's
+    walks compare over the whole ensemble (tree_ens_feature_usage, bitmasks included), and the
+    time of one trace of the batch."""
+    import numpy as np
+    import torch
+    counts, masks = model.feature_usage(Xd)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(reps):
+        model.feature_usage(Xd)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / reps
+    c = counts.cpu().numpy().astype(np.float64)
+    n = int(Xd.shape[0])
+    return {"docs": n, "n_features": cfg.n_features, "avg_features": float(c.mean()),
+            "avg_pct": float(100.0 * c.mean() / cfg.n_features), "min": int(c.min()), "max": int(c.max()),
+            "ms": ms, "doc_tree_per_s": n * cfg.n_trees / (ms * 1e-3), "reps": reps}
+
+
 def cpu_baseline(W, cfg_id, budget_s=10.0):
     import numpy as np
     import oracle
@@ -371,6 +393,9 @@ def main() -> int:
     rr = rerank(T, W, model, Xd, W.CONFIGS[HEADLINE_CFG])
     log(f"rerank top-{rr['k']} of {rr['queries']} queries: top-k kernel {rr['topk_us']:.1f} us, "
         f"score + top-k {rr['predict_topk_ms']:.3f} ms")
+    fu = feature_usage(model, Xd, W.CONFIGS[HEADLINE_CFG])
+    log(f"feature usage: {fu['avg_pct']:.1f}% of {fu['n_features']} features per document, "
+        f"trace {fu['ms']:.3f} ms")
     model.close()
     del Xd, out
     torch.cuda.empty_cache()
@@ -380,6 +405,9 @@ def main() -> int:
         for c, steps, samp in ((1, 20, None), (3, 10, None), (4, 5, None), (5, 3, 16384)):
             r, m, _, xd, o = measure_config(T, W, c, steps, 1, visits_sample=samp)
             r.pop("model", None)
+            r["feature_usage"] = feature_usage(m, xd, W.CONFIGS[c], reps=1 if c >= 4 else 5)
+            log(f"config {c} feature usage: {r['feature_usage']['avg_pct']:.1f}%, "
+                f"trace {r['feature_usage']['ms']:.3f} ms")
             extra[W.CONFIGS[c].name] = r
             m.close()
             del xd, o
@@ -397,7 +425,7 @@ def main() -> int:
                    "n_trees": cfg.n_trees, "n_docs": cfg.n_docs, "n_features": cfg.n_features,
                    "docs_per_block": rec["model"]["docs_per_block"]},
         "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"],
-        "latency_100doc_us": lat, "rerank": rr, "visits": rec["visits"],
+        "latency_100doc_us": lat, "rerank": rr, "feature_usage": fu, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
         "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
     }

@@ -108,6 +108,22 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
                             int32_t n_features, int32_t *leaf_ids);
 
 /*
+ * tree_ens_feature_usage -- feature-access trace (Section 6 and its Table 4: how many of the
+ * features a prediction actually reads). For each document, the set of distinct feature ids
+ * compared at the internal nodes its walks pass through, over all trees, by the same walk as
+ * tree_ens_predict (same tie rule, same flags).
+ *
+ *   counts    device, int32 [n_docs]: the size of document d's set.
+ *   masks     device, uint32 [n_docs][(n_features + 31) / 32] row-major, or NULL: bit (f % 32)
+ *             of word f / 32 is set when feature f is in the set; bits of features the model
+ *             never reads are 0.
+ * Other arguments, errors and behaviour as tree_ens_predict. Documents are read in place (not
+ * staged); one workgroup walks every tree for its block of documents.
+ */
+int tree_ens_feature_usage(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                           int32_t n_features, int32_t *counts, uint32_t *masks);
+
+/*
  * tree_ens_topk -- per-query top-k reranking of scores (Section 6: a query's candidate
  * documents, e.g. 200 of them, are scored and reranked into the final list of the best 20).
  *

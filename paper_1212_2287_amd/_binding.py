@@ -66,6 +66,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tree_ens_predict_leaves.restype = ctypes.c_int
     lib.tree_ens_predict_leaves.argtypes = [P, P, P, i64, i32, P]
     lib.tree_ens_topk.restype = ctypes.c_int
+    lib.tree_ens_feature_usage.restype = ctypes.c_int
+    lib.tree_ens_feature_usage.argtypes = [P, P, P, i64, i32, P, P]
     lib.tree_ens_topk.argtypes = [P, P, i64, P, i64, i32, P, P]
     lib.tree_ens_predict_topk.restype = ctypes.c_int
     lib.tree_ens_predict_topk.argtypes = [P, P, P, i64, i32, P, i64, i32, P, P, P]
@@ -180,6 +182,32 @@ def tree_ens_predict_leaves(h, X, leaf_ids=None, stream=None):
     return leaf_ids
 
 
+def tree_ens_feature_usage(h, X, counts=None, masks=None, want_masks: bool = True, stream=None):
+    """Features examined per document over all trees: (counts int32 [n_docs], masks int32
+    [n_docs, (n_features + 31) // 32] holding the uint32 bit patterns, or None when
+    ``want_masks`` is false and no ``masks`` tensor is given)."""
+    import torch
+    _check_docs(X)
+    n_docs, n_feat = X.shape
+    words = (n_feat + 31) // 32
+    if counts is None:
+        counts = torch.empty(n_docs, dtype=torch.int32, device=X.device)
+    elif counts.dtype != torch.int32 or counts.numel() < n_docs or not counts.is_contiguous() \
+            or counts.device != X.device:
+        raise TypeError("counts must be a contiguous int32 tensor of n_docs entries on X's device")
+    if masks is None and want_masks:
+        masks = torch.empty((n_docs, words), dtype=torch.int32, device=X.device)
+    if masks is not None and (masks.dtype != torch.int32 or masks.numel() < n_docs * words or
+                              not masks.is_contiguous() or masks.device != X.device):
+        raise TypeError("masks must be a contiguous int32 tensor of n_docs*words entries on X's device")
+    rc = load_library().tree_ens_feature_usage(
+        h, _stream_of(X, stream), X.data_ptr() if n_docs else None, n_docs, n_feat,
+        counts.data_ptr() if n_docs else None,
+        masks.data_ptr() if masks is not None and n_docs else None)
+    _check(rc, "tree_ens_feature_usage")
+    return counts, masks
+
+
 def _topk_outputs(device, n_groups, k, top_idx, top_scores):
     import torch
     if top_idx is None:
@@ -288,6 +316,9 @@ class TreeEnsemble:
 
     def predict_leaves(self, X, out=None, stream=None):
         return tree_ens_predict_leaves(self.handle, X, out, stream)
+
+    def feature_usage(self, X, want_masks: bool = True, stream=None):
+        return tree_ens_feature_usage(self.handle, X, want_masks=want_masks, stream=stream)
 
     def predict_topk(self, X, group_offsets, k: int, stream=None):
         """(scores, top_idx, top_scores): scores of X and each query group's k best documents."""

@@ -19,6 +19,11 @@
 // Blocks of a last, partial round of workgroups (and every block of a small batch) are split
 // over the tiles; the per-split partial sums are reduced by a second, tiny kernel in a fixed
 // order, so results are deterministic.
+// The same kernel has two more modes: leaf ids (the reached leaf of every (document, tree)) and
+// the feature-access trace (the set of distinct features each document's walks compare, the
+// measure of Section 6 / Table 4). The trace keeps the documents in global memory and uses the
+// LDS document tile as a per-document bitmask instead, set with LDS atomic ORs at every
+// internal step.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -58,6 +63,10 @@ constexpr int kWaitVmcnt0 = 0x0F70;
 #define TREE_ENS_PREFETCH_DEPTH 2 // tiles in flight with one workgroup per CU
 #endif
 constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves)
+// what a launch of the scoring kernel produces
+constexpr int kModeScore = 0;  // scores
+constexpr int kModeLeaves = 1; // leaf ids
+constexpr int kModeUsage = 2;  // per-document feature bitmasks and their popcounts
 
 // ------------------------------------------------------------------------------------------
 // kernels
@@ -110,7 +119,7 @@ __device__ __forceinline__ uint32_t narrow_child_coded(uint32_t w, uint32_t code
     return r;
 }
 
-template <int DL, int K, bool HALF, bool NARROW, bool CODED, bool LEAVES>
+template <int DL, int K, bool HALF, bool NARROW, bool CODED, int MODE>
 __global__ void __launch_bounds__(kThreads, HALF ? 8 : 4) // min waves per SIMD: 2 or 1 workgroups per CU
 score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, int32_t n_cols,
              const uint2 *__restrict__ images, int32_t slot_recs,
@@ -119,13 +128,18 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
              int32_t xs_bytes, int32_t zero_rec, double *__restrict__ partials,
              float *__restrict__ scores, int32_t *__restrict__ leaf_ids,
              const int32_t *__restrict__ orig_id, const uint32_t *__restrict__ tree_node_off,
-             const int32_t *__restrict__ tree_orig, int32_t n_trees) {
+             const int32_t *__restrict__ tree_orig, int32_t n_trees,
+             uint32_t *__restrict__ masks, int32_t mask_words) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
     //   [0, xs_bytes)            document tile, [(n_cols + 1) x DL] values
     //   [xs_bytes, zero_rec)     tile slot: the current tile image (header, then node records)
     //   zero_rec (8 bytes)       all-zero self-linked leaf of value 0, for idle walker slots
+    // In the usage mode the document tile region holds the bitmasks instead: word j of document
+    // lane dl at [j * DL + dl] (words of 32 feature ids), and features are read from X.
+    constexpr bool LEAVES = MODE == kModeLeaves;
+    constexpr bool USAGE = MODE == kModeUsage;
     constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 : treeens::kLdsPerCu;
     __shared__ __align__(16) unsigned char lds[kLds];
     constexpr int kPre = HALF ? treeens::kPrefetchHalf : treeens::kPrefetchFull; // records per thread
@@ -143,7 +157,12 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // the group loop is scalar
     const int walker = DL == 64 ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
     const int n_walkers = nthr / DL;
-    const uint32_t lane_off = uint32_t(dl) * uint32_t(sizeof(Elem));
+    // a record's column field is the byte offset col * DL * sizeof(Elem) of its feature column
+    const uint32_t lane_off = USAGE ? 0u : uint32_t(dl) * uint32_t(sizeof(Elem));
+    constexpr int kColShift = __builtin_ctz(unsigned(DL * sizeof(Elem)));
+    uint32_t *umask = reinterpret_cast<uint32_t *>(lds);
+    const int model_words = (n_cols + 31) / 32;
+
     const uint32_t col_mask =
         __builtin_amdgcn_readfirstlane(NARROW ? treeens::kNarrowColMask : treeens::kWideColMask);
     // column offsets below this are column 0 (NaN, or code 0), which only leaves name
@@ -163,6 +182,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     const int64_t doc0 = block * DL;
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
     const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
+    // usage mode: this lane's document row in global memory (clamped past the batch end)
+    const Elem *urow = X + min<int64_t>(doc0 + dl, n_docs - 1) * int64_t(n_features);
 
     // Tile images are loaded into registers while the previous tile is walked, so the
     // global-memory latency of a tile load is hidden; the tile loop issues no scalar memory load
@@ -206,6 +227,10 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         }
     }
 
+    if constexpr (USAGE) {
+        for (int i = tid; i < model_words * DL; i += kThreads)
+            umask[i] = 0u;
+    } else {
     // Stage the document tile: lane = document, so each LDS write is conflict-free (bank =
     // lane). The workgroup size is a multiple of DL, so a thread's document (and row) is fixed
     // and it takes every (kThreads / DL)-th group of columns. When rows are 16-byte aligned a
@@ -263,6 +288,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             }
         }
     }
+    } // staging
     if (tid == 0) {
         // value 0 (as -0.0 for codes, whose leaves never hold zero bits), column 0, self link
         const uint32_t thr = CODED ? 0x80000000u : 0u;
@@ -300,10 +326,22 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
 #pragma unroll
                     for (int i = 0; i < K; ++i) {
                         fa[i] = and_or(rec_w(nd[i]), col_mask, lane_off);
-                        if constexpr (CODED)
+                        if constexpr (USAGE) {
+                            // column 0 is a leaf's: no comparison, nothing recorded; a leaf
+                            // compares NaN (code 0) and stays put
+                            const uint32_t col = fa[i] >> kColShift;
+                            const Elem v = urow[col > 0u ? col - 1u : 0u];
+                            if constexpr (CODED)
+                                xv[i] = col > 0u ? uint32_t(v) : 0u;
+                            else
+                                xv[i] = col > 0u ? v : __builtin_nanf("");
+                            if (col > 0u)
+                                atomicOr(&umask[((col - 1u) >> 5) * DL + dl], 1u << ((col - 1u) & 31u));
+                        } else if constexpr (CODED) {
                             xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
-                        else
+                        } else {
                             xv[i] = *reinterpret_cast<const float *>(lds + fa[i]);
+                        }
                     }
                 };
                 auto descend = [&]() {
@@ -376,7 +414,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                             leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
                         }
                     }
-                } else {
+                } else if constexpr (!USAGE) {
                     // K leaf values: exact enough in float, one double add (idle slots hold the
                     // zero record)
                     float group_sum = __uint_as_float(rec_thr(nd[0]));
@@ -432,7 +470,24 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             }
         }
     }
-    if constexpr (!LEAVES) {
+    if constexpr (USAGE) {
+        __syncthreads();
+        // rows of mask_words words (>= model_words; the words past the model's are zero)
+        const int64_t n_here = min<int64_t>(DL, n_docs - doc0);
+        if (masks) {
+            for (int e = tid; e < n_here * mask_words; e += kThreads) {
+                const int d = e / mask_words, j = e - d * mask_words;
+                masks[(doc0 + d) * mask_words + j] = j < model_words ? umask[j * DL + d] : 0u;
+            }
+        }
+        if (walker == 0 && dl < n_here) {
+            int count = 0;
+            for (int j = 0; j < model_words; ++j)
+                count += __popc(umask[j * DL + dl]);
+            leaf_ids[doc0 + dl] = count;
+        }
+    }
+    if constexpr (MODE == kModeScore) {
         __syncthreads();
         double *red = reinterpret_cast<double *>(lds + xs_bytes);
         red[walker * DL + dl] = acc;
@@ -541,43 +596,43 @@ code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int
 using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *, int32_t,
                          const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
                          float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
-                         int32_t);
+                         int32_t, uint32_t *, int32_t);
 
-template <int DL, bool HALF, bool NARROW, bool CODED, bool LEAVES>
+template <int DL, bool HALF, bool NARROW, bool CODED, int MODE>
 ScoreFn pick_k(int k) {
     switch (k) {
-    case 1: return score_kernel<DL, 1, HALF, NARROW, CODED, LEAVES>;
-    case 2: return score_kernel<DL, 2, HALF, NARROW, CODED, LEAVES>;
-    case 4: return score_kernel<DL, 4, HALF, NARROW, CODED, LEAVES>;
+    case 1: return score_kernel<DL, 1, HALF, NARROW, CODED, MODE>;
+    case 2: return score_kernel<DL, 2, HALF, NARROW, CODED, MODE>;
+    case 4: return score_kernel<DL, 4, HALF, NARROW, CODED, MODE>;
     default: return nullptr;
     }
 }
 
-template <bool NARROW, bool CODED, bool LEAVES>
+template <bool NARROW, bool CODED, int MODE>
 ScoreFn pick_dl(const treeens::LdsPlan &p) {
     if (p.lds_bytes == treeens::kLdsPerCu / 2) {
         // two workgroups per CU: only small float tiles of 64-document blocks
         if constexpr (CODED)
             return nullptr;
         else
-            return p.docs_per_block == 64 ? pick_k<64, true, NARROW, false, LEAVES>(p.interleave) : nullptr;
+            return p.docs_per_block == 64 ? pick_k<64, true, NARROW, false, MODE>(p.interleave) : nullptr;
     }
     switch (p.docs_per_block) {
-    case 64: return pick_k<64, false, NARROW, CODED, LEAVES>(p.interleave);
-    case 32: return pick_k<32, false, NARROW, CODED, LEAVES>(p.interleave);
-    case 16: return pick_k<16, false, NARROW, CODED, LEAVES>(p.interleave);
-    case 8: return pick_k<8, false, NARROW, CODED, LEAVES>(p.interleave);
+    case 64: return pick_k<64, false, NARROW, CODED, MODE>(p.interleave);
+    case 32: return pick_k<32, false, NARROW, CODED, MODE>(p.interleave);
+    case 16: return pick_k<16, false, NARROW, CODED, MODE>(p.interleave);
+    case 8: return pick_k<8, false, NARROW, CODED, MODE>(p.interleave);
     default: return nullptr;
     }
 }
 
-template <bool LEAVES>
+template <int MODE>
 ScoreFn pick_kernel(const treeens::LdsPlan &p) {
     if (p.lds_bytes != treeens::kLdsPerCu / 2 && p.lds_bytes != treeens::kLdsPerCu)
         return nullptr;
     if (p.coded)
-        return p.narrow ? pick_dl<true, true, LEAVES>(p) : pick_dl<false, true, LEAVES>(p);
-    return p.narrow ? pick_dl<true, false, LEAVES>(p) : pick_dl<false, false, LEAVES>(p);
+        return p.narrow ? pick_dl<true, true, MODE>(p) : pick_dl<false, true, MODE>(p);
+    return p.narrow ? pick_dl<true, false, MODE>(p) : pick_dl<false, false, MODE>(p);
 }
 
 } // namespace
@@ -759,15 +814,25 @@ int check_predict_args(const tree_ens *h, const float *X, int64_t n_docs, int32_
     return TREE_ENS_OK;
 }
 
-template <bool LEAVES>
+// MODE kModeScore writes scores; kModeLeaves writes leaf_ids [n_docs][n_trees]; kModeUsage
+// writes per-document feature counts into leaf_ids and, if masks is not NULL, the bitmasks
+// (rows of mask_words words).
+template <int MODE>
 int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_t n_docs,
-                   int32_t n_features, float *scores, int32_t *leaf_ids) {
+                   int32_t n_features, float *scores, int32_t *leaf_ids, uint32_t *masks = nullptr,
+                   int32_t mask_words = 0) {
+    constexpr bool kScores = MODE == kModeScore; // only scores have split partial sums
     const int dl = h->plan.docs_per_block;
     const int64_t n_blocks = (n_docs + dl - 1) / dl;
     if (n_blocks > 0x7fffffff)
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     LaunchShape shape;
-    {
+    if (MODE == kModeUsage) {
+        // one workgroup walks every tile of its block: its bitmasks are complete in LDS
+        shape = LaunchShape{0, n_blocks, 1};
+        if (int64_t((h->n_cols + 31) / 32) * dl * 4 > h->plan.xs_bytes)
+            return fail(TREE_ENS_E_ARG, "feature bitmasks do not fit the document tile");
+    } else {
         std::lock_guard<std::mutex> lock(h->shape_mu);
         if (h->shape_blocks == n_blocks) {
             shape = LaunchShape{h->shape_level, h->shape_head, h->shape_splits};
@@ -784,14 +849,14 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const int64_t n_wgs = shape.head + (n_blocks - shape.head) * splits;
     if (n_wgs > 0x7fffffff)
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
-    ScoreFn fn = pick_kernel<LEAVES>(h->plan);
+    ScoreFn fn = pick_kernel<MODE>(h->plan);
     if (!fn)
         return fail(TREE_ENS_E_ARG, "unsupported document block size");
     hipError_t e = hipSuccess;
     double *partials = nullptr;
     bool own_scratch = false; // partials live in the handle's scratch
     std::unique_lock<std::mutex> scratch_lock;
-    if (!LEAVES && splits > 1) {
+    if (kScores && splits > 1) {
         if (size_t(splits) * size_t(tail_docs) <= kScratchDoubles) {
             scratch_lock = std::unique_lock<std::mutex>(h->scratch_mu);
             if (h->scratch_used && h->scratch_stream != stream) {
@@ -841,7 +906,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                        row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs, n_tiles,
                        int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec, partials,
                        scores, leaf_ids, h->d_orig_id, h->d_tree_node_off, h->d_tree_orig,
-                       h->n_trees);
+                       h->n_trees, masks, mask_words);
     e = hipGetLastError();
     if (e == hipSuccess && partials) {
         float *tail_scores = scores + shape.head * dl;
@@ -963,7 +1028,7 @@ int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t 
         hipError_t e = hipGetLastError();
         return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "kernel launch");
     }
-    return launch_predict<false>(h, s, X, n_docs, n_features, scores, nullptr);
+    return launch_predict<kModeScore>(h, s, X, n_docs, n_features, scores, nullptr);
 }
 
 int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
@@ -975,8 +1040,8 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
     DeviceGuard g(h->device);
     if (g.err != hipSuccess)
         return hip_fail(g.err, "hipSetDevice");
-    return launch_predict<true>(h, reinterpret_cast<hipStream_t>(stream), X, n_docs, n_features,
-                                nullptr, leaf_ids);
+    return launch_predict<kModeLeaves>(h, reinterpret_cast<hipStream_t>(stream), X, n_docs,
+                                       n_features, nullptr, leaf_ids);
 }
 
 int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
@@ -986,6 +1051,32 @@ int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int
     if (rc != TREE_ENS_OK)
         return rc;
     return tree_ens_topk(stream, scores, n_docs, group_offsets, n_groups, k, top_idx, top_scores);
+}
+
+int tree_ens_feature_usage(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                           int32_t n_features, int32_t *counts, uint32_t *masks) {
+    g_err.clear();
+    int rc = check_predict_args(h, X, n_docs, n_features, counts);
+    if (rc != TREE_ENS_OK || n_docs == 0)
+        return rc;
+    if (masks && (reinterpret_cast<uintptr_t>(masks) & 3u) != 0)
+        return fail(TREE_ENS_E_ARG, "masks must be 4-byte aligned");
+    DeviceGuard g(h->device);
+    if (g.err != hipSuccess)
+        return hip_fail(g.err, "hipSetDevice");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int32_t words = (n_features + 31) / 32;
+    if (h->n_trees == 0) {
+        const int bs = 256;
+        hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n_docs + bs - 1) / bs)), dim3(bs), 0, s,
+                           reinterpret_cast<float *>(counts), n_docs);
+        if (masks)
+            hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n_docs * words + bs - 1) / bs)),
+                               dim3(bs), 0, s, reinterpret_cast<float *>(masks), n_docs * words);
+        hipError_t e = hipGetLastError();
+        return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "kernel launch");
+    }
+    return launch_predict<kModeUsage>(h, s, X, n_docs, n_features, nullptr, counts, masks, words);
 }
 
 int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features, int32_t *max_depth,
