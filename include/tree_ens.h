@@ -117,8 +117,8 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
  *   masks     device, uint32 [n_docs][(n_features + 31) / 32] row-major, or NULL: bit (f % 32)
  *             of word f / 32 is set when feature f is in the set; bits of features the model
  *             never reads are 0.
- * Other arguments, errors and behaviour as tree_ens_predict. Documents are read in place (not
- * staged); one workgroup walks every tree for its block of documents.
+ * Other arguments, errors and behaviour as tree_ens_predict. One workgroup walks every tree for
+ * its block of documents, holding the block's bitmasks in LDS.
  */
 int tree_ens_feature_usage(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
                            int32_t n_features, int32_t *counts, uint32_t *masks);

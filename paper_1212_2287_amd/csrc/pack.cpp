@@ -48,8 +48,12 @@ LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
     // records per thread a tile may take in the registers that prefetch it: all of the
     // prefetch registers with two workgroups per CU, half of them (two tiles in flight) with one
     const int prefetch = p.lds_bytes == kLdsPerCu / 2 ? kPrefetchHalf : kPrefetchFull / 2;
-    p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve, prefetch * 1024 * 8) & ~15;
+    // one-workgroup plans keep room for the trace's bitmasks after the zero record
+    const int usage_bytes = int((int64_t(n_cols) + 31) / 32 * p.docs_per_block * 4);
+    const int usage_room = p.lds_bytes == kLdsPerCu ? (usage_bytes + 15) & ~15 : 0;
+    p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve - usage_room, prefetch * 1024 * 8) & ~15;
     p.zero_rec = p.xs_bytes + p.tile_bytes;
+    p.usage_off = p.lds_bytes == kLdsPerCu ? (p.zero_rec + 8 + 15) & ~15 : kLdsPerCu / 2;
     // Interleave K trees per lane (latency hiding) only when a tile holds at least K rounds of
     // walker groups; otherwise most walkers would sit idle.
     const double fit = avg_tree_bytes > 0 ? p.tile_bytes / avg_tree_bytes : 1e9;

@@ -76,6 +76,10 @@ struct LdsPlan {
     int32_t narrow;         // 1: narrow record format (see NodeRec), 0: wide
     int32_t coded;          // 1: documents are staged as 16-bit threshold codes (see below)
     int32_t elem_bytes;     // bytes per staged feature value: 4 (float) or 2 (code)
+    // feature-access trace: LDS byte address of the per-document feature bitmasks
+    // (ceil(n_cols / 32) words per document, [word][docs_per_block]); with two-workgroup plans
+    // it lies past their half of the LDS, so the trace runs one workgroup per CU
+    int32_t usage_off;
 };
 
 // Coded features (exact). For each feature f let T_f be the model's distinct thresholds of f,
@@ -104,6 +108,8 @@ constexpr int kPrefetchFull = 16;
 constexpr int kXsMaxBytes = 96 * 1024; // cap on the staged document tile
 constexpr int kTwoWgXsBytes = 40 * 1024; // tiles up to this size leave room for 2 workgroups/CU
 constexpr int kTileLevels = 5;         // tilings at budget, budget/2, ..., budget/16
+// bitmask bytes of a two-workgroup plan's 64-document tile at most (n_cols + 1 <= 160 columns)
+constexpr int kUsageHalfBytes = ((kTwoWgXsBytes / (64 * 4) - 1 + 31) / 32) * 64 * 4;
 
 struct Packed {
     int32_t n_trees = 0;

@@ -21,9 +21,8 @@
 // order, so results are deterministic.
 // The same kernel has two more modes: leaf ids (the reached leaf of every (document, tree)) and
 // the feature-access trace (the set of distinct features each document's walks compare, the
-// measure of Section 6 / Table 4). The trace keeps the documents in global memory and uses the
-// LDS document tile as a per-document bitmask instead, set with LDS atomic ORs at every
-// internal step.
+// measure of Section 6 / Table 4): per-document bitmasks in LDS, set with an LDS atomic OR at
+// every internal step.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -129,18 +128,20 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
              float *__restrict__ scores, int32_t *__restrict__ leaf_ids,
              const int32_t *__restrict__ orig_id, const uint32_t *__restrict__ tree_node_off,
              const int32_t *__restrict__ tree_orig, int32_t n_trees,
-             uint32_t *__restrict__ masks, int32_t mask_words) {
+             uint32_t *__restrict__ masks, int32_t mask_words, int32_t usage_off) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
     //   [0, xs_bytes)            document tile, [(n_cols + 1) x DL] values
     //   [xs_bytes, zero_rec)     tile slot: the current tile image (header, then node records)
     //   zero_rec (8 bytes)       all-zero self-linked leaf of value 0, for idle walker slots
-    // In the usage mode the document tile region holds the bitmasks instead: word j of document
-    // lane dl at [j * DL + dl] (words of 32 feature ids), and features are read from X.
+    //   usage_off                usage mode: word j of document lane dl's feature bitmask at
+    //                            [j * DL + dl] (32 feature ids a word); past the 80 KB half of
+    //                            two-workgroup plans, so usage launches hold a CU alone
     constexpr bool LEAVES = MODE == kModeLeaves;
     constexpr bool USAGE = MODE == kModeUsage;
-    constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 : treeens::kLdsPerCu;
+    constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 + (USAGE ? treeens::kUsageHalfBytes : 0)
+                              : treeens::kLdsPerCu;
     __shared__ __align__(16) unsigned char lds[kLds];
     constexpr int kPre = HALF ? treeens::kPrefetchHalf : treeens::kPrefetchFull; // records per thread
     constexpr int kShift = NARROW ? 16 : treeens::kWideChildShift;
@@ -157,10 +158,10 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // the group loop is scalar
     const int walker = DL == 64 ? __builtin_amdgcn_readfirstlane(tid / DL) : tid / DL;
     const int n_walkers = nthr / DL;
-    // a record's column field is the byte offset col * DL * sizeof(Elem) of its feature column
-    const uint32_t lane_off = USAGE ? 0u : uint32_t(dl) * uint32_t(sizeof(Elem));
+    const uint32_t lane_off = uint32_t(dl) * uint32_t(sizeof(Elem));
+    // a feature address is column * DL * sizeof(Elem) + lane offset (below DL * sizeof(Elem))
     constexpr int kColShift = __builtin_ctz(unsigned(DL * sizeof(Elem)));
-    uint32_t *umask = reinterpret_cast<uint32_t *>(lds);
+    uint32_t *umask = reinterpret_cast<uint32_t *>(lds + usage_off);
     const int model_words = (n_cols + 31) / 32;
 
     const uint32_t col_mask =
@@ -182,8 +183,6 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     const int64_t doc0 = block * DL;
     const int t_lo = int((int64_t(n_tiles) * split) / n_splits);
     const int t_hi = int((int64_t(n_tiles) * (split + 1)) / n_splits);
-    // usage mode: this lane's document row in global memory (clamped past the batch end)
-    const Elem *urow = X + min<int64_t>(doc0 + dl, n_docs - 1) * int64_t(n_features);
 
     // Tile images are loaded into registers while the previous tile is walked, so the
     // global-memory latency of a tile load is hidden; the tile loop issues no scalar memory load
@@ -230,7 +229,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     if constexpr (USAGE) {
         for (int i = tid; i < model_words * DL; i += kThreads)
             umask[i] = 0u;
-    } else {
+    }
     // Stage the document tile: lane = document, so each LDS write is conflict-free (bank =
     // lane). The workgroup size is a multiple of DL, so a thread's document (and row) is fixed
     // and it takes every (kThreads / DL)-th group of columns. When rows are 16-byte aligned a
@@ -288,7 +287,6 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             }
         }
     }
-    } // staging
     if (tid == 0) {
         // value 0 (as -0.0 for codes, whose leaves never hold zero bits), column 0, self link
         const uint32_t thr = CODED ? 0x80000000u : 0u;
@@ -326,21 +324,16 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
 #pragma unroll
                     for (int i = 0; i < K; ++i) {
                         fa[i] = and_or(rec_w(nd[i]), col_mask, lane_off);
+                        if constexpr (CODED)
+                            xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
+                        else
+                            xv[i] = *reinterpret_cast<const float *>(lds + fa[i]);
                         if constexpr (USAGE) {
-                            // column 0 is a leaf's: no comparison, nothing recorded; a leaf
-                            // compares NaN (code 0) and stays put
+                            // column c > 0 holds feature c - 1; column 0 is a leaf's (no
+                            // comparison, nothing recorded)
                             const uint32_t col = fa[i] >> kColShift;
-                            const Elem v = urow[col > 0u ? col - 1u : 0u];
-                            if constexpr (CODED)
-                                xv[i] = col > 0u ? uint32_t(v) : 0u;
-                            else
-                                xv[i] = col > 0u ? v : __builtin_nanf("");
                             if (col > 0u)
                                 atomicOr(&umask[((col - 1u) >> 5) * DL + dl], 1u << ((col - 1u) & 31u));
-                        } else if constexpr (CODED) {
-                            xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
-                        } else {
-                            xv[i] = *reinterpret_cast<const float *>(lds + fa[i]);
                         }
                     }
                 };
@@ -596,7 +589,7 @@ code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int
 using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *, int32_t,
                          const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
                          float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
-                         int32_t, uint32_t *, int32_t);
+                         int32_t, uint32_t *, int32_t, int32_t);
 
 template <int DL, bool HALF, bool NARROW, bool CODED, int MODE>
 ScoreFn pick_k(int k) {
@@ -727,8 +720,11 @@ hipError_t upload(T **dst, const std::vector<T> &src) {
 //     head / W * (1 + c_wg)
 //     + ceil(tail blocks * splits / W) * (share + c_wg)
 //     + (splits > 1 ? c_reduce : 0) + tiny * workgroups,
-// where share = ceil(tiles / splits) * rounds of the fullest tile / rounds of all tiles, c_wg
-// is the per-workgroup cost (staging, prologue, epilogue) and the last term prefers fewer
+// where share = ceil(tiles / splits) * (rounds of the fullest tile + c_tile) / (rounds of all
+// tiles + tiles * c_tile) at tiling 0, c_tile is the cost of switching tiles (two barriers, the
+// copy into LDS, the part of the next tile's load the walk does not hide: about half a round on
+// 20,000 depth-3 trees, measured), c_wg is the per-workgroup cost (staging, prologue, epilogue)
+// and the last term prefers fewer
 // workgroups (fewer partial sums) among equal estimates. Candidates: everything split
 // uniformly (no head; small batches spread over the GPU), and whole rounds of workgroups as
 // head with the remainder split to fill the last round (a batch of 1,563 blocks on 512 resident
@@ -743,15 +739,18 @@ LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
     constexpr double kItemCost = 0.2;    // staging, prologue and restaging of one workgroup (measured)
     constexpr double kReduceCost = 0.05; // the second kernel
     constexpr double kPerWorkgroup = 1e-6;
+    constexpr double kTileRounds = 0.5;  // switching tiles, in walker rounds
     const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
     const int64_t slots = int64_t(kNumCus) * wg_per_cu;
-    const double total = double(std::max<int64_t>(h->total_rounds, 1));
+    const double total = double(std::max<int64_t>(h->total_rounds, 1)) +
+                         kTileRounds * double(h->level_begin[1] - h->level_begin[0]);
     double best = 1e300;
     LaunchShape pick;
     auto consider = [&](int level, int64_t head, int sp) {
         const int nt = h->level_begin[level + 1] - h->level_begin[level];
         const int64_t tail = n_blocks - head;
-        const double share = double((nt + sp - 1) / sp) * h->level_max_rounds[level] / total;
+        const double share =
+            double((nt + sp - 1) / sp) * (h->level_max_rounds[level] + kTileRounds) / total;
         const double cost = double(head / slots) * (1.0 + kItemCost) +
                             double((tail * sp + slots - 1) / slots) * (share + kItemCost) +
                             (sp > 1 ? kReduceCost : 0.0) + kPerWorkgroup * double(head + tail * sp);
@@ -830,8 +829,11 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     if (MODE == kModeUsage) {
         // one workgroup walks every tile of its block: its bitmasks are complete in LDS
         shape = LaunchShape{0, n_blocks, 1};
-        if (int64_t((h->n_cols + 31) / 32) * dl * 4 > h->plan.xs_bytes)
-            return fail(TREE_ENS_E_ARG, "feature bitmasks do not fit the document tile");
+        const int64_t lds_end = h->plan.lds_bytes == treeens::kLdsPerCu
+                                    ? treeens::kLdsPerCu
+                                    : treeens::kLdsPerCu / 2 + treeens::kUsageHalfBytes;
+        if (h->plan.usage_off + int64_t((h->n_cols + 31) / 32) * dl * 4 > lds_end)
+            return fail(TREE_ENS_E_ARG, "feature bitmasks do not fit the LDS plan");
     } else {
         std::lock_guard<std::mutex> lock(h->shape_mu);
         if (h->shape_blocks == n_blocks) {
@@ -906,7 +908,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                        row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs, n_tiles,
                        int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec, partials,
                        scores, leaf_ids, h->d_orig_id, h->d_tree_node_off, h->d_tree_orig,
-                       h->n_trees, masks, mask_words);
+                       h->n_trees, masks, mask_words, h->plan.usage_off);
     e = hipGetLastError();
     if (e == hipSuccess && partials) {
         float *tail_scores = scores + shape.head * dl;

@@ -81,6 +81,16 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         return bad("LDS plan regions overlap or exceed the workgroup's LDS");
     if (int64_t(p.n_cols + 1) * DL * E != pl.xs_bytes)
         return bad("document tile size does not match the column count");
+    {
+        // the feature-access trace's bitmasks: after the zero record, within the LDS the usage
+        // launch declares (two-workgroup plans: past their half, plus kUsageHalfBytes)
+        const int64_t usage_end = int64_t(pl.usage_off) + int64_t(p.n_cols + 31) / 32 * DL * 4;
+        const int64_t lds_end = pl.lds_bytes == treeens::kLdsPerCu
+                                    ? treeens::kLdsPerCu
+                                    : treeens::kLdsPerCu / 2 + treeens::kUsageHalfBytes;
+        if (pl.usage_off % 16 || pl.usage_off < int64_t(zero) + 8 || usage_end > lds_end)
+            return bad("feature bitmask region overlaps the tile or exceeds the LDS");
+    }
     std::vector<uint8_t> lds(size_t(pl.lds_bytes), 0);
     auto rec_at = [&](uint32_t a) {
         treeens::NodeRec r;
