@@ -217,10 +217,11 @@ def rerank(T, W, model, Xd, cfg, k=20, reps=50):
             "queries_per_s": len(sizes) / (fused_ms * 1e-3)}
 
 
-def feature_usage(model, Xd, cfg, reps=5):
+def feature_usage(model, Xd, cfg, visits, reps=5):
     """Section 6 / Table 4's measure on a workload: the share of the features each document's
     walks compare over the whole ensemble (tree_ens_feature_usage, bitmasks included), and the
-    time of one trace of the batch."""
+    time of one trace of the batch. LDS roofline of the trace: per comparison a node record
+    (8 B), a feature (4 B) and an atomic OR into the document's bitmask (4 B)."""
     import numpy as np
     import torch
     counts, masks = model.feature_usage(Xd)
@@ -234,9 +235,29 @@ def feature_usage(model, Xd, cfg, reps=5):
     ms = ev0.elapsed_time(ev1) / reps
     c = counts.cpu().numpy().astype(np.float64)
     n = int(Xd.shape[0])
+    lds = visits * 16
     return {"docs": n, "n_features": cfg.n_features, "avg_features": float(c.mean()),
             "avg_pct": float(100.0 * c.mean() / cfg.n_features), "min": int(c.min()), "max": int(c.max()),
-            "ms": ms, "doc_tree_per_s": n * cfg.n_trees / (ms * 1e-3), "reps": reps}
+            "ms": ms, "doc_tree_per_s": n * cfg.n_trees / (ms * 1e-3), "reps": reps,
+            "roofline": {"bound": "lds", "achieved": lds / (ms * 1e-3) / 1e9, "peak": LDS_PEAK_GBS,
+                         "unit": "GB/s", "frac": lds / (ms * 1e-3) / 1e9 / LDS_PEAK_GBS,
+                         "bytes": lds}}
+
+
+def feature_usage_by_trees(T, ens, Xd, cfg, sizes=(1, 10, 100, 1000)):
+    """Table 4's shape on the ranking workload: the share of features examined per document as
+    the ensemble grows (prefixes of the model, the first 10,000 documents)."""
+    import torch
+    x = Xd[:10_000].contiguous()
+    out = {}
+    for n in sizes:
+        if n > ens.n_trees:
+            continue
+        with T.TreeEnsemble.from_ensemble(ens.take_trees(n)) as m:
+            c, _ = m.feature_usage(x, want_masks=False)
+            torch.cuda.synchronize()
+            out[str(n)] = float(100.0 * c.float().mean().item() / cfg.n_features)
+    return out
 
 
 def cpu_baseline(W, cfg_id, budget_s=10.0):
@@ -393,9 +414,10 @@ def main() -> int:
     rr = rerank(T, W, model, Xd, W.CONFIGS[HEADLINE_CFG])
     log(f"rerank top-{rr['k']} of {rr['queries']} queries: top-k kernel {rr['topk_us']:.1f} us, "
         f"score + top-k {rr['predict_topk_ms']:.3f} ms")
-    fu = feature_usage(model, Xd, W.CONFIGS[HEADLINE_CFG])
+    fu = feature_usage(model, Xd, W.CONFIGS[HEADLINE_CFG], rec["visits"])
+    fu["pct_by_trees"] = feature_usage_by_trees(T, ens, Xd, W.CONFIGS[HEADLINE_CFG])
     log(f"feature usage: {fu['avg_pct']:.1f}% of {fu['n_features']} features per document, "
-        f"trace {fu['ms']:.3f} ms")
+        f"trace {fu['ms']:.3f} ms (LDS frac {fu['roofline']['frac']:.3f}); by trees {fu['pct_by_trees']}")
     model.close()
     del Xd, out
     torch.cuda.empty_cache()
@@ -405,7 +427,7 @@ def main() -> int:
         for c, steps, samp in ((1, 20, None), (3, 10, None), (4, 5, None), (5, 3, 16384)):
             r, m, _, xd, o = measure_config(T, W, c, steps, 1, visits_sample=samp)
             r.pop("model", None)
-            r["feature_usage"] = feature_usage(m, xd, W.CONFIGS[c], reps=1 if c >= 4 else 5)
+            r["feature_usage"] = feature_usage(m, xd, W.CONFIGS[c], r["visits"], reps=1 if c >= 4 else 5)
             log(f"config {c} feature usage: {r['feature_usage']['avg_pct']:.1f}%, "
                 f"trace {r['feature_usage']['ms']:.3f} ms")
             extra[W.CONFIGS[c].name] = r
