@@ -7,7 +7,8 @@ this package. The GPU library never loads it and shares no code with it.
   the score written out -- a branching walk, a predicated walk and the literal padded
   breadth-first predicated walk (Section 3 of the paper), leaf values summed in double precision
   in tree order (Section 5.3); and the feature-access trace, the distinct features each
-  document's walks compare (Section 6, Table 4).
+  document's walks compare (Section 6, Table 4); vector-valued leaves and bagged ensembles
+  (Sections 3 and 5.3).
 * ``brute.py``: a path-conjunction brute force for tiny inputs (a document reaches leaf l iff
   every predicate on the root-to-l path holds), summed with ``math.fsum``.
 
@@ -49,6 +50,8 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_score.argtypes = [i32, P, P, P, P, P, P, P, i64, i32, i32, i32, i32, P, P, P]
     lib.oracle_score_padded.restype = ctypes.c_int
     lib.oracle_score_padded.argtypes = [i32, P, P, P, P, P, P, P, i64, i32, i32, i32, P, P]
+    lib.oracle_score_multi.restype = ctypes.c_int
+    lib.oracle_score_multi.argtypes = [i32, P, P, P, P, P, P, i32, i32, P, i64, i32, i32, i32, P]
     lib.oracle_feature_usage.restype = ctypes.c_int
     lib.oracle_feature_usage.argtypes = [i32, P, P, P, P, P, P, i64, i32, i32, i32, P, P]
     lib.oracle_max_threads.restype = ctypes.c_int
@@ -124,6 +127,25 @@ def score_padded(ens, X: np.ndarray, rule: int = RULE_GE, max_depth: int = 20,
     if rc != 0:
         raise OracleError(f"oracle_score_padded failed with code {rc}")
     return scores, leaves
+
+
+def score_multi(ens, leaf_values: np.ndarray, X: np.ndarray, n_bags: int = 1, rule: int = RULE_GE,
+                threads: int = 0, lib: Optional[ctypes.CDLL] = None) -> np.ndarray:
+    """Vector-valued leaves, bagged ensembles: float64 [n_docs, n_outputs] = (sum over trees of
+    the reached leaves' rows of ``leaf_values`` [n_nodes, n_outputs]) / n_bags."""
+    lib = lib or load()
+    off, fe, th, le, ri, _ = _model_arrays(ens)
+    vals = np.ascontiguousarray(leaf_values, dtype=np.float32)
+    if vals.ndim != 2 or vals.shape[0] != ens.n_nodes:
+        raise ValueError("leaf_values must be [n_nodes, n_outputs]")
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    n_docs, n_feat = X.shape
+    out = np.empty((n_docs, vals.shape[1]), dtype=np.float64)
+    rc = lib.oracle_score_multi(ens.n_trees, _p(off), _p(fe), _p(th), _p(le), _p(ri), _p(vals),
+                                vals.shape[1], n_bags, _p(X), n_docs, n_feat, rule, threads, _p(out))
+    if rc != 0:
+        raise OracleError(f"oracle_score_multi failed with code {rc}")
+    return out
 
 
 def feature_usage(ens, X: np.ndarray, rule: int = RULE_GE, threads: int = 0,

@@ -26,7 +26,8 @@
  *             subtrees both end at the original leaf it replaces, so padding does not change
  *             the prediction (Section 3, end of Pred; Section 6 on unbalanced trees).
  *
- * oracle_feature_usage traces the branching walk and records the distinct feature ids each
+ * oracle_score_multi sums vector-valued leaves component by component and averages bagged
+ * ensembles. oracle_feature_usage traces the branching walk and records the distinct feature ids each
  * document's walks compare over the whole ensemble (the fraction of features a prediction
  * reads, Section 6 and its Table 4).
  */
@@ -133,6 +134,59 @@ int oracle_score(int32_t n_trees, const int64_t *tree_offsets, const int32_t *fe
     }
     if (visits)
         *visits = total_steps;
+    return err;
+}
+
+/*
+ * Vector-valued leaves and bagged ensembles (Section 3: the leaf predictor may be a class, a
+ * real or another model; Section 5.3: an ensemble made of several bagged boosted ensembles).
+ * Every leaf holds n_outputs values (value[node * n_outputs + c]); output c of a document is
+ * the sum over the trees, in tree order and in double precision, of component c of the leaves
+ * reached, divided by n_bags: the trees are the concatenation of n_bags ensembles whose scores
+ * are averaged, and the mean of the bags' sums is the sum over all trees over n_bags.
+ *   scores [n_docs][n_outputs] doubles
+ * Returns ORACLE_OK or an error code.
+ */
+int oracle_score_multi(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                       const float *threshold, const int32_t *left, const int32_t *right,
+                       const float *value, int32_t n_outputs, int32_t n_bags, const float *X,
+                       int64_t n_docs, int32_t n_features, int32_t rule, int32_t n_threads,
+                       double *scores)
+{
+    if (n_trees < 0 || n_docs < 0 || n_features < 0 || n_outputs < 1 || n_bags < 1 ||
+        (n_trees > 0 && !tree_offsets) || !scores)
+        return ORACLE_E_ARG;
+    int err = ORACLE_OK;
+#ifdef _OPENMP
+    if (n_threads > 0)
+        omp_set_num_threads(n_threads);
+#endif
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t d = 0; d < n_docs; d++) {
+        const float *x = X + d * (int64_t)n_features;
+        double *out = scores + d * (int64_t)n_outputs;
+        for (int32_t c = 0; c < n_outputs; c++)
+            out[c] = 0.0;
+        for (int32_t t = 0; t < n_trees; t++) {
+            const int64_t a = tree_offsets[t];
+            const int64_t nn = tree_offsets[t + 1] - a;
+            int64_t steps = 0;
+            int32_t leaf = -1;
+            if (nn > 0)
+                leaf = walk_tree(nn, feature + a, threshold + a, left + a, right + a, x, n_features,
+                                 rule, 0, &steps);
+            if (leaf < 0) {
+#pragma omp atomic write
+                err = ORACLE_E_MODEL;
+                continue;
+            }
+            const float *v = value + (a + leaf) * (int64_t)n_outputs;
+            for (int32_t c = 0; c < n_outputs; c++)
+                out[c] += (double)v[c];
+        }
+        for (int32_t c = 0; c < n_outputs; c++)
+            out[c] /= (double)n_bags;
+    }
     return err;
 }
 

@@ -46,6 +46,16 @@ USAGE_MUTANTS = [
      "for (int64_t w = 0; w < words; w++) {\n                if (w) break;\n                for (int b = 0;", None),
 ]
 
+# mistakes in the vector-valued / bagged sum, caught by tests/test_oracle_multi.py
+MULTI_MUTANTS = [
+    ("multi_row_stride_dropped", "const float *v = value + (a + leaf) * (int64_t)n_outputs;",
+     "const float *v = value + (a + leaf);", None),
+    ("multi_component_shifted", "out[c] += (double)v[c];", "out[c] += (double)v[(c + 1) % n_outputs];", None),
+    ("multi_bags_not_averaged", "out[c] /= (double)n_bags;", "out[c] /= 1.0;", None),
+    ("multi_bags_summed_wrongly", "out[c] /= (double)n_bags;", "out[c] /= (double)(n_bags + 1);", None),
+    ("multi_float_accumulator", "out[c] += (double)v[c];", "out[c] = (double)((float)out[c] + v[c]);", None),
+]
+
 
 def _run_pins(lib, pin_file):
     env = dict(os.environ, ORACLE_LIB=lib)
@@ -81,7 +91,14 @@ def test_usage_pins_catch_mutant(tmp_path, name, old, new, occ):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("pin_file", ["test_oracle_pins.py", "test_oracle_usage.py"])
+@pytest.mark.parametrize("name,old,new,occ", MULTI_MUTANTS, ids=[m[0] for m in MULTI_MUTANTS])
+def test_multi_pins_catch_mutant(tmp_path, name, old, new, occ):
+    r = _run_pins(_build_mutant(tmp_path, name, old, new, occ), "test_oracle_multi.py")
+    assert r.returncode != 0, f"multi-output pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("pin_file", ["test_oracle_pins.py", "test_oracle_usage.py", "test_oracle_multi.py"])
 def test_unmutated_copy_passes(tmp_path, pin_file):
     # control: the same build-and-run route with the source unchanged must pass, so a failure
     # above is the mutation's doing and not the harness's

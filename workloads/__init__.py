@@ -299,6 +299,32 @@ def make_ensemble(cfg: Config, n_trees: Optional[int] = None) -> Ensemble:
                     np.concatenate(rights), np.concatenate(vals), cfg.n_features)
 
 
+def make_leaf_vectors(ens: Ensemble, n_outputs: int, kind: str = "dense", sigma: float = 0.1,
+                      seed: int = 0) -> np.ndarray:
+    """float32 [n_nodes, n_outputs] leaf rows for a vector-valued version of ``ens`` (internal
+    nodes' rows are zero):
+      * "dense": every component N(0, sigma) (multi-output regression);
+      * "class": tree t adds to class t % n_outputs only, with the tree's own leaf value (the
+        one-tree-per-class-per-round layout of multi-class boosting);
+      * "probs": a probability vector per leaf, the normalised magnitudes of N(0, 1) draws
+        (a forest classifier's class distributions)."""
+    rng = _rng(9000, seed, n_outputs)
+    leaf = ens.feature < 0
+    out = np.zeros((ens.n_nodes, n_outputs), dtype=np.float32)
+    if kind == "dense":
+        out[leaf] = rng.normal(0.0, sigma, (int(leaf.sum()), n_outputs)).astype(np.float32)
+    elif kind == "class":
+        tree_of = np.repeat(np.arange(ens.n_trees), np.diff(ens.tree_offsets))
+        rows = np.nonzero(leaf)[0]
+        out[rows, tree_of[rows] % n_outputs] = ens.value[rows]
+    elif kind == "probs":
+        m = np.abs(rng.normal(0.0, 1.0, (int(leaf.sum()), n_outputs)))
+        out[leaf] = (m / m.sum(axis=1, keepdims=True)).astype(np.float32)
+    else:
+        raise ValueError(f"unknown leaf vector kind {kind!r}")
+    return out
+
+
 def scaled(cfg: Config, n_docs: Optional[int] = None, n_trees: Optional[int] = None) -> Config:
     """Same configuration with fewer documents and/or trees (a prefix of the full one)."""
     from dataclasses import replace
