@@ -260,6 +260,36 @@ def feature_usage_by_trees(T, ens, Xd, cfg, sizes=(1, 10, 100, 1000)):
     return out
 
 
+def multi_output(T, W, ens, Xd, cfg, scalar_ms, reps=10):
+    """Vector-valued leaves and bagging on the ranking workload's trees and documents: 4 and 8
+    outputs per leaf (one and two passes over the trees), and 4 averaged bags of 250 trees."""
+    import torch
+    out = {}
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(m):
+        m.predict(Xd)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(reps):
+            m.predict(Xd)
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / reps
+
+    n = int(Xd.shape[0])
+    for n_out in (4, 8):
+        vals = W.make_leaf_vectors(ens, n_out, "dense", seed=n_out)
+        with T.TreeEnsemble.from_ensemble(ens, leaf_values=vals) as m:
+            ms = timed(m)
+        out[f"outputs_{n_out}"] = {"ms": ms, "vs_scalar": ms / scalar_ms,
+                                   "doc_tree_output_per_s": n * ens.n_trees * n_out / (ms * 1e-3)}
+    with T.TreeEnsemble.from_ensemble(ens, n_bags=4) as m:
+        ms = timed(m)
+    out["bags_4"] = {"ms": ms, "vs_scalar": ms / scalar_ms}
+    return out
+
+
 def cpu_baseline(W, cfg_id, budget_s=10.0):
     import numpy as np
     import oracle
@@ -414,6 +444,8 @@ def main() -> int:
     rr = rerank(T, W, model, Xd, W.CONFIGS[HEADLINE_CFG])
     log(f"rerank top-{rr['k']} of {rr['queries']} queries: top-k kernel {rr['topk_us']:.1f} us, "
         f"score + top-k {rr['predict_topk_ms']:.3f} ms")
+    mo = multi_output(T, W, ens, Xd, W.CONFIGS[HEADLINE_CFG], rec["kernel_ms"])
+    log("vector leaves / bags: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in mo.items()))
     fu = feature_usage(model, Xd, W.CONFIGS[HEADLINE_CFG], rec["visits"])
     fu["pct_by_trees"] = feature_usage_by_trees(T, ens, Xd, W.CONFIGS[HEADLINE_CFG])
     log(f"feature usage: {fu['avg_pct']:.1f}% of {fu['n_features']} features per document, "
@@ -447,7 +479,8 @@ def main() -> int:
                    "n_trees": cfg.n_trees, "n_docs": cfg.n_docs, "n_features": cfg.n_features,
                    "docs_per_block": rec["model"]["docs_per_block"]},
         "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"],
-        "latency_100doc_us": lat, "rerank": rr, "feature_usage": fu, "visits": rec["visits"],
+        "latency_100doc_us": lat, "rerank": rr, "feature_usage": fu,
+        "multi_output": mo, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
         "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
     }

@@ -72,6 +72,27 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
                     const int32_t *right, const float *value, uint32_t flags);
 
 /*
+ * tree_ens_create_multi -- tree_ens_create for vector-valued leaves and bagged ensembles
+ * (Section 3: the predictor at a leaf may be a class, a real or another model; Section 5.3:
+ * several boosted ensembles, each trained on a bootstrap sample, whose scores are averaged).
+ *
+ *   value      [n_nodes][n_outputs] float, row-major: the n_outputs values of each leaf (rows
+ *              of internal nodes are ignored). One output per class with one tree per class
+ *              and round is the multi-class boosting layout (zeros in the other columns).
+ *   n_outputs  1 .. 256. tree_ens_predict then writes n_outputs scores per document.
+ *   n_bags     >= 1: the trees are the concatenation of n_bags ensembles and every score is
+ *              the mean of their sums, i.e. the sum over all trees divided by n_bags.
+ * Other arguments, ownership and errors as tree_ens_create (tree_ens_create is this call with
+ * n_outputs = n_bags = 1). With n_outputs > 1 the leaf rows live in a device table of
+ * n_nodes + 1 rows of ceil(n_outputs / 4) * 4 floats, and a predict makes one pass over the
+ * trees per four outputs.
+ */
+int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offsets,
+                          const int32_t *feature, const float *threshold, const int32_t *left,
+                          const int32_t *right, const float *value, int32_t n_outputs,
+                          int32_t n_bags, uint32_t flags);
+
+/*
  * tree_ens_predict -- score n_docs documents (the ensemble sum of Section 5.3).
  *
  *   h           a handle from tree_ens_create.
@@ -83,8 +104,9 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
  *   n_docs      >= 0; 0 returns TREE_ENS_OK without a launch.
  *   n_features  row length; must be >= 1 + the largest feature id of the model (else
  *               TREE_ENS_E_SHAPE). Columns beyond the ones the model reads are never read.
- *   scores      device, float [n_docs]: the sum of the reached leaf values, accumulated in
- *               double precision and rounded once to float.
+ *   scores      device, float [n_docs][n_outputs] (n_outputs = 1 unless the handle comes from
+ *               tree_ens_create_multi): per output, the sum of the reached leaves' values,
+ *               accumulated in double precision, divided by n_bags and rounded once to float.
  *
  * Kernel faults surface at the caller's next synchronisation with the stream. When the launch
  * splits document blocks over several workgroups (small batches, and the blocks of a last,
@@ -147,7 +169,8 @@ int tree_ens_topk(void *stream, const float *scores, int64_t n_docs, const int64
                   int64_t n_groups, int32_t k, int32_t *top_idx, float *top_scores);
 
 /*
- * tree_ens_predict_topk -- tree_ens_predict into `scores` followed by tree_ens_topk over it,
+ * tree_ens_predict_topk -- tree_ens_predict into `scores` followed by tree_ens_topk over it
+ * (handles with one output only; TREE_ENS_E_ARG otherwise),
  * both enqueued on `stream` (scoring and reranking of query candidates in one call). Arguments
  * as for those two functions; `scores` is a device buffer of n_docs floats the caller owns
  * (it receives the scores).
@@ -169,6 +192,10 @@ int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int
 int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features,
                   int32_t *max_depth, int64_t *packed_bytes, int32_t *n_tiles,
                   int32_t *docs_per_block);
+
+/* tree_ens_outputs -- the handle's outputs per document and bag count (either pointer may be
+ * NULL). */
+int tree_ens_outputs(const tree_ens_t *h, int32_t *n_outputs, int32_t *n_bags);
 
 /* tree_ens_destroy -- free the handle and its device memory. NULL is accepted. The caller must
  * ensure no enqueued predict that uses h is still pending. */

@@ -61,6 +61,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     P, i32, i64, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
     lib.tree_ens_create.restype = ctypes.c_int
     lib.tree_ens_create.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, P, P, u32]
+    lib.tree_ens_create_multi.restype = ctypes.c_int
+    lib.tree_ens_create_multi.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, P, P, i32, i32, u32]
+    lib.tree_ens_outputs.restype = ctypes.c_int
+    lib.tree_ens_outputs.argtypes = [P, P, P]
     lib.tree_ens_predict.restype = ctypes.c_int
     lib.tree_ens_predict.argtypes = [P, P, P, i64, i32, P]
     lib.tree_ens_predict_leaves.restype = ctypes.c_int
@@ -102,10 +106,7 @@ def _arr(a, dtype):
     return np.ascontiguousarray(np.asarray(a), dtype=dtype)
 
 
-def tree_ens_create(tree_offsets, feature, threshold, left, right, value,
-                    flags: int = TREE_ENS_RIGHT_IF_GE) -> ctypes.c_void_p:
-    """Validate, pack and upload an ensemble given as flat creation-order arrays (host)."""
-    lib = load_library()
+def _model_args(tree_offsets, feature, threshold, left, right, value, n_outputs=1):
     off = _arr(tree_offsets, np.int64)
     fe, th = _arr(feature, np.int32), _arr(threshold, np.float32)
     le, ri, va = _arr(left, np.int32), _arr(right, np.int32), _arr(value, np.float32)
@@ -113,18 +114,47 @@ def tree_ens_create(tree_offsets, feature, threshold, left, right, value,
     if n_trees < 0:
         raise ValueError("tree_offsets needs n_trees + 1 entries")
     n = int(off[-1]) if n_trees > 0 else 0
-    for name, a in (("feature", fe), ("threshold", th), ("left", le), ("right", ri), ("value", va)):
+    for name, a in (("feature", fe), ("threshold", th), ("left", le), ("right", ri)):
         if a.shape[0] < n:
             raise ValueError(f"{name} has {a.shape[0]} entries; tree_offsets asks for {n}")
-    h = ctypes.c_void_p()
+    if va.size < n * n_outputs:
+        raise ValueError(f"value has {va.size} entries; {n} nodes x {n_outputs} outputs are needed")
 
     def ptr(a):
         return a.ctypes.data if a.size else None
 
-    rc = lib.tree_ens_create(ctypes.byref(h), n_trees, ptr(off), ptr(fe), ptr(th), ptr(le), ptr(ri),
-                             ptr(va), int(flags))
+    # the arrays are returned too: they must outlive the call
+    return n_trees, [ptr(a) for a in (off, fe, th, le, ri, va)], (off, fe, th, le, ri, va)
+
+
+def tree_ens_create(tree_offsets, feature, threshold, left, right, value,
+                    flags: int = TREE_ENS_RIGHT_IF_GE) -> ctypes.c_void_p:
+    """Validate, pack and upload an ensemble given as flat creation-order arrays (host)."""
+    lib = load_library()
+    n_trees, ptrs, _keep = _model_args(tree_offsets, feature, threshold, left, right, value)
+    h = ctypes.c_void_p()
+    rc = lib.tree_ens_create(ctypes.byref(h), n_trees, *ptrs, int(flags))
     _check(rc, "tree_ens_create")
     return h
+
+
+def tree_ens_create_multi(tree_offsets, feature, threshold, left, right, value, n_outputs: int,
+                          n_bags: int = 1, flags: int = TREE_ENS_RIGHT_IF_GE) -> ctypes.c_void_p:
+    """tree_ens_create with leaf rows of ``n_outputs`` values (``value`` [n_nodes, n_outputs])
+    and ``n_bags`` averaged bags."""
+    lib = load_library()
+    n_trees, ptrs, _keep = _model_args(tree_offsets, feature, threshold, left, right, value, n_outputs)
+    h = ctypes.c_void_p()
+    rc = lib.tree_ens_create_multi(ctypes.byref(h), n_trees, *ptrs, int(n_outputs), int(n_bags), int(flags))
+    _check(rc, "tree_ens_create_multi")
+    return h
+
+
+def tree_ens_outputs(h) -> tuple[int, int]:
+    """(n_outputs, n_bags) of a handle."""
+    n_out, n_bags = ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().tree_ens_outputs(h, ctypes.byref(n_out), ctypes.byref(n_bags)), "tree_ens_outputs")
+    return n_out.value, n_bags.value
 
 
 def _stream_of(t, stream) -> Optional[int]:
@@ -147,17 +177,22 @@ def _check_docs(X):
         raise TypeError("X must be a contiguous float32 [n_docs, n_features] tensor")
 
 
-def tree_ens_predict(h, X, scores=None, stream=None):
-    """Scores of the documents ``X`` (device float32 [n_docs, n_features]) as float32 [n_docs],
-    enqueued on ``stream`` (default: torch's current stream for X's device)."""
+def tree_ens_predict(h, X, scores=None, stream=None, n_outputs=None):
+    """Scores of the documents ``X`` (device float32 [n_docs, n_features]) as float32 [n_docs]
+    (or [n_docs, n_outputs] for a handle with several outputs), enqueued on ``stream``
+    (default: torch's current stream for X's device)."""
     import torch
     _check_docs(X)
     n_docs, n_feat = X.shape
+    if n_outputs is None:
+        n_outputs = tree_ens_outputs(h)[0]
     if scores is None:
-        scores = torch.empty(n_docs, dtype=torch.float32, device=X.device)
-    elif scores.dtype != torch.float32 or scores.numel() < n_docs or not scores.is_contiguous() \
-            or scores.device != X.device:
-        raise TypeError("scores must be a contiguous float32 tensor of n_docs entries on X's device")
+        shape = (n_docs,) if n_outputs == 1 else (n_docs, n_outputs)
+        scores = torch.empty(shape, dtype=torch.float32, device=X.device)
+    elif scores.dtype != torch.float32 or scores.numel() < n_docs * n_outputs or \
+            not scores.is_contiguous() or scores.device != X.device:
+        raise TypeError("scores must be a contiguous float32 tensor of n_docs * n_outputs entries "
+                        "on X's device")
     rc = load_library().tree_ens_predict(h, _stream_of(X, stream), X.data_ptr() if n_docs else None,
                                          n_docs, n_feat, scores.data_ptr() if n_docs else None)
     _check(rc, "tree_ens_predict")
@@ -294,16 +329,28 @@ class TreeEnsemble:
 
     def __init__(self, handle):
         self._h = handle
+        self.n_outputs, self.n_bags = tree_ens_outputs(handle)
 
     @classmethod
     def from_arrays(cls, tree_offsets, feature, threshold, left, right, value,
-                    flags: int = TREE_ENS_RIGHT_IF_GE) -> "TreeEnsemble":
-        return cls(tree_ens_create(tree_offsets, feature, threshold, left, right, value, flags))
+                    flags: int = TREE_ENS_RIGHT_IF_GE, n_outputs: int = 1, n_bags: int = 1) -> "TreeEnsemble":
+        if n_outputs == 1 and n_bags == 1:
+            return cls(tree_ens_create(tree_offsets, feature, threshold, left, right, value, flags))
+        return cls(tree_ens_create_multi(tree_offsets, feature, threshold, left, right, value,
+                                         n_outputs, n_bags, flags))
 
     @classmethod
-    def from_ensemble(cls, ens, flags: int = TREE_ENS_RIGHT_IF_GE) -> "TreeEnsemble":
+    def from_ensemble(cls, ens, flags: int = TREE_ENS_RIGHT_IF_GE, leaf_values=None,
+                      n_bags: int = 1) -> "TreeEnsemble":
+        """``leaf_values`` [n_nodes, n_outputs] replaces ``ens.value`` (vector-valued leaves)."""
+        value, n_out = ens.value, 1
+        if leaf_values is not None:
+            value = np.ascontiguousarray(leaf_values, dtype=np.float32)
+            if value.ndim != 2 or value.shape[0] != ens.n_nodes:
+                raise ValueError("leaf_values must be [n_nodes, n_outputs]")
+            n_out = value.shape[1]
         return cls.from_arrays(ens.tree_offsets, ens.feature, ens.threshold, ens.left, ens.right,
-                               ens.value, flags)
+                               value, flags, n_out, n_bags)
 
     @property
     def handle(self):
@@ -312,7 +359,7 @@ class TreeEnsemble:
         return self._h
 
     def predict(self, X, out=None, stream=None):
-        return tree_ens_predict(self.handle, X, out, stream)
+        return tree_ens_predict(self.handle, X, out, stream, self.n_outputs)
 
     def predict_leaves(self, X, out=None, stream=None):
         return tree_ens_predict_leaves(self.handle, X, out, stream)

@@ -69,11 +69,17 @@ LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
 
 int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
                const float *threshold, const int32_t *left, const int32_t *right,
-               const float *value, uint32_t flags, Packed &out, std::string &err) {
+               const float *value, int32_t n_outputs, uint32_t flags, Packed &out,
+               std::string &err) {
     if (n_trees < 0) {
         err = "n_trees must be >= 0";
         return kErrArg;
     }
+    if (n_outputs < 1 || n_outputs > kMaxOutputs) {
+        err = "n_outputs must be in [1, " + std::to_string(kMaxOutputs) + "]";
+        return kErrArg;
+    }
+    const bool vec = n_outputs > 1;
     if ((flags & ~1u) != 0) {
         err = "unknown flag bits";
         return kErrArg;
@@ -98,8 +104,8 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         err = "a node array is NULL";
         return kErrArg;
     }
-    if (n_nodes >= (int64_t(1) << 32)) {
-        err = "more than 2^32 nodes";
+    if (n_nodes >= (int64_t(1) << 32) || (vec && n_nodes >= (int64_t(1) << 31))) {
+        err = vec ? "more than 2^31 nodes with vector-valued leaves" : "more than 2^32 nodes";
         return kErrModel;
     }
 
@@ -240,6 +246,11 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     p.n_trees = n_trees;
     p.n_cols = n_cols;
     p.plan = plan;
+    p.n_outputs = n_outputs;
+    if (vec) {
+        p.vec_stride = (n_outputs + 3) / 4 * 4;
+        p.leaf_vec.assign(size_t(n_nodes + 1) * size_t(p.vec_stride), 0.0f);
+    }
     p.tree_orig.resize(size_t(n_trees));
     std::iota(p.tree_orig.begin(), p.tree_orig.end(), 0);
     std::stable_sort(p.tree_orig.begin(), p.tree_orig.end(),
@@ -293,6 +304,14 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                 const uint32_t col = uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) *
                                      uint32_t(plan.elem_bytes);
                 r.w = link(uint32_t(new_id[size_t(left[a + i])])) | col;
+            } else if (vec) {
+                // never 0: a coded leaf (code 0 >= thr is false) stays put as well
+                const size_t packed = base + size_t(ni);
+                r.thr_bits = uint32_t(packed) + 2u;
+                for (int32_t c = 0; c < n_outputs; c++)
+                    p.leaf_vec[(packed + 1) * size_t(p.vec_stride) + size_t(c)] =
+                        value[(a + i) * n_outputs + c];
+                r.w = link(uint32_t(ni));
             } else {
                 r.thr_bits = float_bits(value[a + i]);
                 if (plan.coded && r.thr_bits == 0u)
@@ -382,7 +401,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             img[0] = NodeRec{uint32_t(ntr), uint32_t(tl.complete_depth)};
             img[1] = NodeRec{uint32_t(tl.tree_begin),
                              i + 1 < n_level ? p.tile_recs[size_t(p.level_begin[k] + i + 1)] : 0u};
-            const NodeRec zero_leaf{plan.coded ? 0x80000000u : 0u, (zero_addr / 8u) << shift};
+            const NodeRec zero_leaf{zero_record_value(plan, vec), (zero_addr / 8u) << shift};
             for (int32_t t = 0; t < hrecs - kHeaderFixedWords / 2; t++) {
                 NodeRec r = zero_leaf;
                 if (t < ntr) {

@@ -132,19 +132,37 @@ struct Packed {
     // and of all tiles of tiling 0: the launch planner's unit of time
     int32_t level_max_rounds[kTileLevels] = {};
     int64_t total_rounds = 0;
+    // vector-valued leaves (n_outputs > 1): a leaf's threshold slot holds 2 + its packed node
+    // index instead of a value, and row (thr - 1) of leaf_vec holds its n_outputs values,
+    // padded to vec_stride (a multiple of 4) floats; row 0 is zero (the all-zero record's row)
+    int32_t n_outputs = 1;
+    int32_t vec_stride = 0;
+    std::vector<float> leaf_vec;
     // coded models only
     std::vector<float> code_table;         // T_0, T_1, ... concatenated
     std::vector<uint32_t> code_table_off;  // [n_cols + 1] start of T_f in code_table
     std::vector<CodeChunk> code_chunks;    // features grouped for the coding kernel
 };
 
+// Outputs per leaf at most (vector-valued leaves).
+constexpr int kMaxOutputs = 256;
+
+// Threshold slot of the all-zero self-linked record (idle walker slots, root-copy padding):
+// value 0.0 for float leaves, -0.0 for coded ones (never zero bits), and row 0 of the
+// leaf-vector table (all zeros) for vector-valued leaves.
+inline uint32_t zero_record_value(const LdsPlan &plan, bool vec) {
+    return vec ? 1u : plan.coded ? 0x80000000u : 0u;
+}
+
 // Status codes match the public header.
 constexpr int kOk = 0, kErrArg = -1, kErrModel = -2;
 
 // Validate and pack. Returns kOk or an error code with a message in `err`. Pure host code:
 // no HIP call is made, so every model error is reported without a device.
+// value holds n_outputs floats per node ([n_nodes][n_outputs], read at leaves only).
 int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
                const float *threshold, const int32_t *left, const int32_t *right,
-               const float *value, uint32_t flags, Packed &out, std::string &err);
+               const float *value, int32_t n_outputs, uint32_t flags, Packed &out,
+               std::string &err);
 
 } // namespace treeens

@@ -19,10 +19,11 @@
 // Blocks of a last, partial round of workgroups (and every block of a small batch) are split
 // over the tiles; the per-split partial sums are reduced by a second, tiny kernel in a fixed
 // order, so results are deterministic.
-// The same kernel has two more modes: leaf ids (the reached leaf of every (document, tree)) and
+// The same kernel has three more modes: leaf ids (the reached leaf of every (document, tree)),
 // the feature-access trace (the set of distinct features each document's walks compare, the
-// measure of Section 6 / Table 4): per-document bitmasks in LDS, set with an LDS atomic OR at
-// every internal step.
+// measure of Section 6 / Table 4: per-document bitmasks in LDS, set with an LDS atomic OR at
+// every internal step), and vector-valued leaves (a leaf names a row of a leaf-vector table in
+// global memory; a launch sums four of its components).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -66,6 +67,8 @@ constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves
 constexpr int kModeScore = 0;  // scores
 constexpr int kModeLeaves = 1; // leaf ids
 constexpr int kModeUsage = 2;  // per-document feature bitmasks and their popcounts
+constexpr int kModeVector = 3; // four components of vector-valued scores
+constexpr int kVecPerLaunch = 4;
 
 // ------------------------------------------------------------------------------------------
 // kernels
@@ -119,7 +122,8 @@ __device__ __forceinline__ uint32_t narrow_child_coded(uint32_t w, uint32_t code
 }
 
 template <int DL, int K, bool HALF, bool NARROW, bool CODED, int MODE>
-__global__ void __launch_bounds__(kThreads, HALF ? 8 : 4) // min waves per SIMD: 2 or 1 workgroups per CU
+// min waves per SIMD: 2 or 1 workgroups per CU (a feature trace holds a CU alone)
+__global__ void __launch_bounds__(kThreads, HALF && MODE != kModeUsage ? 8 : 4)
 score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, int32_t n_cols,
              const uint2 *__restrict__ images, int32_t slot_recs,
              const uint32_t *__restrict__ tile_recs, int32_t n_tiles, int32_t head_blocks,
@@ -128,7 +132,9 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
              float *__restrict__ scores, int32_t *__restrict__ leaf_ids,
              const int32_t *__restrict__ orig_id, const uint32_t *__restrict__ tree_node_off,
              const int32_t *__restrict__ tree_orig, int32_t n_trees,
-             uint32_t *__restrict__ masks, int32_t mask_words, int32_t usage_off) {
+             uint32_t *__restrict__ masks, int32_t mask_words, int32_t usage_off,
+             const float4 *__restrict__ leaf_vec, int32_t vec_stride4, int32_t n_out,
+             int32_t chunk, double out_scale) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
@@ -140,6 +146,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     //                            two-workgroup plans, so usage launches hold a CU alone
     constexpr bool LEAVES = MODE == kModeLeaves;
     constexpr bool USAGE = MODE == kModeUsage;
+    constexpr bool VEC = MODE == kModeVector;
     constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 + (USAGE ? treeens::kUsageHalfBytes : 0)
                               : treeens::kLdsPerCu;
     __shared__ __align__(16) unsigned char lds[kLds];
@@ -288,12 +295,14 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         }
     }
     if (tid == 0) {
-        // value 0 (as -0.0 for codes, whose leaves never hold zero bits), column 0, self link
-        const uint32_t thr = CODED ? 0x80000000u : 0u;
+        // value 0 (as -0.0 for codes, whose leaves never hold zero bits; the all-zero row 0 of
+        // the leaf-vector table for vector-valued leaves), column 0, self link
+        const uint32_t thr = VEC ? 1u : CODED ? 0x80000000u : 0u;
         *reinterpret_cast<uint2 *>(lds + zero_rec) = make_uint2(thr, (uint32_t(zero_rec) / 8u) << kShift);
     }
 
     double acc = 0.0;
+    double accv[kVecPerLaunch] = {0.0, 0.0, 0.0, 0.0};
     // Walk the tile image in the LDS slot.
     auto walk_tile = [&]() {
         const uint4 h = *reinterpret_cast<const uint4 *>(hdr);
@@ -407,6 +416,20 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                             leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
                         }
                     }
+                } else if constexpr (VEC) {
+                    // a leaf's threshold slot holds its table row + 1 (idle slots: row 0, zeros)
+                    float gs[kVecPerLaunch] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                    for (int i = 0; i < K; ++i) {
+                        const float4 v = leaf_vec[int64_t(rec_thr(nd[i]) - 1u) * vec_stride4 + chunk];
+                        gs[0] += v.x;
+                        gs[1] += v.y;
+                        gs[2] += v.z;
+                        gs[3] += v.w;
+                    }
+#pragma unroll
+                    for (int c = 0; c < kVecPerLaunch; ++c)
+                        accv[c] += double(gs[c]);
                 } else if constexpr (!USAGE) {
                     // K leaf values: exact enough in float, one double add (idle slots hold the
                     // zero record)
@@ -480,6 +503,32 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             leaf_ids[doc0 + dl] = count;
         }
     }
+    if constexpr (VEC) {
+        __syncthreads();
+        double *red = reinterpret_cast<double *>(lds + xs_bytes); // 4 x 1,024 doubles (32 KiB)
+#pragma unroll
+        for (int c = 0; c < kVecPerLaunch; ++c)
+            red[(c * n_walkers + walker) * DL + dl] = accv[c];
+        __syncthreads();
+        if (walker == 0) {
+            const int64_t doc = doc0 + dl;
+            for (int c = 0; c < kVecPerLaunch; ++c) {
+                double sum = 0.0;
+                for (int w = 0; w < n_walkers; ++w)
+                    sum += red[(c * n_walkers + w) * DL + dl];
+                const int oc = kVecPerLaunch * chunk + c;
+                if (doc < n_docs) {
+                    if (n_splits == 1) {
+                        if (oc < n_out)
+                            scores[doc * n_out + oc] = float(sum * out_scale);
+                    } else {
+                        const int64_t tail0 = int64_t(head_blocks) * DL;
+                        partials[(int64_t(split) * (n_docs - tail0) + (doc - tail0)) * kVecPerLaunch + c] = sum;
+                    }
+                }
+            }
+        }
+    }
     if constexpr (MODE == kModeScore) {
         __syncthreads();
         double *red = reinterpret_cast<double *>(lds + xs_bytes);
@@ -492,7 +541,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 sum += red[w * DL + dl];
             if (doc < n_docs) {
                 if (n_splits == 1) {
-                    scores[doc] = float(sum);
+                    scores[doc] = float(sum * out_scale);
                 } else {
                     const int64_t tail0 = int64_t(head_blocks) * DL;
                     partials[int64_t(split) * (n_docs - tail0) + (doc - tail0)] = sum;
@@ -502,11 +551,25 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     }
 }
 
-// Sum of the split partials of each document in a fixed order (so the rounding never
-// changes). Few splits: one thread per document, in split order. Many splits (small batches):
-// one wave per document, lanes interleave the splits, then a fixed butterfly.
+// Sum of the split partials of each entry in a fixed order (so the rounding never changes).
+// Entry j is component j % comps of document j / comps; it goes to output column
+// c_base + j % comps of a row of n_out scores (if that column exists), scaled by out_scale.
+// Few splits: one thread per entry, in split order. Many splits (small batches): one wave per
+// entry, lanes interleave the splits, then a fixed butterfly.
+struct ReduceOut {
+    float *scores;
+    int32_t comps, n_out, c_base;
+    double scale;
+    __device__ void store(int64_t j, double s) const {
+        const int64_t doc = j / comps;
+        const int c = c_base + int(j - doc * comps);
+        if (c < n_out)
+            scores[doc * n_out + c] = float(s * scale);
+    }
+};
+
 __global__ void reduce_partials_thread_kernel(const double *__restrict__ partials, int32_t n_splits,
-                                              int64_t n_docs, float *__restrict__ scores) {
+                                              int64_t n_docs, ReduceOut out) {
     const int64_t d = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (d < n_docs) {
         // eight independent loads in flight, then summed in split order
@@ -523,13 +586,13 @@ __global__ void reduce_partials_thread_kernel(const double *__restrict__ partial
         }
         for (; k < n_splits; ++k)
             s += partials[int64_t(k) * n_docs + d];
-        scores[d] = float(s);
+        out.store(d, s);
     }
 }
 
 __global__ void __launch_bounds__(64)
 reduce_partials_wave_kernel(const double *__restrict__ partials, int32_t n_splits, int64_t n_docs,
-                            float *__restrict__ scores) {
+                            ReduceOut out) {
     const int64_t d = blockIdx.x;
     double s = 0.0;
     for (int k = threadIdx.x; k < n_splits; k += 64)
@@ -538,7 +601,7 @@ reduce_partials_wave_kernel(const double *__restrict__ partials, int32_t n_split
     for (int off = 32; off >= 1; off >>= 1)
         s += __shfl_xor(s, off);
     if (threadIdx.x == 0)
-        scores[d] = float(s);
+        out.store(d, s);
 }
 
 __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
@@ -589,7 +652,8 @@ code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int
 using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *, int32_t,
                          const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
                          float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
-                         int32_t, uint32_t *, int32_t, int32_t);
+                         int32_t, uint32_t *, int32_t, int32_t, const float4 *, int32_t,
+                         int32_t, int32_t, double);
 
 template <int DL, bool HALF, bool NARROW, bool CODED, int MODE>
 ScoreFn pick_k(int k) {
@@ -659,6 +723,12 @@ struct tree_ens {
     uint32_t *d_tree_node_off = nullptr;
     int32_t *d_tree_orig = nullptr;
     int32_t *d_orig_id = nullptr;
+    // vector-valued leaves and bagging: outputs per document, the table of leaf rows, and the
+    // factor 1 / n_bags applied to every sum
+    int32_t n_outputs = 1;
+    int32_t n_bags = 1;
+    int32_t vec_stride = 0;
+    float *d_leaf_vec = nullptr;
     // coded models
     float *d_code_table = nullptr;
     uint32_t *d_code_table_off = nullptr;
@@ -692,6 +762,7 @@ void free_device(tree_ens *h) {
     (void)hipFree(h->d_tree_node_off);
     (void)hipFree(h->d_tree_orig);
     (void)hipFree(h->d_orig_id);
+    (void)hipFree(h->d_leaf_vec);
     (void)hipFree(h->d_code_table);
     (void)hipFree(h->d_code_table_off);
     (void)hipFree(h->d_code_chunks);
@@ -813,14 +884,20 @@ int check_predict_args(const tree_ens *h, const float *X, int64_t n_docs, int32_
     return TREE_ENS_OK;
 }
 
-// MODE kModeScore writes scores; kModeLeaves writes leaf_ids [n_docs][n_trees]; kModeUsage
-// writes per-document feature counts into leaf_ids and, if masks is not NULL, the bitmasks
-// (rows of mask_words words).
+// MODE kModeScore writes scores; kModeVector writes scores [n_docs][n_outputs] (one launch per
+// four outputs); kModeLeaves writes leaf_ids [n_docs][n_trees]; kModeUsage writes per-document
+// feature counts into leaf_ids and, if masks is not NULL, the bitmasks (rows of mask_words
+// words).
 template <int MODE>
 int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_t n_docs,
                    int32_t n_features, float *scores, int32_t *leaf_ids, uint32_t *masks = nullptr,
                    int32_t mask_words = 0) {
-    constexpr bool kScores = MODE == kModeScore; // only scores have split partial sums
+    constexpr bool kScores = MODE == kModeScore || MODE == kModeVector; // split partial sums
+    // entries per document in the partial sums, and launches (four outputs each)
+    const int comps = MODE == kModeVector ? kVecPerLaunch : 1;
+    const int n_chunks = MODE == kModeVector ? (h->n_outputs + kVecPerLaunch - 1) / kVecPerLaunch : 1;
+    if (MODE == kModeVector && h->plan.tile_bytes < kThreads * kVecPerLaunch * int(sizeof(double)))
+        return fail(TREE_ENS_E_ARG, "the tile slot cannot hold the vector reduction");
     const int dl = h->plan.docs_per_block;
     const int64_t n_blocks = (n_docs + dl - 1) / dl;
     if (n_blocks > 0x7fffffff)
@@ -859,7 +936,8 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     bool own_scratch = false; // partials live in the handle's scratch
     std::unique_lock<std::mutex> scratch_lock;
     if (kScores && splits > 1) {
-        if (size_t(splits) * size_t(tail_docs) <= kScratchDoubles) {
+        const size_t n_partials = size_t(splits) * size_t(tail_docs) * size_t(comps);
+        if (n_partials <= kScratchDoubles) {
             scratch_lock = std::unique_lock<std::mutex>(h->scratch_mu);
             if (h->scratch_used && h->scratch_stream != stream) {
                 e = hipStreamWaitEvent(stream, h->scratch_done, 0);
@@ -869,8 +947,8 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
             partials = h->d_scratch;
             own_scratch = true;
         } else {
-            e = hipMallocAsync(reinterpret_cast<void **>(&partials),
-                               size_t(splits) * size_t(tail_docs) * sizeof(double), stream);
+            e = hipMallocAsync(reinterpret_cast<void **>(&partials), n_partials * sizeof(double),
+                               stream);
             if (e != hipSuccess)
                 return hip_fail(e, "hipMallocAsync(partials)");
         }
@@ -904,21 +982,30 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         docs = codes;
         row_stride = h->n_cols;
     }
-    hipLaunchKernelGGL(fn, dim3(unsigned(n_wgs)), dim3(kThreads), 0, stream, docs, n_docs,
-                       row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs, n_tiles,
-                       int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec, partials,
-                       scores, leaf_ids, h->d_orig_id, h->d_tree_node_off, h->d_tree_orig,
-                       h->n_trees, masks, mask_words, h->plan.usage_off);
-    e = hipGetLastError();
-    if (e == hipSuccess && partials) {
-        float *tail_scores = scores + shape.head * dl;
-        if (splits <= 64)
-            hipLaunchKernelGGL(reduce_partials_thread_kernel, dim3(unsigned((tail_docs + 255) / 256)),
-                               dim3(256), 0, stream, partials, splits, tail_docs, tail_scores);
-        else
-            hipLaunchKernelGGL(reduce_partials_wave_kernel, dim3(unsigned(tail_docs)), dim3(64), 0,
-                               stream, partials, splits, tail_docs, tail_scores);
+    const double scale = 1.0 / double(h->n_bags);
+    const int n_out = MODE == kModeVector ? h->n_outputs : 1;
+    for (int chunk = 0; chunk < n_chunks && e == hipSuccess; ++chunk) {
+        hipLaunchKernelGGL(fn, dim3(unsigned(n_wgs)), dim3(kThreads), 0, stream, docs, n_docs,
+                           row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs,
+                           n_tiles, int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec,
+                           partials, scores, leaf_ids, h->d_orig_id, h->d_tree_node_off,
+                           h->d_tree_orig, h->n_trees, masks, mask_words, h->plan.usage_off,
+                           reinterpret_cast<const float4 *>(h->d_leaf_vec), h->vec_stride / 4, n_out,
+                           chunk, scale);
         e = hipGetLastError();
+        if (e == hipSuccess && partials) {
+            // the tail blocks' entries, in [doc][component] order
+            const int64_t n_entries = tail_docs * comps;
+            const ReduceOut out{scores + shape.head * dl * n_out, comps, n_out, chunk * comps, scale};
+            if (splits <= 64)
+                hipLaunchKernelGGL(reduce_partials_thread_kernel,
+                                   dim3(unsigned((n_entries + 255) / 256)), dim3(256), 0, stream,
+                                   partials, splits, n_entries, out);
+            else
+                hipLaunchKernelGGL(reduce_partials_wave_kernel, dim3(unsigned(n_entries)), dim3(64),
+                                   0, stream, partials, splits, n_entries, out);
+            e = hipGetLastError();
+        }
     }
     if (own_scratch) {
         // the next call from another stream waits for this one's reduction
@@ -948,15 +1035,25 @@ extern "C" {
 int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offsets,
                     const int32_t *feature, const float *threshold, const int32_t *left,
                     const int32_t *right, const float *value, uint32_t flags) {
+    return tree_ens_create_multi(out, n_trees, tree_offsets, feature, threshold, left, right, value,
+                                 1, 1, flags);
+}
+
+int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offsets,
+                          const int32_t *feature, const float *threshold, const int32_t *left,
+                          const int32_t *right, const float *value, int32_t n_outputs,
+                          int32_t n_bags, uint32_t flags) {
     g_err.clear();
     if (!out)
         return fail(TREE_ENS_E_ARG, "out is NULL");
     *out = nullptr;
+    if (n_bags < 1)
+        return fail(TREE_ENS_E_ARG, "n_bags must be >= 1");
     Packed p;
     std::string err;
     int rc;
     try {
-        rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value, flags,
+        rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value, n_outputs, flags,
                                  p, err);
     } catch (const std::bad_alloc &) {
         return fail(TREE_ENS_E_NOMEM, "host allocation failed while packing");
@@ -972,6 +1069,9 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
     h->max_depth = p.max_depth;
     h->n_nodes = int64_t(p.nodes.size());
     h->plan = p.plan;
+    h->n_outputs = p.n_outputs;
+    h->n_bags = n_bags;
+    h->vec_stride = p.vec_stride;
     std::memcpy(h->level_begin, p.level_begin, sizeof h->level_begin);
     hipError_t e = hipGetDevice(&h->device);
     std::memcpy(h->level_image_off, p.level_image_off, sizeof h->level_image_off);
@@ -995,6 +1095,8 @@ int tree_ens_create(tree_ens_t **out, int32_t n_trees, const int64_t *tree_offse
         e = hipMalloc(reinterpret_cast<void **>(&h->d_scratch), kScratchDoubles * sizeof(double));
     if (e == hipSuccess)
         e = hipEventCreateWithFlags(&h->scratch_done, hipEventDisableTiming);
+    if (e == hipSuccess && p.n_outputs > 1)
+        e = upload(&h->d_leaf_vec, p.leaf_vec);
     if (e == hipSuccess && p.plan.coded) {
         e = upload(&h->d_code_table, p.code_table);
         if (e == hipSuccess)
@@ -1025,11 +1127,14 @@ int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (h->n_trees == 0) {
         const int bs = 256;
-        hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n_docs + bs - 1) / bs)), dim3(bs), 0, s,
-                           scores, n_docs);
+        const int64_t n = n_docs * h->n_outputs;
+        hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n + bs - 1) / bs)), dim3(bs), 0, s,
+                           scores, n);
         hipError_t e = hipGetLastError();
         return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "kernel launch");
     }
+    if (h->n_outputs > 1)
+        return launch_predict<kModeVector>(h, s, X, n_docs, n_features, scores, nullptr);
     return launch_predict<kModeScore>(h, s, X, n_docs, n_features, scores, nullptr);
 }
 
@@ -1049,6 +1154,8 @@ int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, i
 int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
                           int32_t n_features, const int64_t *group_offsets, int64_t n_groups,
                           int32_t k, float *scores, int32_t *top_idx, float *top_scores) {
+    if (h && h->n_outputs != 1)
+        return fail(TREE_ENS_E_ARG, "reranking needs one score per document (n_outputs = 1)");
     int rc = tree_ens_predict(h, stream, X, n_docs, n_features, scores);
     if (rc != TREE_ENS_OK)
         return rc;
@@ -1098,6 +1205,17 @@ int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features, 
         *n_tiles = h->level_begin[1] - h->level_begin[0];
     if (docs_per_block)
         *docs_per_block = h->plan.docs_per_block;
+    return TREE_ENS_OK;
+}
+
+int tree_ens_outputs(const tree_ens_t *h, int32_t *n_outputs, int32_t *n_bags) {
+    g_err.clear();
+    if (!h)
+        return fail(TREE_ENS_E_ARG, "handle is NULL");
+    if (n_outputs)
+        *n_outputs = h->n_outputs;
+    if (n_bags)
+        *n_bags = h->n_bags;
     return TREE_ENS_OK;
 }
 

@@ -49,16 +49,17 @@ extern "C" {
 const char *emu_message(void) { return g_msg.c_str(); }
 
 // Walk all documents through tiling `level`. Outputs leaf ids [n_docs][n_trees] (input node ids)
-// and fp64 scores. Returns 0, or 1 with a message naming the first violated invariant, or a
-// negative packer status.
+// and fp64 scores [n_docs][n_outputs] (vector-valued leaves read through the leaf-vector table).
+// Returns 0, or 1 with a message naming the first violated invariant, or a negative packer
+// status.
 int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
              const float *threshold, const int32_t *left, const int32_t *right, const float *value,
-             uint32_t flags, const float *X, int64_t n_docs, int32_t n_features, int32_t level,
-             int32_t *leaf_ids, double *scores, int32_t *plan_out) {
+             int32_t n_outputs, uint32_t flags, const float *X, int64_t n_docs, int32_t n_features,
+             int32_t level, int32_t *leaf_ids, double *scores, int32_t *plan_out) {
     treeens::Packed p;
     std::string err;
     const int rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value,
-                                       flags, p, err);
+                                       n_outputs, flags, p, err);
     if (rc != treeens::kOk) {
         g_msg = err;
         return rc;
@@ -116,7 +117,11 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
     std::vector<int32_t> seen(size_t(n_trees), 0);
     for (int64_t i = 0; i < n_docs * n_trees; i++)
         leaf_ids[i] = -1;
-    for (int64_t d = 0; d < n_docs; d++)
+    const bool vec = n_outputs > 1;
+    if (vec && (p.vec_stride < n_outputs || p.vec_stride % 4 ||
+                p.leaf_vec.size() != size_t(p.nodes.size() + 1) * size_t(p.vec_stride)))
+        return bad("leaf-vector table has the wrong shape");
+    for (int64_t d = 0; d < n_docs * n_outputs; d++)
         scores[d] = 0.0;
 
     for (int64_t doc0 = 0; doc0 < n_docs; doc0 += DL) {
@@ -134,7 +139,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                 }
             }
         }
-        const treeens::NodeRec z{pl.coded ? 0x80000000u : 0u, (zero / 8u) << shift};
+        const treeens::NodeRec z{treeens::zero_record_value(pl, vec), (zero / 8u) << shift};
         std::memcpy(lds.data() + zero, &z, 8);
 
         for (int32_t t = t0; t < t1; t++) {
@@ -219,7 +224,16 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                         return bad("leaf outside its tree");
                     const int32_t orig_tree = p.tree_orig[size_t(gt)];
                     leaf_ids[doc * n_trees + orig_tree] = p.orig_id[p.tree_node_off[size_t(gt)] + size_t(self)];
-                    scores[doc] += double(as_float(r.thr_bits));
+                    if (vec) {
+                        const int64_t row = int64_t(r.thr_bits) - 1;
+                        if (row < 1 || row > int64_t(p.nodes.size()))
+                            return bad("leaf names a row outside the leaf-vector table");
+                        for (int c = 0; c < n_outputs; c++)
+                            scores[doc * n_outputs + c] +=
+                                double(p.leaf_vec[size_t(row) * size_t(p.vec_stride) + size_t(c)]);
+                    } else {
+                        scores[doc] += double(as_float(r.thr_bits));
+                    }
                 }
                 seen[size_t(p.tree_orig[size_t(gt)])]++;
             }

@@ -29,24 +29,26 @@ def emu(tmp_path_factory):
     lib = ctypes.CDLL(out)
     P = ctypes.c_void_p
     lib.emu_walk.restype = ctypes.c_int
-    lib.emu_walk.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_uint32, P, ctypes.c_int64,
-                             ctypes.c_int32, ctypes.c_int32, P, P, P]
+    lib.emu_walk.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_uint32, P,
+                             ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
     lib.emu_message.restype = ctypes.c_char_p
     return lib
 
 
-def _walk(lib, ens, X, level, flags=0):
+def _walk(lib, ens, X, level, flags=0, leaf_values=None):
+    vals = ens.value if leaf_values is None else leaf_values
+    n_out = 1 if leaf_values is None else leaf_values.shape[1]
     arrs = [np.ascontiguousarray(ens.tree_offsets, np.int64), np.ascontiguousarray(ens.feature, np.int32),
             np.ascontiguousarray(ens.threshold, np.float32), np.ascontiguousarray(ens.left, np.int32),
-            np.ascontiguousarray(ens.right, np.int32), np.ascontiguousarray(ens.value, np.float32)]
+            np.ascontiguousarray(ens.right, np.int32), np.ascontiguousarray(vals, np.float32)]
     X = np.ascontiguousarray(X, np.float32)
     leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
-    scores = np.empty(X.shape[0], np.float64)
+    scores = np.empty((X.shape[0], n_out), np.float64)
     plan = np.zeros(6, np.int32)
-    rc = lib.emu_walk(ens.n_trees, *[a.ctypes.data for a in arrs], flags, X.ctypes.data, X.shape[0],
-                      X.shape[1], level, leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
+    rc = lib.emu_walk(ens.n_trees, *[a.ctypes.data for a in arrs], n_out, flags, X.ctypes.data,
+                      X.shape[0], X.shape[1], level, leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
     assert rc == 0, lib.emu_message().decode()
-    return leaves, scores, plan
+    return leaves, (scores[:, 0] if leaf_values is None else scores), plan
 
 
 def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
@@ -93,3 +95,24 @@ def test_workload_shapes(emu, cfg_id, n_trees, n_docs, expect):
     assert plan[0] == expect["dl"] and plan[3] == expect["coded"], plan
     if "narrow" in expect:
         assert plan[2] == expect["narrow"], plan
+
+
+@pytest.mark.parametrize("cfg_id,n_trees,n_out,kind", [
+    (1, None, 3, "probs"),
+    (2, 120, 5, "class"),
+    (4, 800, 2, "dense"),  # complete-depth tiles
+    (5, 60, 7, "dense"),  # coded documents
+])
+def test_vector_valued_leaves(emu, cfg_id, n_trees, n_out, kind):
+    """Leaf records name their row of the leaf-vector table (row 0 = the zero record's); the
+    rows summed over the walks equal the oracle's vector-valued scores."""
+    cfg = W.CONFIGS[cfg_id]
+    ens = W.make_ensemble(cfg, n_trees=n_trees)
+    X = W.make_docs(cfg, n_docs=90)
+    vals = W.make_leaf_vectors(ens, n_out, kind, seed=cfg_id)
+    ref = oracle.score_multi(ens, vals, X)
+    _, ref_leaves, _ = oracle.score(ens, X)
+    for lv in (0, 4):
+        leaves, scores, _ = _walk(emu, ens, X, lv, leaf_values=vals)
+        np.testing.assert_array_equal(leaves, ref_leaves, err_msg=f"tiling {lv}")
+        np.testing.assert_allclose(scores, ref, rtol=1e-12, atol=1e-12, err_msg=f"tiling {lv}")
