@@ -44,5 +44,22 @@ def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
     return out
 
 
+C_CLIENT_SRC = os.path.join(ROOT, "tests", "c_client.c")
+C_CLIENT = os.path.join(ROOT, "tests", "c_client")
+
+
+def build_c_client(out: str = C_CLIENT, lib_dir: str = PKG) -> str:
+    """Compile the plain-C test client of the C ABI (gcc, no HIP device code) against the
+    built library; it finds the library next to this file through its run path."""
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(_hipcc())))
+    rel = os.path.relpath(lib_dir, os.path.dirname(os.path.abspath(out)))
+    subprocess.run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                    "-I", INCLUDE, "-I", os.path.join(rocm, "include"), C_CLIENT_SRC, "-o", out,
+                    "-L", lib_dir, "-ltreeens", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+                    f"-Wl,-rpath,$ORIGIN/{rel}", "-Wl,-rpath," + os.path.join(rocm, "lib")], check=True)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_c_client())

@@ -107,3 +107,13 @@ def test_null_arguments(lib):
     h = ctypes.c_void_p()
     assert lib.tree_ens_create(ctypes.byref(h), -1, None, None, None, None, None, None, 0) == T.TREE_ENS_E_ARG
     assert h.value is None
+
+
+def test_c_client_reports_errors_without_a_device(tmp_path):
+    """A plain C program linked against the library (no Python, no torch) sees the same model
+    and argument errors through include/tree_ens.h."""
+    import subprocess
+    from paper_1212_2287_amd import _build
+    exe = _build.build_c_client(out=str(tmp_path / "c_client"))
+    r = subprocess.run([exe, "errors"], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
