@@ -442,8 +442,12 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             while (fe < n_cols && fe - fb < kCodeChunkFeatures &&
                    p.code_table_off[size_t(fe) + 1] - p.code_table_off[size_t(fb)] <= uint32_t(kCodeTableFloats))
                 fe++;
+            int32_t steps = 0;
+            for (int32_t f = fb; f < fe; f++)
+                while ((p.code_table_off[size_t(f) + 1] - p.code_table_off[size_t(f)]) >> steps)
+                    steps++;
             p.code_chunks.push_back(CodeChunk{fb, fe, int32_t(p.code_table_off[size_t(fb)]),
-                                              int32_t(p.code_table_off[size_t(fe)])});
+                                              int32_t(p.code_table_off[size_t(fe)]), steps});
             fb = fe;
         }
     }

@@ -94,6 +94,7 @@ struct LdsPlan {
 struct CodeChunk {
     int32_t f_begin, f_end;         // features [f_begin, f_end)
     int32_t table_begin, table_end; // their thresholds in the concatenated table
+    int32_t search_steps;           // bits of the longest threshold list of the chunk
 };
 constexpr int kCodeTableFloats = 16384;  // LDS thresholds per coding workgroup (64 KiB)
 constexpr int kCodeChunkFeatures = 256;  // features per coding workgroup at most

@@ -611,9 +611,12 @@ __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
 }
 
 // Threshold codes of a block of documents for a chunk of features: code_f(x) is the number of
-// f's sorted distinct thresholds t with x >= t (upper-bound binary search over the chunk's
-// thresholds, staged in LDS; a NaN x compares false everywhere and gets 0). Output rows hold
-// n_cols 16-bit codes.
+// f's sorted distinct thresholds t with x >= t (a NaN x compares false everywhere and gets 0).
+// The chunk's thresholds are staged in LDS; the count is found by a branch-free binary descent
+// of the chunk's fixed number of steps (2^steps exceeds every list of the chunk), the same for
+// every lane. Thread e takes elements e, e + 1,024, ... of the block's [doc][feature] order,
+// stepping its (document, feature) pair without a division. Output rows hold n_cols 16-bit
+// codes.
 constexpr int kCodeThreads = 1024;
 __global__ void __launch_bounds__(kCodeThreads)
 code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
@@ -631,21 +634,26 @@ code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int
     __syncthreads();
     const int64_t d0 = int64_t(blockIdx.x) * docs_per_wg;
     const int n = int(min<int64_t>(docs_per_wg, n_docs - d0)) * nf;
+    // nf <= 256: every step moves at least 4 documents on
+    const int step_d = kCodeThreads / nf, step_j = kCodeThreads - step_d * nf;
+    int d = int(threadIdx.x) / nf, j = int(threadIdx.x) - d * nf;
     for (int e = threadIdx.x; e < n; e += kCodeThreads) {
-        const int d = e / nf;
-        const int j = e - d * nf;
         const int64_t doc = d0 + d;
         const float x = X[doc * n_features + ch.f_begin + j];
-        const uint32_t first = toff[j];
-        uint32_t lo = first, hi = toff[j + 1];
-        while (lo < hi) {
-            const uint32_t mid = (lo + hi) >> 1;
-            if (x >= tab[mid])
-                lo = mid + 1;
-            else
-                hi = mid;
+        const uint32_t first = toff[j], len = toff[j + 1] - first;
+        uint32_t pos = 0; // thresholds known to be <= x
+        for (int s = ch.search_steps - 1; s >= 0; --s) {
+            const uint32_t probe = pos + (1u << s);
+            if (probe <= len && x >= tab[first + probe - 1])
+                pos = probe;
         }
-        codes[doc * n_cols + ch.f_begin + j] = uint16_t(lo - first);
+        codes[doc * n_cols + ch.f_begin + j] = uint16_t(pos);
+        d += step_d;
+        j += step_j;
+        if (j >= nf) {
+            j -= nf;
+            ++d;
+        }
     }
 }
 

@@ -42,6 +42,31 @@ uint16_t code_of(const treeens::Packed &p, int f, float x) {
     return c;
 }
 
+// code_f(x) by the coding kernel's branch-free descent over its chunk's table: the largest pos
+// with x >= t[pos - 1], found in the chunk's fixed number of halving steps. Returns -1 when the
+// chunk layout cannot hold feature f's list.
+int32_t code_by_descent(const treeens::Packed &p, int f, float x) {
+    for (const treeens::CodeChunk &ch : p.code_chunks) {
+        if (f < ch.f_begin || f >= ch.f_end)
+            continue;
+        const uint32_t first = p.code_table_off[size_t(f)];
+        const uint32_t len = p.code_table_off[size_t(f) + 1] - first;
+        if (ch.search_steps < 0 || ch.search_steps > 16 || (uint64_t(1) << ch.search_steps) <= len ||
+            int64_t(first) < ch.table_begin || int64_t(first + len) > ch.table_end ||
+            ch.table_end - ch.table_begin > treeens::kCodeTableFloats ||
+            ch.f_end - ch.f_begin > treeens::kCodeChunkFeatures)
+            return -1;
+        uint32_t pos = 0;
+        for (int s = ch.search_steps - 1; s >= 0; --s) {
+            const uint32_t probe = pos + (1u << s);
+            if (probe <= len && x >= p.code_table[first + probe - 1])
+                pos = probe;
+        }
+        return int32_t(pos);
+    }
+    return -1;
+}
+
 } // namespace
 
 extern "C" {
@@ -135,6 +160,9 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                     std::memcpy(dst, &v, 4);
                 } else {
                     uint16_t v = c == 0 || doc >= n_docs ? 0 : code_of(p, c - 1, X[doc * n_features + c - 1]);
+                    if (c > 0 && doc < n_docs &&
+                        code_by_descent(p, c - 1, X[doc * n_features + c - 1]) != int32_t(v))
+                        return bad("the coding kernel's descent disagrees with the threshold count");
                     std::memcpy(dst, &v, 2);
                 }
             }

@@ -116,3 +116,23 @@ def test_vector_valued_leaves(emu, cfg_id, n_trees, n_out, kind):
         leaves, scores, _ = _walk(emu, ens, X, lv, leaf_values=vals)
         np.testing.assert_array_equal(leaves, ref_leaves, err_msg=f"tiling {lv}")
         np.testing.assert_allclose(scores, ref, rtol=1e-12, atol=1e-12, err_msg=f"tiling {lv}")
+
+
+def test_coded_documents_with_corner_values(emu):
+    """Coded plan: NaN, +-inf, +-0 and values equal to thresholds; the emulator checks every
+    staged code of the coding kernel's branch-free descent against a plain count."""
+    cfg = W.CONFIGS[5]
+    ens = W.make_ensemble(cfg, n_trees=40)
+    X = W.make_docs(cfg, n_docs=80)
+    rng = np.random.default_rng(0)
+    internal = np.nonzero(ens.feature >= 0)[0]
+    for k in range(400):  # exact ties with thresholds of the features the nodes read
+        n = internal[rng.integers(0, internal.size)]
+        X[rng.integers(0, 80), ens.feature[n]] = ens.threshold[n]
+    X[1] = np.nan
+    X[2] = np.inf
+    X[3] = -np.inf
+    X[4] = -0.0
+    X[5, ::3] = np.float32(3.4e38)
+    plan = _check(emu, ens, X, levels=(0,))
+    assert plan[3] == 1, plan
