@@ -290,6 +290,43 @@ def multi_output(T, W, ens, Xd, cfg, scalar_ms, reps=10):
     return out
 
 
+def codegen(T, W, reps=10):
+    """The model-specialised kernel (TREE_ENS_CODEGEN, the CodeGen form of Section 3) against
+    the generic one on small models: the tiny workload, and prefixes of the ranking and the
+    shallow workloads (compile time included in the record)."""
+    import torch
+    out = {}
+    for name, cfg_id, n_trees, n_docs in (("tiny_10x8", 1, None, None), ("rank_1kx32_200trees", 2, 200, None),
+                                          ("shallow_20kx8_1000trees", 4, 1000, None)):
+        cfg = W.CONFIGS[cfg_id]
+        ens = W.make_ensemble(cfg, n_trees=n_trees)
+        Xd = torch.from_numpy(W.make_docs(cfg, n_docs=n_docs)).to("cuda")
+        rec = {"trees": ens.n_trees, "nodes": ens.n_nodes, "docs": int(Xd.shape[0])}
+        for label, flags in (("generic", 0), ("codegen", T.TREE_ENS_CODEGEN)):
+            t0 = time.perf_counter()
+            h = T.tree_ens_create(ens.tree_offsets, ens.feature, ens.threshold, ens.left, ens.right,
+                                  ens.value, flags)
+            create_s = time.perf_counter() - t0
+            with T.TreeEnsemble(h) as m:
+                o = torch.empty(Xd.shape[0], dtype=torch.float32, device="cuda")
+                for _ in range(3):
+                    m.predict(Xd, o)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    m.predict(Xd, o)
+                e1.record()
+                torch.cuda.synchronize()
+                ms = e0.elapsed_time(e1) / reps
+            rec[label] = {"ms": ms, "create_s": create_s,
+                          "doc_tree_per_s": Xd.shape[0] * ens.n_trees / (ms * 1e-3)}
+        out[name] = rec
+        del Xd
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(W, cfg_id, budget_s=10.0):
     import numpy as np
     import oracle
@@ -455,7 +492,12 @@ def main() -> int:
     torch.cuda.empty_cache()
 
     extra = {}
+    cg = None
     if not args.no_extra:
+        cg = codegen(T, W)
+        log("codegen vs generic: " + ", ".join(
+            f"{k} {v['codegen']['ms']:.3f} / {v['generic']['ms']:.3f} ms (compile {v['codegen']['create_s']:.1f} s)"
+            for k, v in cg.items()))
         for c, steps, samp in ((1, 20, None), (3, 10, None), (4, 5, None), (5, 3, 16384)):
             r, m, _, xd, o = measure_config(T, W, c, steps, 1, visits_sample=samp)
             r.pop("model", None)
@@ -480,7 +522,7 @@ def main() -> int:
                    "docs_per_block": rec["model"]["docs_per_block"]},
         "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"],
         "latency_100doc_us": lat, "rerank": rr, "feature_usage": fu,
-        "multi_output": mo, "visits": rec["visits"],
+        "multi_output": mo, "codegen": cg, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
         "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
     }

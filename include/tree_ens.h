@@ -40,6 +40,14 @@ typedef struct tree_ens tree_ens_t;
 /* create-time flags */
 #define TREE_ENS_RIGHT_IF_GE 0u /* right iff x[f] >= theta: the paper's rule (default) */
 #define TREE_ENS_RIGHT_IF_GT 1u /* right iff x[f] >  theta: the other tie convention */
+/* Also compile, at create time, a scoring kernel specialised for the model (the CodeGen form of
+ * Section 3: the trees as nested if/else blocks with constant feature ids, thresholds and leaf
+ * values; one document per thread, features read in place) with hiprtc; tree_ens_predict then
+ * runs it. Other entry points keep the generic kernels. Models of at most 65,536 nodes and
+ * depth 64, one value per leaf (else TREE_ENS_E_MODEL / TREE_ENS_E_ARG); a compiler failure is
+ * TREE_ENS_E_DEVICE with the compiler log in the message. Compiling takes about 6 s per
+ * 15,000 nodes (this call returns when it is done). */
+#define TREE_ENS_CODEGEN 2u
 
 /*
  * tree_ens_create -- validate an ensemble given as flat host arrays, pack it for the GPU and
@@ -57,7 +65,7 @@ typedef struct tree_ens tree_ens_t;
  *   left, right   [n_nodes] int32: tree-local child ids of an internal node; ignored for leaves.
  *                 Node 0 of every tree is its root.
  *   value         [n_nodes] float: leaf values; ignored for internal nodes.
- *   flags         TREE_ENS_RIGHT_IF_GE or TREE_ENS_RIGHT_IF_GT.
+ *   flags         TREE_ENS_RIGHT_IF_GE or TREE_ENS_RIGHT_IF_GT, optionally | TREE_ENS_CODEGEN.
  *
  * All arrays are host memory, read during the call only; the caller keeps ownership. Node ids
  * need not be in any particular order. TREE_ENS_E_MODEL is returned when a child id is out of
@@ -192,6 +200,20 @@ int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int
 int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features,
                   int32_t *max_depth, int64_t *packed_bytes, int32_t *n_tiles,
                   int32_t *docs_per_block);
+
+/*
+ * tree_ens_codegen_source -- the HIP source that TREE_ENS_CODEGEN compiles for a model (for
+ * inspection or offline compilation; its entry point is `tree_ens_cg(const float *X,
+ * long long n_docs, int n_features, float *scores, double scale)`, one document per thread in
+ * blocks of 256). Model arguments and validation as tree_ens_create; host only.
+ *   buf, buf_size  receives the source, truncated to buf_size - 1 characters and NUL-terminated
+ *                  (buf may be NULL when buf_size is 0).
+ *   src_len        receives the full length without the NUL (may be NULL).
+ */
+int tree_ens_codegen_source(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                            const float *threshold, const int32_t *left, const int32_t *right,
+                            const float *value, uint32_t flags, char *buf, int64_t buf_size,
+                            int64_t *src_len);
 
 /* tree_ens_outputs -- the handle's outputs per document and bag count (either pointer may be
  * NULL). */

@@ -26,6 +26,7 @@ TREE_ENS_E_DEVICE = -4
 TREE_ENS_E_NOMEM = -5
 TREE_ENS_RIGHT_IF_GE = 0
 TREE_ENS_RIGHT_IF_GT = 1
+TREE_ENS_CODEGEN = 2  # also compile a kernel specialised for the model (hiprtc)
 
 _CODE_NAMES = {0: "OK", -1: "E_ARG", -2: "E_MODEL", -3: "E_SHAPE", -4: "E_DEVICE", -5: "E_NOMEM"}
 
@@ -63,6 +64,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tree_ens_create.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, P, P, u32]
     lib.tree_ens_create_multi.restype = ctypes.c_int
     lib.tree_ens_create_multi.argtypes = [ctypes.POINTER(P), i32, P, P, P, P, P, P, i32, i32, u32]
+    lib.tree_ens_codegen_source.restype = ctypes.c_int
+    lib.tree_ens_codegen_source.argtypes = [i32, P, P, P, P, P, P, u32, P, i64, P]
     lib.tree_ens_outputs.restype = ctypes.c_int
     lib.tree_ens_outputs.argtypes = [P, P, P]
     lib.tree_ens_predict.restype = ctypes.c_int
@@ -148,6 +151,20 @@ def tree_ens_create_multi(tree_offsets, feature, threshold, left, right, value, 
     rc = lib.tree_ens_create_multi(ctypes.byref(h), n_trees, *ptrs, int(n_outputs), int(n_bags), int(flags))
     _check(rc, "tree_ens_create_multi")
     return h
+
+
+def tree_ens_codegen_source(tree_offsets, feature, threshold, left, right, value,
+                            flags: int = TREE_ENS_RIGHT_IF_GE) -> str:
+    """The HIP source TREE_ENS_CODEGEN compiles for the model (host only)."""
+    lib = load_library()
+    n_trees, ptrs, _keep = _model_args(tree_offsets, feature, threshold, left, right, value)
+    n = ctypes.c_int64()
+    _check(lib.tree_ens_codegen_source(n_trees, *ptrs, int(flags), None, 0, ctypes.byref(n)),
+           "tree_ens_codegen_source")
+    buf = ctypes.create_string_buffer(n.value + 1)
+    _check(lib.tree_ens_codegen_source(n_trees, *ptrs, int(flags), buf, n.value + 1, None),
+           "tree_ens_codegen_source")
+    return buf.value.decode()
 
 
 def tree_ens_outputs(h) -> tuple[int, int]:

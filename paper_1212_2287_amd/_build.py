@@ -29,18 +29,23 @@ def _hipcc() -> str:
 
 
 def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
-    """Compile the packer (host C++) and the kernels + C ABI (HIP) into one shared library."""
+    """Compile the packer and the code generator (host C++) and the kernels + C ABI (HIP) into
+    one shared library (linked with hiprtc for the model-specialised kernels)."""
     tmp = out + ".tmp"
-    obj = out + ".pack.o"
     run = (lambda c: subprocess.run(c, check=True)) if verbose else \
         (lambda c: subprocess.run(c, check=True, stdout=subprocess.DEVNULL))
-    run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", *[f"-D{d}" for d in defines], "-c",
-         os.path.join(CSRC, "pack.cpp"), "-o", obj])
+    objs = []
+    for name in ("pack", "codegen"):
+        o = f"{out}.{name}.o"
+        run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", *[f"-D{d}" for d in defines], "-c",
+             os.path.join(CSRC, f"{name}.cpp"), "-o", o])
+        objs.append(o)
     run([_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC, "-shared",
-         os.path.join(CSRC, "tree_ens.hip"), os.path.join(CSRC, "topk.hip"), "-x", "none", obj,
-         "-o", tmp])
+         os.path.join(CSRC, "tree_ens.hip"), os.path.join(CSRC, "topk.hip"), "-x", "none", *objs,
+         "-lhiprtc", "-o", tmp])
     os.replace(tmp, out)
-    os.remove(obj)
+    for o in objs:
+        os.remove(o)
     return out
 
 

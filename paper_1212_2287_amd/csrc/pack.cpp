@@ -80,7 +80,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         return kErrArg;
     }
     const bool vec = n_outputs > 1;
-    if ((flags & ~1u) != 0) {
+    if ((flags & ~(1u | kCodegenFlag)) != 0) {
         err = "unknown flag bits";
         return kErrArg;
     }

@@ -155,6 +155,14 @@ inline uint32_t zero_record_value(const LdsPlan &plan, bool vec) {
     return vec ? 1u : plan.coded ? 0x80000000u : 0u;
 }
 
+// Kernels specialised for one model (create flag TREE_ENS_CODEGEN): limits of the generated
+// program and its block size.
+constexpr uint32_t kCodegenFlag = 2u;
+constexpr int kCodegenMaxNodes = 1 << 16;
+constexpr int kCodegenMaxDepth = 64;
+constexpr int kCodegenThreads = 256;
+constexpr int kCodegenTreesPerFunction = 32;
+
 // Status codes match the public header.
 constexpr int kOk = 0, kErrArg = -1, kErrModel = -2;
 
@@ -165,5 +173,12 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                const float *threshold, const int32_t *left, const int32_t *right,
                const float *value, int32_t n_outputs, uint32_t flags, Packed &out,
                std::string &err);
+
+// HIP source of a scoring kernel specialised for the model (nested if/else with constant
+// feature ids, thresholds and leaf values; entry point `tree_ens_cg`). Validates the model as
+// pack_model does; kErrModel beyond kCodegenMaxNodes nodes or depth kCodegenMaxDepth.
+int codegen_source(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                   const float *threshold, const int32_t *left, const int32_t *right,
+                   const float *value, uint32_t flags, std::string &src, std::string &err);
 
 } // namespace treeens

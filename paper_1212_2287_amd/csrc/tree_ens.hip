@@ -25,6 +25,7 @@
 // every internal step), and vector-valued leaves (a leaf names a row of a leaf-vector table in
 // global memory; a launch sums four of its components).
 #include <hip/hip_runtime.h>
+#include <hip/hiprtc.h>
 
 #include <algorithm>
 #include <cmath>
@@ -139,7 +140,9 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
     //   [0, xs_bytes)            document tile, [(n_cols + 1) x DL] values
-    //   [xs_bytes, zero_rec)     tile slot: the current tile image (header, then node records)
+    //   [xs_bytes, zero_rec)     tile slot: the current tile image (header, then node records);
+    //                            after the last tile, the cross-walker reduction (1,024 doubles,
+    //                            4 x 1,024 with vector-valued leaves)
     //   zero_rec (8 bytes)       all-zero self-linked leaf of value 0, for idle walker slots
     //   usage_off                usage mode: word j of document lane dl's feature bitmask at
     //                            [j * DL + dl] (32 feature ids a word); past the 80 KB half of
@@ -742,6 +745,9 @@ struct tree_ens {
     uint32_t *d_code_table_off = nullptr;
     treeens::CodeChunk *d_code_chunks = nullptr;
     int32_t n_code_chunks = 0;
+    // kernel specialised for the model (TREE_ENS_CODEGEN), used by tree_ens_predict
+    hipModule_t cg_module = nullptr;
+    hipFunction_t cg_fn = nullptr;
     // Small batches: partial sums of the tile splits, reused by every call (no allocation per
     // call). Calls from different streams are ordered with an event, so they never share the
     // scratch at the same time.
@@ -777,6 +783,47 @@ void free_device(tree_ens *h) {
     (void)hipFree(h->d_scratch);
     if (h->scratch_done)
         (void)hipEventDestroy(h->scratch_done);
+    if (h->cg_module)
+        (void)hipModuleUnload(h->cg_module);
+}
+
+// Compile generated HIP source for gfx950 with hiprtc (host only: no device is needed).
+int compile_codegen(const std::string &src, std::vector<char> &code, std::string &err) {
+    hiprtcProgram prog;
+    hiprtcResult r = hiprtcCreateProgram(&prog, src.c_str(), "tree_ens_cg.hip", 0, nullptr, nullptr);
+    if (r != HIPRTC_SUCCESS) {
+        err = std::string("hiprtcCreateProgram: ") + hiprtcGetErrorString(r);
+        return TREE_ENS_E_DEVICE;
+    }
+    // the same code-generation settings as the library's own kernels
+    const char *opts[] = {"--offload-arch=gfx950", "-O3", "-fno-gpu-flush-denormals-to-zero",
+                          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"};
+    r = hiprtcCompileProgram(prog, int(sizeof opts / sizeof opts[0]), opts);
+    if (r != HIPRTC_SUCCESS) {
+        size_t n = 0;
+        std::string log;
+        if (hiprtcGetProgramLogSize(prog, &n) == HIPRTC_SUCCESS && n > 1) {
+            log.resize(n);
+            if (hiprtcGetProgramLog(prog, &log[0]) != HIPRTC_SUCCESS)
+                log.clear();
+        }
+        err = std::string("code generation: hiprtc failed (") + hiprtcGetErrorString(r) + ")" +
+              (log.empty() ? "" : ": " + log.substr(0, 2000));
+        (void)hiprtcDestroyProgram(&prog);
+        return TREE_ENS_E_DEVICE;
+    }
+    size_t size = 0;
+    r = hiprtcGetCodeSize(prog, &size);
+    if (r == HIPRTC_SUCCESS) {
+        code.resize(size);
+        r = hiprtcGetCode(prog, code.data());
+    }
+    (void)hiprtcDestroyProgram(&prog);
+    if (r != HIPRTC_SUCCESS) {
+        err = std::string("code generation: ") + hiprtcGetErrorString(r);
+        return TREE_ENS_E_DEVICE;
+    }
+    return TREE_ENS_OK;
 }
 
 template <typename T>
@@ -1057,6 +1104,9 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
     *out = nullptr;
     if (n_bags < 1)
         return fail(TREE_ENS_E_ARG, "n_bags must be >= 1");
+    const bool codegen = (flags & TREE_ENS_CODEGEN) != 0;
+    if (codegen && n_outputs != 1)
+        return fail(TREE_ENS_E_ARG, "code generation supports one value per leaf");
     Packed p;
     std::string err;
     int rc;
@@ -1068,6 +1118,21 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
     }
     if (rc != treeens::kOk)
         return fail(rc, err);
+    std::vector<char> cg_code;
+    if (codegen && n_trees > 0) {
+        std::string src;
+        try {
+            rc = treeens::codegen_source(n_trees, tree_offsets, feature, threshold, left, right, value,
+                                         flags, src, err);
+        } catch (const std::bad_alloc &) {
+            return fail(TREE_ENS_E_NOMEM, "host allocation failed while generating code");
+        }
+        if (rc != treeens::kOk)
+            return fail(rc, err);
+        rc = compile_codegen(src, cg_code, err);
+        if (rc != TREE_ENS_OK)
+            return fail(rc, err);
+    }
 
     tree_ens *h = new (std::nothrow) tree_ens();
     if (!h)
@@ -1105,6 +1170,11 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
         e = hipEventCreateWithFlags(&h->scratch_done, hipEventDisableTiming);
     if (e == hipSuccess && p.n_outputs > 1)
         e = upload(&h->d_leaf_vec, p.leaf_vec);
+    if (e == hipSuccess && !cg_code.empty()) {
+        e = hipModuleLoadData(&h->cg_module, cg_code.data());
+        if (e == hipSuccess)
+            e = hipModuleGetFunction(&h->cg_fn, h->cg_module, "tree_ens_cg");
+    }
     if (e == hipSuccess && p.plan.coded) {
         e = upload(&h->d_code_table, p.code_table);
         if (e == hipSuccess)
@@ -1143,6 +1213,22 @@ int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t 
     }
     if (h->n_outputs > 1)
         return launch_predict<kModeVector>(h, s, X, n_docs, n_features, scores, nullptr);
+    if (h->cg_fn) {
+        // the model's own kernel: one document per thread
+        const float *x = X;
+        long long n = n_docs;
+        int nf = n_features;
+        float *out = scores;
+        double scale = 1.0 / double(h->n_bags);
+        void *args[] = {&x, &n, &nf, &out, &scale};
+        const int64_t blocks = (n_docs + treeens::kCodegenThreads - 1) / treeens::kCodegenThreads;
+        if (blocks > 0x7fffffff)
+            return fail(TREE_ENS_E_ARG, "too many documents for one launch");
+        (void)hipGetLastError();
+        hipError_t e = hipModuleLaunchKernel(h->cg_fn, unsigned(blocks), 1, 1, treeens::kCodegenThreads,
+                                             1, 1, 0, s, args, nullptr);
+        return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "specialised kernel launch");
+    }
     return launch_predict<kModeScore>(h, s, X, n_docs, n_features, scores, nullptr);
 }
 
@@ -1213,6 +1299,33 @@ int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features, 
         *n_tiles = h->level_begin[1] - h->level_begin[0];
     if (docs_per_block)
         *docs_per_block = h->plan.docs_per_block;
+    return TREE_ENS_OK;
+}
+
+int tree_ens_codegen_source(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                            const float *threshold, const int32_t *left, const int32_t *right,
+                            const float *value, uint32_t flags, char *buf, int64_t buf_size,
+                            int64_t *src_len) {
+    g_err.clear();
+    if (buf_size < 0 || (buf_size > 0 && !buf))
+        return fail(TREE_ENS_E_ARG, "buf is NULL with a positive buf_size");
+    std::string src, err;
+    int rc;
+    try {
+        rc = treeens::codegen_source(n_trees, tree_offsets, feature, threshold, left, right, value,
+                                     flags | TREE_ENS_CODEGEN, src, err);
+    } catch (const std::bad_alloc &) {
+        return fail(TREE_ENS_E_NOMEM, "host allocation failed while generating code");
+    }
+    if (rc != treeens::kOk)
+        return fail(rc, err);
+    if (src_len)
+        *src_len = int64_t(src.size());
+    if (buf_size > 0) {
+        const size_t n = std::min(src.size(), size_t(buf_size - 1));
+        std::memcpy(buf, src.data(), n);
+        buf[n] = '\0';
+    }
     return TREE_ENS_OK;
 }
 
