@@ -11,8 +11,10 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   ns_per_doc   wall time per document
   latency_100doc_us   one 100-document batch: host wall clock of predict + stream sync
   rerank       per-query top-20 of the headline workload's query groups (Section 6's reranking)
-  roofline     the scoring kernel against the LDS roofline (node bytes)
+  roofline     the scoring kernel against the LDS byte roofline (node bytes: 8 per comparison
+               and 4 per leaf, over 256 B/clk/CU)
   roofline_hbm the same kernel against HBM (feature + score bytes)
+  roofline_lds_issue  the node bytes against the LDS instruction ceiling of the walk
   cpu_baseline the oracle on the host cores, same workload
   configs_extra the other workload sizes (1M-document ones included), same measurements
 """
@@ -32,13 +34,19 @@ sys.path.insert(0, ROOT)
 METRIC = "doc·tree evals/sec; ns/doc at 1k×32-leaf trees; µs per 100-doc batch"
 HEADLINE_CFG = 2
 
-# MI355X figures ("Rooflines"): 256 CUs at 2.4 GHz; LDS read width 256 B/clk/CU;
-# HBM3E 8 TB/s.
+# MI355X figures: 256 CUs at 2.4 GHz; LDS read width 256 B/clk/CU (a ds_read_b128 probe
+# reached 240); HBM3E 8 TB/s.
 N_CU = 256
 CLOCK_HZ = 2.4e9
 LDS_BYTES_PER_CLK_CU = 256
 LDS_PEAK_GBS = N_CU * CLOCK_HZ * LDS_BYTES_PER_CLK_CU / 1e9  # 157,286 GB/s
 HBM_PEAK_GBS = 8000.0
+# The LDS pipe's instruction ceiling for the walk: SQ_LDS_IDX_ACTIVE / SQ_INSTS_LDS of the
+# scoring kernel on the ranking workload is 2.2 busy cycles per wave-level LDS instruction, and
+# a comparison takes two (feature, node record), so at most 64 x 8 node bytes move per 4.4
+# cycles per CU whatever the byte width allows.
+LDS_CLK_PER_INSTR = 2.2
+LDS_ISSUE_NODE_GBS = N_CU * CLOCK_HZ * 64 * 8 / (2 * LDS_CLK_PER_INSTR) / 1e9  # 71,494 GB/s
 KERNEL_SRC = os.path.join(ROOT, "paper_1212_2287_amd", "csrc", "tree_ens.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
@@ -115,7 +123,10 @@ def roofline(kernel_s, lds_bytes, hbm_bytes, traffic):
              "unit": "GB/s", "frac": round(lds_bytes / kernel_s / 1e9 / LDS_PEAK_GBS, 4),
              "traffic": traffic},
             {"bound": "hbm", "achieved": round(hbm_bytes / kernel_s / 1e9, 1), "peak": HBM_PEAK_GBS,
-             "unit": "GB/s", "frac": round(hbm_bytes / kernel_s / 1e9 / HBM_PEAK_GBS, 4)})
+             "unit": "GB/s", "frac": round(hbm_bytes / kernel_s / 1e9 / HBM_PEAK_GBS, 4)},
+            {"bound": "lds_issue", "achieved": round(lds_bytes / kernel_s / 1e9, 1),
+             "peak": round(LDS_ISSUE_NODE_GBS, 1), "unit": "GB/s",
+             "frac": round(lds_bytes / kernel_s / 1e9 / LDS_ISSUE_NODE_GBS, 4)})
 
 
 def load_traffic(workload: str):
@@ -151,14 +162,15 @@ def measure_config(T, W, cfg_id, steps, warmup, n_docs=None, visits_sample=None)
     visits, sampled = count_visits(model, ens, Xd, visits_sample)
     lds_bytes = visits * 8 + doc_trees * 4
     hbm_bytes = cfg.n_docs * cfg.n_features * 4 + cfg.n_docs * 4 + model.info()["packed_bytes"]
-    rl, rl_hbm = roofline(kern_s, lds_bytes, hbm_bytes, load_traffic(cfg.name))
+    rl, rl_hbm, rl_issue = roofline(kern_s, lds_bytes, hbm_bytes, load_traffic(cfg.name))
     rec = {"workload": cfg.name, "n_trees": cfg.n_trees, "n_leaves": cfg.n_leaves,
            "n_features": cfg.n_features, "n_docs": cfg.n_docs,
            "value": doc_trees / wall_s, "ms_per_step": wall_s * 1e3, "kernel_ms": kern_s * 1e3,
            "ns_per_doc": wall_s * 1e9 / cfg.n_docs, "visits": int(visits), "visits_sampled": sampled,
-           "roofline": rl, "roofline_hbm": rl_hbm, "model": model.info()}
+           "roofline": rl, "roofline_hbm": rl_hbm, "roofline_lds_issue": rl_issue,
+           "model": model.info()}
     log(f"config {cfg_id}: {rec['ms_per_step']:.3f} ms/step, {rec['value']:.3e} doc*tree/s, "
-        f"LDS frac {rl['frac']:.3f}")
+        f"LDS frac {rl['frac']:.3f} (issue ceiling {rl_issue['frac']:.3f})")
     return rec, model, ens, Xd, out
 
 
@@ -405,6 +417,7 @@ def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) 
     w_factor = copy_bytes / 1024.0 / w_copy
     read_b = f_score * 1024.0 * f_factor
     write_b = w_score * 1024.0 * w_factor
+    fetch_dir, write_dir = os.path.dirname(fetch_csv), os.path.dirname(write_csv)
     rec = {
         "kernel_hash": kernel_hash(),
         "note": (f"HBM bytes per launch of the scoring kernel on {cfg.name} ({cfg.n_docs} docs), mean "
@@ -412,10 +425,9 @@ def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) 
                  f"its reading on a plain device copy of {copy_bytes} bytes (FETCH_SIZE {f_copy:.1f} "
                  f"KiB, WRITE_SIZE {w_copy:.1f} KiB for {copy_bytes / 1024:.1f} KiB moved)."),
         "commands": [
-            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o fetch -- python -u bench.py --pmc-probe",
-            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o write -- python -u bench.py --pmc-probe",
-            "python bench.py --write-traffic gpurun_out/pmc_fetch/fetch_counter_collection.csv "
-            "gpurun_out/pmc_write/write_counter_collection.csv",
+            f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o fetch -- python -u bench.py --pmc-probe",
+            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o write -- python -u bench.py --pmc-probe",
+            f"python bench.py --write-traffic {fetch_csv} {write_csv}",
         ],
         "calibration": {"fetch_factor": f_factor, "write_factor": w_factor},
         "workloads": {cfg.name: {
@@ -524,6 +536,7 @@ def main() -> int:
         "latency_100doc_us": lat, "rerank": rr, "feature_usage": fu,
         "multi_output": mo, "codegen": cg, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
+        "roofline_lds_issue": rec["roofline_lds_issue"],
         "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
     }
     print(json.dumps(line), flush=True)
