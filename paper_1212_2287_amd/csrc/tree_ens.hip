@@ -58,6 +58,7 @@ int hip_fail(hipError_t e, const char *what) {
 }
 
 constexpr int kNumCus = 256;
+constexpr int kXcds = 8; // accelerator complex dies, each with its own L2
 // s_waitcnt immediate for gfx9: vmcnt(0), expcnt and lgkmcnt left at their maxima (no wait)
 constexpr int kWaitVmcnt0 = 0x0F70;
 #ifndef TREE_ENS_PREFETCH_DEPTH
@@ -182,12 +183,24 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // remaining block is split over tail_splits workgroups that walk a contiguous share of the
     // tiles each and leave fp64 partial sums (the tail fills what would be a last, mostly idle
     // round of workgroups; small batches have no head at all).
+    // After a head of whole rounds (a multiple of the XCD count), the splits of one tail block
+    // are given workgroup indices of one residue mod kXcds: workgroups are dealt to the XCDs in
+    // index order, so all splits of a block share one XCD's L2 and its document rows come from
+    // HBM once. Indices past the last block (padding to whole XCD columns) exit at once.
     int64_t block = blockIdx.x;
     int split = 0, n_splits = 1;
     if (block >= head_blocks) {
         const int64_t t = block - head_blocks;
-        block = head_blocks + t / tail_splits;
-        split = int(t % tail_splits);
+        if (head_blocks > 0) {
+            const int64_t x = t % kXcds, r = t / kXcds;
+            block = head_blocks + (r / tail_splits) * kXcds + x;
+            split = int(r % tail_splits);
+            if (block * DL >= n_docs)
+                return;
+        } else {
+            block = head_blocks + t / tail_splits;
+            split = int(t % tail_splits);
+        }
         n_splits = tail_splits;
     }
     const int64_t doc0 = block * DL;
@@ -980,7 +993,10 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     }
     const int level = shape.level, splits = shape.splits;
     const int64_t tail_docs = n_docs - shape.head * dl;
-    const int64_t n_wgs = shape.head + (n_blocks - shape.head) * splits;
+    // tail blocks after a head are laid out in whole XCD columns (see the kernel)
+    const int64_t tail_blocks = n_blocks - shape.head;
+    const int64_t tail_slots = shape.head > 0 ? (tail_blocks + kXcds - 1) / kXcds * kXcds : tail_blocks;
+    const int64_t n_wgs = shape.head + tail_slots * splits;
     if (n_wgs > 0x7fffffff)
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     ScoreFn fn = pick_kernel<MODE>(h->plan);
