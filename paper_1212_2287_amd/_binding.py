@@ -341,8 +341,11 @@ def tree_ens_destroy(h) -> None:
 class TreeEnsemble:
     """Owner of a packed model on the current device.
 
-    ``TreeEnsemble.from_arrays(tree_offsets, feature, threshold, left, right, value, flags)``
-    or ``TreeEnsemble.from_ensemble(ens)`` for any object with those attributes."""
+    ``TreeEnsemble.from_arrays(tree_offsets, feature, threshold, left, right, value, flags,
+    n_outputs, n_bags)`` or ``TreeEnsemble.from_ensemble(ens, flags, leaf_values, n_bags)`` for
+    any object with those attributes; ``TreeEnsemble(handle)`` adopts a handle from the
+    module-level create functions. ``n_outputs`` and ``n_bags`` are read back from the handle;
+    ``flags`` may include ``TREE_ENS_CODEGEN``."""
 
     def __init__(self, handle):
         self._h = handle
