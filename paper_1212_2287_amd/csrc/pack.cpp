@@ -424,6 +424,13 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
 
+    if (plan.lds_bytes == kLdsPerCu / 2) {
+        const int64_t off = (int64_t(plan.xs_bytes) + int64_t(p.level_slot_recs[0]) * 8 + 15) & ~int64_t(15);
+        const int64_t mask_bytes = (int64_t(n_cols) + 31) / 32 * plan.docs_per_block * 4;
+        if (off + mask_bytes <= plan.zero_rec)
+            p.usage_slot_off = int32_t(off);
+    }
+
     // The one-workgroup-per-CU kernels copy whole windows of 1,024-record chunks: pad the images
     // so that the window of the last tile stays inside the buffer.
     p.images.resize(p.images.size() + size_t(kPrefetchFull / 2) * 1024, NodeRec{0u, 0u});

@@ -133,6 +133,9 @@ struct Packed {
     // and of all tiles of tiling 0: the launch planner's unit of time
     int32_t level_max_rounds[kTileLevels] = {};
     int64_t total_rounds = 0;
+    // feature trace of a two-workgroup plan: LDS byte address of the bitmasks in the tile slot
+    // past the largest tiling-0 image, or -1 when they do not fit before the zero record
+    int32_t usage_slot_off = -1;
     // vector-valued leaves (n_outputs > 1): a leaf's threshold slot holds 2 + its packed node
     // index instead of a value, and row (thr - 1) of leaf_vec holds its n_outputs values,
     // padded to vec_stride (a multiple of 4) floats; row 0 is zero (the all-zero record's row)

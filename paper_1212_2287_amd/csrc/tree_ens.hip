@@ -69,6 +69,7 @@ constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves
 constexpr int kModeScore = 0;  // scores
 constexpr int kModeLeaves = 1; // leaf ids
 constexpr int kModeUsage = 2;  // per-document feature bitmasks and their popcounts
+constexpr int kModeUsageSlot = 4; // the same with the bitmasks in the unused end of the tile slot
 constexpr int kModeVector = 3; // four components of vector-valued scores
 constexpr int kVecPerLaunch = 4;
 
@@ -145,13 +146,15 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     //                            after the last tile, the cross-walker reduction (1,024 doubles,
     //                            4 x 1,024 with vector-valued leaves)
     //   zero_rec (8 bytes)       all-zero self-linked leaf of value 0, for idle walker slots
-    //   usage_off                usage mode: word j of document lane dl's feature bitmask at
-    //                            [j * DL + dl] (32 feature ids a word); past the 80 KB half of
-    //                            two-workgroup plans, so usage launches hold a CU alone
+    //   usage_off                usage modes: word j of document lane dl's feature bitmask at
+    //                            [j * DL + dl] (32 feature ids a word); in the slot past the
+    //                            largest tile image when it fits there (kModeUsageSlot, two
+    //                            workgroups per CU as for scoring), else past the 80 KB half of
+    //                            two-workgroup plans (kModeUsage: the launch holds a CU alone)
     constexpr bool LEAVES = MODE == kModeLeaves;
-    constexpr bool USAGE = MODE == kModeUsage;
+    constexpr bool USAGE = MODE == kModeUsage || MODE == kModeUsageSlot;
     constexpr bool VEC = MODE == kModeVector;
-    constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 + (USAGE ? treeens::kUsageHalfBytes : 0)
+    constexpr int kLds = HALF ? treeens::kLdsPerCu / 2 + (MODE == kModeUsage ? treeens::kUsageHalfBytes : 0)
                               : treeens::kLdsPerCu;
     __shared__ __align__(16) unsigned char lds[kLds];
     constexpr int kPre = HALF ? treeens::kPrefetchHalf : treeens::kPrefetchFull; // records per thread
@@ -698,6 +701,9 @@ ScoreFn pick_dl(const treeens::LdsPlan &p) {
         else
             return p.docs_per_block == 64 ? pick_k<64, true, NARROW, false, MODE>(p.interleave) : nullptr;
     }
+    if constexpr (MODE == kModeUsageSlot)
+        return nullptr; // one-workgroup plans keep room for the bitmasks after the zero record
+    else
     switch (p.docs_per_block) {
     case 64: return pick_k<64, false, NARROW, CODED, MODE>(p.interleave);
     case 32: return pick_k<32, false, NARROW, CODED, MODE>(p.interleave);
@@ -739,6 +745,7 @@ struct tree_ens {
     int32_t level_begin[treeens::kTileLevels + 1] = {};
     int32_t level_max_rounds[treeens::kTileLevels] = {}; // walker rounds of the fullest tile
     int64_t total_rounds = 0;                            // walker rounds of all tiles, tiling 0
+    int32_t usage_slot_off = -1; // feature-trace bitmasks in the tile slot (two-workgroup plans)
     int64_t level_image_off[treeens::kTileLevels] = {};
     int32_t level_slot_recs[treeens::kTileLevels] = {};
     uint2 *d_images = nullptr;      // tile images of every tiling
@@ -971,14 +978,22 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     if (n_blocks > 0x7fffffff)
         return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     LaunchShape shape;
-    if (MODE == kModeUsage) {
+    int32_t usage_off = h->plan.usage_off;
+    if (MODE == kModeUsage || MODE == kModeUsageSlot) {
         // one workgroup walks every tile of its block: its bitmasks are complete in LDS
         shape = LaunchShape{0, n_blocks, 1};
-        const int64_t lds_end = h->plan.lds_bytes == treeens::kLdsPerCu
-                                    ? treeens::kLdsPerCu
-                                    : treeens::kLdsPerCu / 2 + treeens::kUsageHalfBytes;
-        if (h->plan.usage_off + int64_t((h->n_cols + 31) / 32) * dl * 4 > lds_end)
-            return fail(TREE_ENS_E_ARG, "feature bitmasks do not fit the LDS plan");
+        const int64_t mask_bytes = int64_t((h->n_cols + 31) / 32) * dl * 4;
+        if (MODE == kModeUsageSlot) {
+            usage_off = h->usage_slot_off;
+            if (usage_off < 0 || usage_off + mask_bytes > h->plan.zero_rec)
+                return fail(TREE_ENS_E_ARG, "feature bitmasks do not fit the tile slot");
+        } else {
+            const int64_t lds_end = h->plan.lds_bytes == treeens::kLdsPerCu
+                                        ? treeens::kLdsPerCu
+                                        : treeens::kLdsPerCu / 2 + treeens::kUsageHalfBytes;
+            if (usage_off + mask_bytes > lds_end)
+                return fail(TREE_ENS_E_ARG, "feature bitmasks do not fit the LDS plan");
+        }
     } else {
         std::lock_guard<std::mutex> lock(h->shape_mu);
         if (h->shape_blocks == n_blocks) {
@@ -1060,7 +1075,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                            row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs,
                            n_tiles, int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec,
                            partials, scores, leaf_ids, h->d_orig_id, h->d_tree_node_off,
-                           h->d_tree_orig, h->n_trees, masks, mask_words, h->plan.usage_off,
+                           h->d_tree_orig, h->n_trees, masks, mask_words, usage_off,
                            reinterpret_cast<const float4 *>(h->d_leaf_vec), h->vec_stride / 4, n_out,
                            chunk, scale);
         e = hipGetLastError();
@@ -1166,6 +1181,7 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
     std::memcpy(h->level_image_off, p.level_image_off, sizeof h->level_image_off);
     std::memcpy(h->level_max_rounds, p.level_max_rounds, sizeof h->level_max_rounds);
     h->total_rounds = p.total_rounds;
+    h->usage_slot_off = p.usage_slot_off;
     std::memcpy(h->level_slot_recs, p.level_slot_recs, sizeof h->level_slot_recs);
     std::vector<uint2> images(p.images.size());
     if (!p.images.empty())
@@ -1295,6 +1311,10 @@ int tree_ens_feature_usage(const tree_ens_t *h, void *stream, const float *X, in
         hipError_t e = hipGetLastError();
         return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "kernel launch");
     }
+    // two-workgroup plans whose level-0 tiles leave room in the slot keep two workgroups per CU
+    if (h->usage_slot_off >= 0)
+        return launch_predict<kModeUsageSlot>(h, s, X, n_docs, n_features, nullptr, counts, masks,
+                                              words);
     return launch_predict<kModeUsage>(h, s, X, n_docs, n_features, nullptr, counts, masks, words);
 }
 

@@ -116,6 +116,18 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                                     : treeens::kLdsPerCu / 2 + treeens::kUsageHalfBytes;
         if (pl.usage_off % 16 || pl.usage_off < int64_t(zero) + 8 || usage_end > lds_end)
             return bad("feature bitmask region overlaps the tile or exceeds the LDS");
+        // the in-slot placement of two-workgroup plans: past every tiling-0 image, before the
+        // zero record
+        if (p.usage_slot_off >= 0) {
+            const int64_t mask_bytes = int64_t(p.n_cols + 31) / 32 * DL * 4;
+            if (pl.lds_bytes != treeens::kLdsPerCu / 2 || p.usage_slot_off % 16 ||
+                p.usage_slot_off < int64_t(xs) + int64_t(p.level_slot_recs[0]) * 8 ||
+                p.usage_slot_off + mask_bytes > int64_t(zero))
+                return bad("in-slot feature bitmasks overlap a tile image or the zero record");
+            for (int32_t t = p.level_begin[0]; t < p.level_begin[1]; t++)
+                if (int64_t(xs) + int64_t(p.tile_recs[size_t(t)]) * 8 > p.usage_slot_off)
+                    return bad("a tiling-0 image reaches the in-slot feature bitmasks");
+        }
     }
     std::vector<uint8_t> lds(size_t(pl.lds_bytes), 0);
     auto rec_at = [&](uint32_t a) {
