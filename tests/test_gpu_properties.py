@@ -1,5 +1,6 @@
 """Property tests (hypothesis) of the HIP path through the C ABI: random small ensembles and
-documents against the oracle, and invariants of the mathematics checked on the GPU alone —
+documents against the oracle (scores and leaves, vector-valued leaves with bags, the feature
+trace), and invariants of the mathematics checked on the GPU alone —
 doubling leaf values doubles every score exactly, permuting documents permutes the scores bit
 for bit, renumbering nodes maps the leaf ids and keeps the scores bit for bit, reordering trees
 keeps the scores within the tolerance."""
@@ -105,3 +106,32 @@ def test_invariants_on_the_gpu(T, c):
     sr, ir = _run(T, rev, X, rule)
     assert_scores_close(sr, s.astype(np.float64), "reversed trees")
     assert np.array_equal(ir[:, ::-1], ids)
+
+
+@SETTINGS
+@given(c=cases, n_out=st.integers(2, 9), n_bags=st.integers(1, 4))
+def test_vector_leaves_and_bags_match_the_oracle(T, c, n_out, n_bags):
+    import torch
+    ens, X = _make(c)
+    vals = W.make_leaf_vectors(ens, n_out, ("dense", "class", "probs")[c["seed"] % 3], seed=c["seed"])
+    flags = T.TREE_ENS_RIGHT_IF_GT if c["rule"] else T.TREE_ENS_RIGHT_IF_GE
+    with T.TreeEnsemble.from_ensemble(ens, flags, leaf_values=vals, n_bags=n_bags) as m:
+        s = m.predict(dev(X))
+        torch.cuda.synchronize()
+        s = s.cpu().numpy().astype(np.float64)
+    ref = oracle.score_multi(ens, vals, X, n_bags=n_bags, rule=c["rule"])
+    assert_scores_close(s.ravel(), ref.ravel(), str(c))
+
+
+@SETTINGS
+@given(c=cases)
+def test_feature_trace_matches_the_oracle(T, c):
+    import torch
+    ens, X = _make(c)
+    flags = T.TREE_ENS_RIGHT_IF_GT if c["rule"] else T.TREE_ENS_RIGHT_IF_GE
+    with T.TreeEnsemble.from_ensemble(ens, flags) as m:
+        cnt, masks = m.feature_usage(dev(X))
+        torch.cuda.synchronize()
+        cnt, masks = cnt.cpu().numpy(), masks.cpu().numpy().view(np.uint32)
+    ref_c, ref_m = oracle.feature_usage(ens, X, rule=c["rule"])
+    assert np.array_equal(cnt, ref_c) and np.array_equal(masks, ref_m), str(c)
