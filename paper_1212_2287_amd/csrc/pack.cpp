@@ -241,7 +241,70 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
 
-    // ---- pass 2: order trees by depth (deepest first), re-lay each out breadth-first --------
+    // ---- tree order: expected lockstep length ----------------------------------------------
+    // A wave steps through a tree until the longest of its 64 documents' paths ends, so the trees
+    // walked side by side (a group of K, the walkers of one round) should end together. With no
+    // documents at hand, a split's chance of sending a document right is estimated from the
+    // model's own thresholds on that feature (the share of them below this one: thresholds are
+    // cut where the training data lies, so their spread follows the feature's); a tree's
+    // leaf-depth distribution follows, and its key is the expected longest of 64 independent
+    // paths. Complete trees (every path equally long) get exactly their depth, and come before
+    // any other tree of an equal key, so that they still form complete-depth tiles. The order
+    // changes only the rounding of the sums.
+    std::vector<double> lock_key(size_t(n_trees), 0.0);
+    std::vector<uint8_t> complete_tree(size_t(n_trees), 0);
+    {
+        std::vector<std::vector<float>> thr_sorted(static_cast<size_t>(n_cols));
+        for (int64_t i = 0; i < n_nodes; i++) {
+            const float v = feature[i] >= 0 ? canon(threshold[i]) : 0.0f;
+            if (feature[i] >= 0 && !std::isnan(v)) // NaN: a strict +inf split, never right
+                thr_sorted[size_t(feature[i])].push_back(v);
+        }
+        for (auto &v : thr_sorted)
+            std::sort(v.begin(), v.end());
+        std::vector<double> reach, at_depth;
+        for (int32_t t = 0; t < n_trees; t++) {
+            const int64_t a = tree_offsets[t];
+            const int64_t n = tree_offsets[t + 1] - a;
+            complete_tree[size_t(t)] = n == (int64_t(2) << depth_of[size_t(t)]) - 1;
+            reach.assign(size_t(n), 0.0);
+            level.assign(size_t(n), 0);
+            at_depth.assign(size_t(depth_of[size_t(t)]) + 1, 0.0);
+            reach[0] = 1.0;
+            order.clear();
+            order.push_back(0);
+            for (size_t q = 0; q < order.size(); q++) {
+                const int32_t i = order[q];
+                if (feature[a + i] < 0) {
+                    at_depth[size_t(level[size_t(i)])] += reach[size_t(i)];
+                    continue;
+                }
+                const auto &ts = thr_sorted[size_t(feature[a + i])];
+                const float v = canon(threshold[a + i]);
+                const size_t below = size_t(std::lower_bound(ts.begin(), ts.end(), v) - ts.begin());
+                const double p_right = std::isnan(v) ? 0.0 : 1.0 - double(below) / double(ts.size());
+                const int32_t l = left[a + i], r = right[a + i];
+                reach[size_t(r)] = reach[size_t(i)] * p_right;
+                reach[size_t(l)] = reach[size_t(i)] * (1.0 - p_right);
+                level[size_t(l)] = level[size_t(r)] = level[size_t(i)] + 1;
+                order.push_back(l);
+                order.push_back(r);
+            }
+            // E[max of 64 paths] = sum over d of P(some path is longer than d)
+            double cdf = 0.0, key = 0.0;
+            for (int32_t d = 0; d < depth_of[size_t(t)]; d++) {
+                cdf = std::min(cdf + at_depth[size_t(d)], 1.0);
+                double c = cdf;
+                for (int k = 0; k < 6; k++)
+                    c *= c; // cdf^64
+                key += 1.0 - c;
+            }
+            lock_key[size_t(t)] = complete_tree[size_t(t)] ? double(depth_of[size_t(t)]) : key;
+        }
+    }
+
+    // ---- pass 2: order trees by expected lockstep length (longest first), re-lay each out
+    // breadth-first ------------------------------------------------------------------------------
     Packed p;
     p.n_trees = n_trees;
     p.n_cols = n_cols;
@@ -253,8 +316,13 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     }
     p.tree_orig.resize(size_t(n_trees));
     std::iota(p.tree_orig.begin(), p.tree_orig.end(), 0);
-    std::stable_sort(p.tree_orig.begin(), p.tree_orig.end(),
-                     [&](int32_t x, int32_t y) { return depth_of[size_t(x)] > depth_of[size_t(y)]; });
+    std::stable_sort(p.tree_orig.begin(), p.tree_orig.end(), [&](int32_t x, int32_t y) {
+        if (lock_key[size_t(x)] != lock_key[size_t(y)])
+            return lock_key[size_t(x)] > lock_key[size_t(y)];
+        if (complete_tree[size_t(x)] != complete_tree[size_t(y)])
+            return complete_tree[size_t(x)] > complete_tree[size_t(y)];
+        return depth_of[size_t(x)] > depth_of[size_t(y)];
+    });
     p.nodes.reserve(size_t(n_nodes));
     p.orig_id.reserve(size_t(n_nodes));
     p.tree_node_off.resize(size_t(n_trees) + 1, 0);

@@ -286,4 +286,26 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
     return 0;
 }
 
+// The packer's tree order (order[i] = input index of the i-th packed tree) and, per tile of
+// tiling 0, its complete depth (-1: not all trees complete of one depth). Returns the number
+// of tiles (at most max_tiles are written), or a negative packer status.
+int emu_tree_order(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                   const float *threshold, const int32_t *left, const int32_t *right, const float *value,
+                   uint32_t flags, int32_t *order, int32_t *tile_complete, int32_t max_tiles) {
+    treeens::Packed p;
+    std::string err;
+    const int rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value, 1,
+                                       flags, p, err);
+    if (rc != treeens::kOk) {
+        g_msg = err;
+        return rc;
+    }
+    for (int32_t t = 0; t < n_trees; t++)
+        order[t] = p.tree_orig[size_t(t)];
+    const int32_t n_tiles = p.level_begin[1] - p.level_begin[0];
+    for (int32_t i = 0; i < n_tiles && i < max_tiles; i++)
+        tile_complete[i] = p.tiles[size_t(p.level_begin[0] + i)].complete_depth;
+    return n_tiles;
+}
+
 } // extern "C"

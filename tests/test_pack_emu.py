@@ -32,6 +32,8 @@ def emu(tmp_path_factory):
     lib.emu_walk.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_uint32, P,
                              ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
     lib.emu_message.restype = ctypes.c_char_p
+    lib.emu_tree_order.restype = ctypes.c_int
+    lib.emu_tree_order.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_uint32, P, P, ctypes.c_int32]
     return lib
 
 
@@ -136,3 +138,95 @@ def test_coded_documents_with_corner_values(emu):
     X[5, ::3] = np.float32(3.4e38)
     plan = _check(emu, ens, X, levels=(0,))
     assert plan[3] == 1, plan
+
+
+def _order(lib, ens, flags=0):
+    arrs = [np.ascontiguousarray(ens.tree_offsets, np.int64), np.ascontiguousarray(ens.feature, np.int32),
+            np.ascontiguousarray(ens.threshold, np.float32), np.ascontiguousarray(ens.left, np.int32),
+            np.ascontiguousarray(ens.right, np.int32), np.ascontiguousarray(ens.value, np.float32)]
+    order = np.empty(ens.n_trees, np.int32)
+    tiles = np.empty(4096, np.int32)
+    n = lib.emu_tree_order(ens.n_trees, *[a.ctypes.data for a in arrs], flags, order.ctypes.data,
+                           tiles.ctypes.data, tiles.size)
+    assert n >= 0, lib.emu_message().decode()
+    assert np.array_equal(np.sort(order), np.arange(ens.n_trees))
+    return order, tiles[:min(n, tiles.size)]
+
+
+def _stack(trees, n_features):
+    offs = np.cumsum([0] + [len(t[0]) for t in trees]).astype(np.int64)
+    cat = [np.concatenate([np.asarray(t[k], dt) for t in trees]) for k, dt in
+           enumerate((np.int32, np.float32, np.int32, np.int32, np.float32))]
+    return W.Ensemble(offs, *cat, n_features)
+
+
+def test_tree_order_known_answer(emu):
+    """Trees are ordered by the expected longest of 64 paths, each split's chance of going right
+    estimated by the share of the model's thresholds on its feature below its own. A complete
+    tree's key is its depth; a deep chain whose root threshold is the lowest of its feature
+    sends every document right to a leaf at depth 1 (key 1); complete trees come first among
+    equal keys. Depth-first ordering would put the chain first."""
+    complete2 = ([0, 0, 0, -1, -1, -1, -1], [0.5, 0.25, 0.75, 0, 0, 0, 0], [1, 3, 5, -1, -1, -1, -1],
+                 [2, 4, 6, -1, -1, -1, -1], [0, 0, 0, 1, 2, 3, 4])
+    # root (lowest threshold) -> right leaf 2; left: a chain 1 -> 3 -> 5 of depth 4
+    chain = ([0, 0, -1, 0, -1, 0, -1, -1, -1], [-1.0, 0.1, 0, 0.2, 0, 0.3, 0, 0, 0],
+             [1, 3, -1, 5, -1, 7, -1, -1, -1], [2, 4, -1, 6, -1, 8, -1, -1, -1], [0] * 9)
+    stump = ([0, -1, -1], [0.6, 0, 0], [1, -1, -1], [2, -1, -1], [0, 5, 6])
+    ens = _stack([chain, stump, complete2], 1)
+    for flags in (0, 1):
+        order, _ = _order(emu, ens, flags)
+        assert order.tolist() == [2, 1, 0], (flags, order)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_tree_order_ignores_node_numbering(emu, seed):
+    """The order depends on the trees, not on how their nodes are numbered (special thresholds,
+    +inf under the strict rule included)."""
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf], dtype=np.float32)
+    ens = W.random_ensemble(seed, n_trees=60, n_features=1 + seed, min_leaves=1, max_leaves=24,
+                            thr_values=pool if seed % 2 == 0 else None)
+    ren, _ = W.relabel_nodes(ens, seed)
+    for flags in (0, 1):
+        assert np.array_equal(_order(emu, ens, flags)[0], _order(emu, ren, flags)[0]), flags
+
+
+def test_tree_order_keeps_complete_trees_together(emu):
+    """Complete trees of one depth stay contiguous in a mixed model, and a model of complete trees
+    is cut into complete-depth tiles only."""
+    rand = W.make_ensemble(W.CONFIGS[2], n_trees=300)
+    comp = W.make_ensemble(W.CONFIGS[4], n_trees=500)
+    trees = []
+    for i in range(800):
+        e, t = (comp, i // 2) if i % 8 < 5 and i // 2 < 500 else (rand, i % 300)
+        trees.append(e.tree(t))
+    ens = _stack(trees, 136)
+    order, tiles = _order(emu, ens)
+    is_complete = np.array([len(trees[t][0]) == 15 for t in order])
+    pos = np.nonzero(is_complete)[0]
+    assert pos.size > 0 and pos[-1] - pos[0] + 1 == pos.size
+    _, tiles = _order(emu, comp)
+    assert tiles.size > 1 and (tiles == 3).all()
+
+
+def test_tree_order_shortens_the_lockstep_walk(emu):
+    """On the ranking-shaped model, groups of 4 trees taken in the packed order need fewer
+    lockstep steps (per 64-document wave, the longest path of any tree in the group) than in the
+    input order: the estimate tracks the real path lengths."""
+    cfg = W.CONFIGS[2]
+    ens = W.make_ensemble(cfg)
+    X = W.make_docs(cfg, n_docs=64 * 16)
+    _, leaves, _ = oracle.score(ens, X)
+    depth = np.zeros(ens.feature.shape[0], np.int64)
+    for t in range(ens.n_trees):
+        a = int(ens.tree_offsets[t])
+        for q in range(int(ens.tree_offsets[t + 1]) - a):  # creation order: parents first
+            if ens.feature[a + q] >= 0:
+                depth[a + ens.left[a + q]] = depth[a + ens.right[a + q]] = depth[a + q] + 1
+    paths = depth[ens.tree_offsets[:-1][None, :] + leaves]
+    wave_max = paths.reshape(-1, 64, ens.n_trees).max(axis=1)
+
+    def steps(order):
+        return wave_max[:, order].reshape(wave_max.shape[0], -1, 4).max(axis=2).sum()
+
+    order, _ = _order(emu, ens)
+    assert steps(order) < 0.9 * steps(np.arange(ens.n_trees))
