@@ -3,8 +3,8 @@
 // Turns the caller's flat creation-order arrays into the device layout the kernels walk:
 // one 8-byte record per node, trees re-laid out breadth-first with the two children of a node
 // in adjacent slots (the contiguous Struct+ layout of Section 3, which keeps explicit child
-// links so unbalanced trees pack without empty slots), trees ordered by depth, and a plan of
-// LDS tiles (runs of whole trees that fit the per-workgroup LDS budget).
+// links so unbalanced trees pack without empty slots), trees ordered by their expected lockstep
+// length, and a plan of LDS tiles (runs of whole trees that fit the per-workgroup LDS budget).
 #pragma once
 
 #include <cstdint>
