@@ -408,13 +408,13 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                             internal |= fa[i] >= kLeafCol;
                         return __builtin_amdgcn_ballot_w64(internal) != 0;
                     };
+                    // The first step is taken untested: a group whose K roots are all leaves
+                    // (single-leaf trees, idle slots) is rare, and a leaf absorbs the extra step.
                     read_features();
-                    if (any_internal()) {
-                        do {
-                            descend();
-                            read_features();
-                        } while (any_internal());
-                    }
+                    do {
+                        descend();
+                        read_features();
+                    } while (any_internal());
                     // The exit path "uses" the last feature reads, so the compiler cannot sink
                     // them below the test (where they would serialise with it again).
 #pragma unroll
