@@ -16,7 +16,7 @@ Prints ONE JSON line on stdout (progress goes to stderr):
   roofline_hbm the same kernel against HBM (feature + score bytes)
   roofline_lds_issue  the node bytes against the LDS instruction ceiling of the walk
   cpu_baseline the oracle on the host cores, same workload
-  configs_extra the other workload sizes (1M-document ones included), same measurements
+  workloads_extra the other workloads (1M-document ones included), same measurements
 """
 from __future__ import annotations
 
@@ -32,7 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "doc·tree evals/sec; ns/doc at 1k×32-leaf trees; µs per 100-doc batch"
-HEADLINE_CFG = 2
+HEADLINE = "rank_1kx32"
 
 # MI355X figures: 256 CUs at 2.4 GHz; LDS read width 256 B/clk/CU (a ds_read_b128 probe
 # reached 240); HBM3E 8 TB/s.
@@ -143,15 +143,15 @@ def load_traffic(workload: str):
     return ent.get("hbm_bytes_per_launch")
 
 
-def measure_config(T, W, cfg_id, steps, warmup, n_docs=None, visits_sample=None):
+def measure_workload(T, W, wl, steps, warmup, n_docs=None, visits_sample=None):
     import torch
-    cfg = W.CONFIGS[cfg_id]
+    cfg = W.WORKLOADS[wl]
     if n_docs is not None:
         cfg = W.scaled(cfg, n_docs=n_docs)
     t0 = time.perf_counter()
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
-    log(f"config {cfg_id} ({cfg.name}): generated {cfg.n_trees} trees, {cfg.n_docs} docs in "
+    log(f"{wl}: generated {cfg.n_trees} trees, {cfg.n_docs} docs in "
         f"{time.perf_counter() - t0:.1f}s")
     model = T.TreeEnsemble.from_ensemble(ens)
     Xd = torch.from_numpy(X).to("cuda")
@@ -169,7 +169,7 @@ def measure_config(T, W, cfg_id, steps, warmup, n_docs=None, visits_sample=None)
            "ns_per_doc": wall_s * 1e9 / cfg.n_docs, "visits": int(visits), "visits_sampled": sampled,
            "roofline": rl, "roofline_hbm": rl_hbm, "roofline_lds_issue": rl_issue,
            "model": model.info()}
-    log(f"config {cfg_id}: {rec['ms_per_step']:.3f} ms/step, {rec['value']:.3e} doc*tree/s, "
+    log(f"{wl}: {rec['ms_per_step']:.3f} ms/step, {rec['value']:.3e} doc*tree/s, "
         f"LDS frac {rl['frac']:.3f} (issue ceiling {rl_issue['frac']:.3f})")
     return rec, model, ens, Xd, out
 
@@ -308,9 +308,10 @@ def codegen(T, W, reps=10):
     shallow workloads (compile time included in the record)."""
     import torch
     out = {}
-    for name, cfg_id, n_trees, n_docs in (("tiny_10x8", 1, None, None), ("rank_1kx32_200trees", 2, 200, None),
-                                          ("shallow_20kx8_1000trees", 4, 1000, None)):
-        cfg = W.CONFIGS[cfg_id]
+    for name, wl, n_trees, n_docs in (("tiny_10x8", "tiny_10x8", None, None),
+                                      ("rank_1kx32_200trees", "rank_1kx32", 200, None),
+                                      ("shallow_20kx8_1000trees", "shallow_20kx8_1M", 1000, None)):
+        cfg = W.WORKLOADS[wl]
         ens = W.make_ensemble(cfg, n_trees=n_trees)
         Xd = torch.from_numpy(W.make_docs(cfg, n_docs=n_docs)).to("cuda")
         rec = {"trees": ens.n_trees, "nodes": ens.n_nodes, "docs": int(Xd.shape[0])}
@@ -339,10 +340,10 @@ def codegen(T, W, reps=10):
     return out
 
 
-def cpu_baseline(W, cfg_id, budget_s=10.0):
+def cpu_baseline(W, wl, budget_s=10.0):
     import numpy as np
     import oracle
-    cfg = W.CONFIGS[cfg_id]
+    cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
     threads = min(16, len(os.sched_getaffinity(0)))
@@ -370,7 +371,7 @@ def pmc_probe(T, W) -> int:
     """Copy the feature matrix once (reads and writes exactly its bytes: the calibration for the
     FETCH_SIZE / WRITE_SIZE counters), then score it three times."""
     import torch
-    cfg = W.CONFIGS[HEADLINE_CFG]
+    cfg = W.WORKLOADS[HEADLINE]
     ens = W.make_ensemble(cfg)
     Xd = torch.from_numpy(W.make_docs(cfg)).to("cuda")
     copy = torch.empty_like(Xd)
@@ -393,7 +394,7 @@ def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) 
     and writes exactly that many bytes). Runs on the host; writes profiles/hbm_traffic.json."""
     import csv
     import workloads as W
-    cfg = W.CONFIGS[HEADLINE_CFG]
+    cfg = W.WORKLOADS[HEADLINE]
     copy_bytes = cfg.n_docs * cfg.n_features * 4
 
     def per_kernel(path, counter):
@@ -487,16 +488,16 @@ def main() -> int:
 
     if args.pmc_probe:
         return pmc_probe(T, W)
-    rec, model, ens, Xd, out = measure_config(T, W, HEADLINE_CFG, args.steps, args.warmup)
+    rec, model, ens, Xd, out = measure_workload(T, W, HEADLINE, args.steps, args.warmup)
     lat = latency_100(model, Xd)
     log(f"100-doc batch: median {lat['median_us']:.1f} us, device {lat['device_us_per_call']:.1f} us/call")
-    rr = rerank(T, W, model, Xd, W.CONFIGS[HEADLINE_CFG])
+    rr = rerank(T, W, model, Xd, W.WORKLOADS[HEADLINE])
     log(f"rerank top-{rr['k']} of {rr['queries']} queries: top-k kernel {rr['topk_us']:.1f} us, "
         f"score + top-k {rr['predict_topk_ms']:.3f} ms")
-    mo = multi_output(T, W, ens, Xd, W.CONFIGS[HEADLINE_CFG], rec["kernel_ms"])
+    mo = multi_output(T, W, ens, Xd, W.WORKLOADS[HEADLINE], rec["kernel_ms"])
     log("vector leaves / bags: " + ", ".join(f"{k} {v['ms']:.3f} ms" for k, v in mo.items()))
-    fu = feature_usage(model, Xd, W.CONFIGS[HEADLINE_CFG], rec["visits"])
-    fu["pct_by_trees"] = feature_usage_by_trees(T, ens, Xd, W.CONFIGS[HEADLINE_CFG])
+    fu = feature_usage(model, Xd, W.WORKLOADS[HEADLINE], rec["visits"])
+    fu["pct_by_trees"] = feature_usage_by_trees(T, ens, Xd, W.WORKLOADS[HEADLINE])
     log(f"feature usage: {fu['avg_pct']:.1f}% of {fu['n_features']} features per document, "
         f"trace {fu['ms']:.3f} ms (LDS frac {fu['roofline']['frac']:.3f}); by trees {fu['pct_by_trees']}")
     model.close()
@@ -510,19 +511,21 @@ def main() -> int:
         log("codegen vs generic: " + ", ".join(
             f"{k} {v['codegen']['ms']:.3f} / {v['generic']['ms']:.3f} ms (compile {v['codegen']['create_s']:.1f} s)"
             for k, v in cg.items()))
-        for c, steps, samp in ((1, 20, None), (3, 10, None), (4, 5, None), (5, 3, 16384)):
-            r, m, _, xd, o = measure_config(T, W, c, steps, 1, visits_sample=samp)
+        for wl, steps, samp in (("tiny_10x8", 20, None), ("wide_1kx64_f700", 10, None),
+                                ("shallow_20kx8_1M", 5, None), ("large_5kx256_f700_1M", 3, 16384)):
+            r, m, _, xd, o = measure_workload(T, W, wl, steps, 1, visits_sample=samp)
             r.pop("model", None)
-            r["feature_usage"] = feature_usage(m, xd, W.CONFIGS[c], r["visits"], reps=1 if c >= 4 else 5)
-            log(f"config {c} feature usage: {r['feature_usage']['avg_pct']:.1f}%, "
+            big = W.WORKLOADS[wl].n_docs >= 1_000_000
+            r["feature_usage"] = feature_usage(m, xd, W.WORKLOADS[wl], r["visits"], reps=1 if big else 5)
+            log(f"{wl} feature usage: {r['feature_usage']['avg_pct']:.1f}%, "
                 f"trace {r['feature_usage']['ms']:.3f} ms")
-            extra[W.CONFIGS[c].name] = r
+            extra[wl] = r
             m.close()
             del xd, o
             torch.cuda.empty_cache()
 
-    cpu = None if args.no_cpu_baseline else cpu_baseline(W, HEADLINE_CFG)
-    cfg = W.CONFIGS[HEADLINE_CFG]
+    cpu = None if args.no_cpu_baseline else cpu_baseline(W, HEADLINE)
+    cfg = W.WORKLOADS[HEADLINE]
     line = {
         "metric": METRIC, "value": rec["value"], "unit": "doc·tree/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": rec["ms_per_step"],
@@ -537,7 +540,7 @@ def main() -> int:
         "multi_output": mo, "codegen": cg, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],
         "roofline_lds_issue": rec["roofline_lds_issue"],
-        "cpu_baseline": cpu, "configs_extra": extra, "kernel_hash": kernel_hash(),
+        "cpu_baseline": cpu, "workloads_extra": extra, "kernel_hash": kernel_hash(),
     }
     print(json.dumps(line), flush=True)
     return 0

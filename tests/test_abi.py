@@ -89,7 +89,7 @@ def test_oversized_tree_is_rejected():
 def test_valid_model_reaches_the_device_step():
     # on a host without a GPU a valid model passes validation and fails at the upload
     import torch
-    ens = W.make_ensemble(W.CONFIGS[1])
+    ens = W.make_ensemble(W.WORKLOADS["tiny_10x8"])
     if torch.cuda.is_available():
         pytest.skip("a GPU is present")
     with pytest.raises(T.TreeEnsError) as ei:

@@ -76,7 +76,7 @@ def test_generated_program_matches_the_oracle(tmp_path, seed):
 
 def test_generated_source_compiles_for_gfx950():
     # hiprtc needs no device
-    ens = W.make_ensemble(W.CONFIGS[1])
+    ens = W.make_ensemble(W.WORKLOADS["tiny_10x8"])
     src = _source(ens).encode()
     rtc = ctypes.CDLL("libhiprtc.so")
     prog = ctypes.c_void_p()
@@ -96,7 +96,7 @@ def test_source_shape_and_limits():
     src = _source(ens)
     assert 'extern "C" __global__' in src and "tree_ens_cg" in src and "x[1] >= 0x0p+0f" in src
     assert "x[1] > 0x0p+0f" in _source(ens, T.TREE_ENS_RIGHT_IF_GT)
-    big = W.make_ensemble(W.CONFIGS[4], n_trees=5000)  # 75,000 nodes
+    big = W.make_ensemble(W.WORKLOADS["shallow_20kx8_1M"], n_trees=5000)  # 75,000 nodes
     with pytest.raises(T.TreeEnsError) as ei:
         _source(big)
     assert ei.value.code == T.TREE_ENS_E_MODEL and "65536" in ei.value.message

@@ -42,14 +42,14 @@ def test_hand_ensemble_exact(T, rule, name):
     assert got.tolist() == [e[1] for e in expects[name]]
 
 
-@pytest.mark.parametrize("cfg_id,n_trees,n_docs", [(1, None, None), (2, 150, 20000), (3, 40, 5000),
-                                                   (4, 300, 100000)])
-def test_workload_prefixes(T, cfg_id, n_trees, n_docs):
-    cfg = W.CONFIGS[cfg_id]
+@pytest.mark.parametrize("wl,n_trees,n_docs", [("tiny_10x8", None, None), ("rank_1kx32", 150, 20000), ("wide_1kx64_f700", 40, 5000),
+                                                   ("shallow_20kx8_1M", 300, 100000)])
+def test_workload_prefixes(T, wl, n_trees, n_docs):
+    cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg, n_trees=n_trees)
     X = W.make_docs(cfg, n_docs=n_docs)
     ref, _, _ = oracle.score(ens, X, want_leaves=False)
-    assert_scores_close(_gpu(T, ens, X), ref, f"config {cfg_id} prefix")
+    assert_scores_close(_gpu(T, ens, X), ref, f"{wl} prefix")
 
 
 _POOL = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf, np.nan, 1e-45], dtype=np.float32)
@@ -70,7 +70,7 @@ def test_random_ensembles_corner_values(T, seed, n_docs):
 
 def test_other_entry_points_keep_the_generic_kernels(T):
     import torch
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=60)
     X = W.make_docs(cfg, n_docs=900)
     h = T.tree_ens_create(ens.tree_offsets, ens.feature, ens.threshold, ens.left, ens.right, ens.value,

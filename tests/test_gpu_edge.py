@@ -44,7 +44,7 @@ def test_hand_golden_on_gpu(T, rule, name):
 # workgroups plus a remainder, whose blocks the launch splits over the tiles (partial sums)
 @pytest.mark.parametrize("n_docs", [1, 7, 63, 64, 65, 127, 4097, 32773, 67331])
 def test_batch_sizes(T, n_docs):
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=300)
     X = W.make_docs(cfg, n_docs=n_docs)
     s, ids = _gpu(T, ens, X)
@@ -55,7 +55,7 @@ def test_batch_sizes(T, n_docs):
 
 def test_zero_docs_and_empty_model(T):
     import torch
-    ens = W.make_ensemble(W.CONFIGS[1])
+    ens = W.make_ensemble(W.WORKLOADS["tiny_10x8"])
     with T.TreeEnsemble.from_ensemble(ens) as m:
         out = m.predict(torch.empty((0, 136), dtype=torch.float32, device="cuda"))
         assert out.shape == (0,)
@@ -98,7 +98,7 @@ def test_single_leaf_trees_and_last_feature(T):
 
 def test_wider_rows_and_slices(T):
     import torch
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=200)
     X = W.make_docs(cfg, n_docs=3000)
     wide = np.concatenate([X, np.full((3000, 21), np.nan, np.float32)], axis=1)  # unused columns
@@ -116,7 +116,7 @@ def test_wider_rows_and_slices(T):
 
 def test_deterministic(T):
     import torch
-    cfg = W.CONFIGS[3]
+    cfg = W.WORKLOADS["wide_1kx64_f700"]
     ens = W.make_ensemble(cfg, n_trees=500)
     X = dev(W.make_docs(cfg, n_docs=20000))
     with T.TreeEnsemble.from_ensemble(ens) as m:
@@ -130,8 +130,8 @@ def test_deterministic(T):
 
 def test_streams_and_errors(T):
     import torch
-    ens = W.make_ensemble(W.CONFIGS[1])
-    X = W.make_docs(W.CONFIGS[1], n_docs=500)
+    ens = W.make_ensemble(W.WORKLOADS["tiny_10x8"])
+    X = W.make_docs(W.WORKLOADS["tiny_10x8"], n_docs=500)
     ref, _, _ = oracle.score(ens, X)
     with T.TreeEnsemble.from_ensemble(ens) as m:
         st = torch.cuda.Stream()

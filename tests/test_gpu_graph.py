@@ -23,7 +23,7 @@ def T():
 @pytest.mark.parametrize("n_docs", [100, 20000])
 def test_captured_predict_replays_match_eager(T, n_docs):
     import torch
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg, n_docs=n_docs)
     other_X = W.make_docs(cfg, n_docs=3000, start=n_docs)

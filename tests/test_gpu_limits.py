@@ -67,7 +67,7 @@ def test_largest_tree_one_tile_holds(T):
     # 2,923 leaves (5,845 nodes) is the largest tree accepted at 136 features; one more leaf
     # is refused at create
     ens = W.random_ensemble(1, n_trees=1, n_features=136, min_leaves=2923, max_leaves=2923)
-    X = W.make_docs(W.CONFIGS[2], n_docs=3000)
+    X = W.make_docs(W.WORKLOADS["rank_1kx32"], n_docs=3000)
     _check(T, ens, X, "largest tree")
     big = W.random_ensemble(1, n_trees=1, n_features=136, min_leaves=2924, max_leaves=2924)
     with pytest.raises(T.TreeEnsError) as ei:

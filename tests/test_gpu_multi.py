@@ -56,42 +56,42 @@ def test_golden_hand_ensemble(T, rule, name, n_bags):
     _close(got, np.stack([s, 2 * s + 3, -s], axis=1) / n_bags, f"golden {name} bags {n_bags}")
 
 
-@pytest.mark.parametrize("cfg_id,n_out,kind", [(1, 3, "probs"), (2, 5, "dense"), (2, 4, "class"),
-                                               (3, 6, "dense")])
-def test_configs_full(T, cfg_id, n_out, kind):
-    cfg = W.CONFIGS[cfg_id]
-    _say(f"[multi] config {cfg_id} ({cfg.name}): {n_out} outputs ({kind}), {cfg.n_docs} docs")
+@pytest.mark.parametrize("wl,n_out,kind", [("tiny_10x8", 3, "probs"), ("rank_1kx32", 5, "dense"), ("rank_1kx32", 4, "class"),
+                                               ("wide_1kx64_f700", 6, "dense")])
+def test_workloads_full(T, wl, n_out, kind):
+    cfg = W.WORKLOADS[wl]
+    _say(f"[multi] {wl}: {n_out} outputs ({kind}), {cfg.n_docs} docs")
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
-    vals = W.make_leaf_vectors(ens, n_out, kind, seed=cfg_id)
+    vals = W.make_leaf_vectors(ens, n_out, kind, seed=cfg.seed_key)
     got = _gpu(T, ens, vals, X)
     assert got.shape == (cfg.n_docs, n_out)
-    _close(got, oracle.score_multi(ens, vals, X), f"config {cfg_id} {kind}")
+    _close(got, oracle.score_multi(ens, vals, X), f"{wl} {kind}")
 
 
-@pytest.mark.parametrize("cfg_id,n_out", [(4, 6), (5, 2)])
-def test_config_1M_sampled(T, cfg_id, n_out):
+@pytest.mark.parametrize("wl,n_out", [("shallow_20kx8_1M", 6), ("large_5kx256_f700_1M", 2)])
+def test_workload_1M_sampled(T, wl, n_out):
     import torch
-    cfg = W.CONFIGS[cfg_id]
-    _say(f"[multi] config {cfg_id} ({cfg.name}) at full size, {n_out} outputs: generating")
+    cfg = W.WORKLOADS[wl]
+    _say(f"[multi] {wl} at full size, {n_out} outputs: generating")
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
-    vals = W.make_leaf_vectors(ens, n_out, "dense", sigma=0.01, seed=cfg_id)
-    sample = np.sort(np.random.default_rng(20 + cfg_id).choice(cfg.n_docs, size=2048, replace=False))
-    _say(f"[multi] config {cfg_id}: scoring {cfg.n_docs} docs on the GPU")
+    vals = W.make_leaf_vectors(ens, n_out, "dense", sigma=0.01, seed=cfg.seed_key)
+    sample = np.sort(np.random.default_rng(20 + cfg.seed_key).choice(cfg.n_docs, size=2048, replace=False))
+    _say(f"[multi] {wl}: scoring {cfg.n_docs} docs on the GPU")
     with T.TreeEnsemble.from_ensemble(ens, leaf_values=vals) as m:
         s = m.predict(dev(X))
         torch.cuda.synchronize()
         s = s.cpu().numpy()
-    _say(f"[multi] config {cfg_id}: oracle on {sample.size} sampled docs")
-    _close(s[sample], oracle.score_multi(ens, vals, X[sample]), f"config {cfg_id} sample")
+    _say(f"[multi] {wl}: oracle on {sample.size} sampled docs")
+    _close(s[sample], oracle.score_multi(ens, vals, X[sample]), f"{wl} sample")
 
 
 @pytest.mark.parametrize("n_docs", [1, 63, 65, 4097, 67331])
 def test_ragged_batches_and_splits(T, n_docs):
     # small batches split blocks over workgroups: four partial sums per document and launch,
     # reduced into the right columns (5 outputs: two launches, the second one partial)
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=300)
     X = W.make_docs(cfg, n_docs=n_docs)
     vals = W.make_leaf_vectors(ens, 5, "dense", seed=7)
@@ -101,7 +101,7 @@ def test_ragged_batches_and_splits(T, n_docs):
 
 @pytest.mark.parametrize("n_docs", [65, 5000])
 def test_coded_documents(T, n_docs):
-    cfg = W.CONFIGS[5]
+    cfg = W.WORKLOADS["large_5kx256_f700_1M"]
     ens = W.make_ensemble(cfg, n_trees=80)
     X = W.make_docs(cfg, n_docs=n_docs)
     vals = W.make_leaf_vectors(ens, 9, "probs", seed=2)
@@ -112,7 +112,7 @@ def test_coded_documents(T, n_docs):
 
 def test_bagging_scalar(T):
     import torch
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=400)
     X = W.make_docs(cfg, n_docs=3000)
     for b in (3, 7):
@@ -129,7 +129,7 @@ def test_bagging_scalar(T):
 
 def test_leaves_and_usage_of_a_vector_model(T):
     import torch
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=100)
     X = W.make_docs(cfg, n_docs=700)
     vals = W.make_leaf_vectors(ens, 3, "dense", seed=1)

@@ -40,42 +40,42 @@ def _run(T, ens, X, leaves_rows=None, flags=0):
         return s.cpu().numpy(), None if ids is None else ids.cpu().numpy()
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3])
-def test_config_full(T, cfg_id):
-    cfg = W.CONFIGS[cfg_id]
-    _say(f"[parity] config {cfg_id} ({cfg.name}): {cfg.n_trees} trees, {cfg.n_docs} docs")
+@pytest.mark.parametrize("wl", ["tiny_10x8", "rank_1kx32", "wide_1kx64_f700"])
+def test_workload_full(T, wl):
+    cfg = W.WORKLOADS[wl]
+    _say(f"[parity] {wl}: {cfg.n_trees} trees, {cfg.n_docs} docs")
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
     rows = min(cfg.n_docs, 8192)
     s, ids = _run(T, ens, X, leaves_rows=rows)
     ref, _, _ = oracle.score(ens, X, want_leaves=False)
-    assert_scores_close(s, ref, f"config {cfg_id}")
+    assert_scores_close(s, ref, f"{wl}")
     _, ref_ids, _ = oracle.score(ens, X[:rows])
-    assert_leaves_equal(ids, ref_ids, f"config {cfg_id}")
+    assert_leaves_equal(ids, ref_ids, f"{wl}")
 
 
 def test_config2_latency_batch(T):
     # the 100-document batch: too few documents to fill the GPU, so the trees are split over
     # workgroups and partial sums are reduced by a second kernel
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg, n_docs=100)
     s, ids = _run(T, ens, X, leaves_rows=100)
     ref, ref_ids, _ = oracle.score(ens, X)
-    assert_scores_close(s, ref, "config 2, 100 docs")
-    assert_leaves_equal(ids, ref_ids, "config 2, 100 docs")
+    assert_scores_close(s, ref, "rank_1kx32, 100 docs")
+    assert_leaves_equal(ids, ref_ids, "rank_1kx32, 100 docs")
 
 
-@pytest.mark.parametrize("cfg_id", [4, 5])
-def test_config_1M_sampled(T, cfg_id):
+@pytest.mark.parametrize("wl", ["shallow_20kx8_1M", "large_5kx256_f700_1M"])
+def test_workload_1M_sampled(T, wl):
     import torch
-    cfg = W.CONFIGS[cfg_id]
-    _say(f"[parity] config {cfg_id} ({cfg.name}) at full size: generating")
+    cfg = W.WORKLOADS[wl]
+    _say(f"[parity] {wl} at full size: generating")
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
-    rng = np.random.default_rng(cfg_id)
+    rng = np.random.default_rng(cfg.seed_key)
     sample = np.sort(rng.choice(cfg.n_docs, size=4096, replace=False))
-    _say(f"[parity] config {cfg_id}: scoring {cfg.n_docs} docs on the GPU")
+    _say(f"[parity] {wl}: scoring {cfg.n_docs} docs on the GPU")
     with T.TreeEnsemble.from_ensemble(ens) as m:
         Xd = dev(X)
         s = m.predict(Xd)
@@ -85,9 +85,9 @@ def test_config_1M_sampled(T, cfg_id):
         s = s.cpu().numpy()
         ids = ids.cpu().numpy()
         del Xd
-    _say(f"[parity] config {cfg_id}: oracle on the sample")
+    _say(f"[parity] {wl}: oracle on the sample")
     ref, _, _ = oracle.score(ens, X[sample], want_leaves=False)
-    assert_scores_close(s[sample], ref, f"config {cfg_id} sample")
+    assert_scores_close(s[sample], ref, f"{wl} sample")
     _, ref_ids, _ = oracle.score(ens, X[lo:])
-    assert_leaves_equal(ids, ref_ids, f"config {cfg_id} last 2048 docs")
+    assert_leaves_equal(ids, ref_ids, f"{wl} last 2048 docs")
     assert np.all(np.isfinite(s))

@@ -93,7 +93,7 @@ def test_predict_topk_on_ranking_workload(T):
     """Scoring and reranking of the ranking-shaped workload's query groups (20-200 candidates per
     query, the best 20 kept), in one call."""
     import torch
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
     sizes = W.make_query_groups(cfg)

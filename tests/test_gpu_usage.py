@@ -61,32 +61,32 @@ def test_golden_hand_ensemble(T, rule, name):
         assert counts[d] == len(feats)
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3])
-def test_config_full(T, cfg_id):
-    cfg = W.CONFIGS[cfg_id]
-    _say(f"[usage] config {cfg_id} ({cfg.name}): {cfg.n_trees} trees, {cfg.n_docs} docs")
+@pytest.mark.parametrize("wl", ["tiny_10x8", "rank_1kx32", "wide_1kx64_f700"])
+def test_workload_full(T, wl):
+    cfg = W.WORKLOADS[wl]
+    _say(f"[usage] {wl}: {cfg.n_trees} trees, {cfg.n_docs} docs")
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
     got = _gpu_usage(T, ens, X)
-    _assert_usage_equal(got, oracle.feature_usage(ens, X), f"config {cfg_id}")
+    _assert_usage_equal(got, oracle.feature_usage(ens, X), f"{wl}")
 
 
-@pytest.mark.parametrize("cfg_id", [4, 5])
-def test_config_1M_sampled(T, cfg_id):
+@pytest.mark.parametrize("wl", ["shallow_20kx8_1M", "large_5kx256_f700_1M"])
+def test_workload_1M_sampled(T, wl):
     import torch
-    cfg = W.CONFIGS[cfg_id]
-    _say(f"[usage] config {cfg_id} ({cfg.name}) at full size: generating")
+    cfg = W.WORKLOADS[wl]
+    _say(f"[usage] {wl} at full size: generating")
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
-    sample = np.sort(np.random.default_rng(10 + cfg_id).choice(cfg.n_docs, size=4096, replace=False))
-    _say(f"[usage] config {cfg_id}: tracing {cfg.n_docs} docs on the GPU")
+    sample = np.sort(np.random.default_rng(10 + cfg.seed_key).choice(cfg.n_docs, size=4096, replace=False))
+    _say(f"[usage] {wl}: tracing {cfg.n_docs} docs on the GPU")
     with T.TreeEnsemble.from_ensemble(ens) as m:
         c, mk = m.feature_usage(dev(X))
         torch.cuda.synchronize()
         c, mk = c.cpu().numpy(), mk.cpu().numpy().view(np.uint32)
-    _say(f"[usage] config {cfg_id}: oracle on {sample.size} sampled docs")
+    _say(f"[usage] {wl}: oracle on {sample.size} sampled docs")
     ref = oracle.feature_usage(ens, X[sample])
-    _assert_usage_equal((c[sample], mk[sample]), ref, f"config {cfg_id} sample")
+    _assert_usage_equal((c[sample], mk[sample]), ref, f"{wl} sample")
     # properties over every document: the count is the mask's popcount and at least the number
     # of distinct root features
     pop = np.unpackbits(mk.view(np.uint8), axis=1).sum(axis=1)
@@ -96,14 +96,14 @@ def test_config_1M_sampled(T, cfg_id):
 
 
 @pytest.mark.parametrize("n_docs", [1, 63, 64, 65, 4097])
-@pytest.mark.parametrize("cfg_id", [2, 3])
-def test_ragged_batches(T, cfg_id, n_docs):
-    # config 3 (700 features) runs the coded-document kernels
-    cfg = W.CONFIGS[cfg_id]
+@pytest.mark.parametrize("wl", ["rank_1kx32", "wide_1kx64_f700"])
+def test_ragged_batches(T, wl, n_docs):
+    # wide_1kx64_f700 (700 features) runs the one-workgroup float kernels
+    cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg, n_trees=150)
     X = W.make_docs(cfg, n_docs=n_docs)
     _assert_usage_equal(_gpu_usage(T, ens, X), oracle.feature_usage(ens, X),
-                        f"config {cfg_id}, {n_docs} docs")
+                        f"{wl}, {n_docs} docs")
 
 
 _POOL = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf, np.nan], dtype=np.float32)
@@ -125,7 +125,7 @@ def test_random_ensembles_rules_and_special_values(T, seed):
 def test_extra_document_columns_and_counts_only(T):
     # documents wider than the model reads: the mask rows follow the document width and the
     # words past the model's features are zero; counts alone when no mask is wanted
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=80)
     X = W.make_docs(cfg, n_docs=500)
     wide = np.concatenate([X, np.full((500, 100), 0.5, np.float32)], axis=1)
@@ -159,7 +159,7 @@ def test_leaf_only_and_empty_models(T):
 
 
 def test_argument_errors(T):
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=20)
     X = W.make_docs(cfg, n_docs=10)
     with T.TreeEnsemble.from_ensemble(ens) as m:

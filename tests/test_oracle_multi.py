@@ -39,7 +39,7 @@ def test_golden_hand_ensemble(rule, name):
 def test_each_component_is_the_scalar_score(kind, rule):
     # component c equals the scalar oracle's score of the ensemble whose leaf values are
     # column c (the same fp64 sum in the same tree order): pins the row stride and the column
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=70)
     X = W.make_docs(cfg, n_docs=300)
     vals = W.make_leaf_vectors(ens, 5, kind, seed=3)
@@ -54,7 +54,7 @@ def test_one_tree_per_class_closed_form():
     # multi-class boosting layout: tree t feeds class t % C only, so class c's output is the
     # scalar score of the sub-ensemble of trees c, c + C, c + 2C, ... (adding exact zeros
     # elsewhere changes nothing)
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     C = 4
     ens = W.make_ensemble(cfg, n_trees=41)
     X = W.make_docs(cfg, n_docs=250)
@@ -68,7 +68,7 @@ def test_one_tree_per_class_closed_form():
 def test_probability_leaves_sum_to_tree_count():
     # every leaf row of a forest classifier sums to 1: the outputs of a document sum to the
     # number of trees (up to float32 rounding of the rows)
-    cfg = W.CONFIGS[1]
+    cfg = W.WORKLOADS["tiny_10x8"]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
     vals = W.make_leaf_vectors(ens, 3, "probs", seed=1)

@@ -149,7 +149,7 @@ def test_complete_oblivious_tree_closed_form(depth, rule):
     # sum_k b_k 2^(d-1-k) (the implicit layout i -> 2i+1+b of the Pred form, Section 3).
     rng = np.random.default_rng(depth)
     n_trees, F = 6, 9
-    ens = W.make_ensemble(W.scaled(W.CONFIGS[4], n_trees=n_trees))
+    ens = W.make_ensemble(W.scaled(W.WORKLOADS["shallow_20kx8_1M"], n_trees=n_trees))
     ens = W.Ensemble(ens.tree_offsets, ens.feature.copy(), ens.threshold.copy(), ens.left, ens.right,
                      ens.value, F)
     if depth != 3:
@@ -276,10 +276,10 @@ def test_leaf_equiprobable_known_answers(seed, rule):
 # ------------------------------------------------------------------------------------------
 # the three walks agree on the configurations' own shapes
 # ------------------------------------------------------------------------------------------
-@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("wl", ["tiny_10x8", "rank_1kx32", "wide_1kx64_f700", "shallow_20kx8_1M", "large_5kx256_f700_1M"])
 @pytest.mark.parametrize("rule", RULES)
-def test_walks_agree_on_configs(cfg_id, rule):
-    cfg = W.CONFIGS[cfg_id]
+def test_walks_agree_on_workloads(wl, rule):
+    cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg, n_trees=min(cfg.n_trees, 40))
     X = W.make_docs(cfg, n_docs=300)
     s0, i0, v0 = oracle.score(ens, X, rule=rule, walk=0)
@@ -307,7 +307,7 @@ def _cat(a, b):
 
 
 def test_invariants():
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=60)
     X = W.make_docs(cfg, n_docs=400)
     s, ids, _ = oracle.score(ens, X)
@@ -349,7 +349,7 @@ def test_strict_rule_equals_nudged_threshold():
     # right iff x > theta  <=>  right iff x >= next float32 above theta (no float32 lies
     # strictly between them); theta = +inf has no successor: x > +inf is never true, which is
     # what a NaN threshold gives under >=.
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=50)
     X = W.make_docs(cfg, n_docs=500)
     internal = ens.feature >= 0
@@ -369,7 +369,7 @@ def test_strict_rule_equals_nudged_threshold():
 
 
 def test_thread_count_does_not_change_results():
-    cfg = W.CONFIGS[3]
+    cfg = W.WORKLOADS["wide_1kx64_f700"]
     ens = W.make_ensemble(cfg, n_trees=30)
     X = W.make_docs(cfg, n_docs=700)
     a = oracle.score(ens, X, threads=1)

@@ -137,7 +137,7 @@ def _slice(ens, a, b):
 
 
 def test_invariants():
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=80)
     X = W.make_docs(cfg, n_docs=300)
     F = ens.n_features
@@ -180,7 +180,7 @@ def test_invariants():
 
 
 def test_thread_count_does_not_change_results():
-    cfg = W.CONFIGS[3]
+    cfg = W.WORKLOADS["wide_1kx64_f700"]
     ens = W.make_ensemble(cfg, n_trees=40)
     X = W.make_docs(cfg, n_docs=500)
     a = oracle.feature_usage(ens, X, threads=1)

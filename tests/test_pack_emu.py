@@ -80,17 +80,17 @@ def test_random_ensembles(emu, seed):
     _check(emu, ens, X, flags=seed % 2)
 
 
-@pytest.mark.parametrize("cfg_id,n_trees,n_docs,expect", [
-    (1, None, 200, dict(dl=64, coded=0)),
-    (2, None, 130, dict(dl=64, coded=0)),
-    (3, 300, 70, dict(dl=32, coded=0)),
-    (4, 3000, 70, dict(dl=64, coded=0)),
-    (5, 200, 70, dict(dl=64, coded=1, narrow=0)),
+@pytest.mark.parametrize("wl,n_trees,n_docs,expect", [
+    ("tiny_10x8", None, 200, dict(dl=64, coded=0)),
+    ("rank_1kx32", None, 130, dict(dl=64, coded=0)),
+    ("wide_1kx64_f700", 300, 70, dict(dl=32, coded=0)),
+    ("shallow_20kx8_1M", 3000, 70, dict(dl=64, coded=0)),
+    ("large_5kx256_f700_1M", 200, 70, dict(dl=64, coded=1, narrow=0)),
 ])
-def test_workload_shapes(emu, cfg_id, n_trees, n_docs, expect):
+def test_workload_shapes(emu, wl, n_trees, n_docs, expect):
     """Prefixes of the benchmark workloads: both record formats, float and coded documents,
-    complete-depth tiles (configuration 4), several interleave factors."""
-    cfg = W.CONFIGS[cfg_id]
+    complete-depth tiles (shallow_20kx8_1M), several interleave factors."""
+    cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg, n_trees=n_trees)
     X = W.make_docs(cfg, n_docs=n_docs)
     plan = _check(emu, ens, X, levels=(0, 4))
@@ -99,19 +99,19 @@ def test_workload_shapes(emu, cfg_id, n_trees, n_docs, expect):
         assert plan[2] == expect["narrow"], plan
 
 
-@pytest.mark.parametrize("cfg_id,n_trees,n_out,kind", [
-    (1, None, 3, "probs"),
-    (2, 120, 5, "class"),
-    (4, 800, 2, "dense"),  # complete-depth tiles
-    (5, 60, 7, "dense"),  # coded documents
+@pytest.mark.parametrize("wl,n_trees,n_out,kind", [
+    ("tiny_10x8", None, 3, "probs"),
+    ("rank_1kx32", 120, 5, "class"),
+    ("shallow_20kx8_1M", 800, 2, "dense"),  # complete-depth tiles
+    ("large_5kx256_f700_1M", 60, 7, "dense"),  # coded documents
 ])
-def test_vector_valued_leaves(emu, cfg_id, n_trees, n_out, kind):
+def test_vector_valued_leaves(emu, wl, n_trees, n_out, kind):
     """Leaf records name their row of the leaf-vector table (row 0 = the zero record's); the
     rows summed over the walks equal the oracle's vector-valued scores."""
-    cfg = W.CONFIGS[cfg_id]
+    cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg, n_trees=n_trees)
     X = W.make_docs(cfg, n_docs=90)
-    vals = W.make_leaf_vectors(ens, n_out, kind, seed=cfg_id)
+    vals = W.make_leaf_vectors(ens, n_out, kind, seed=cfg.seed_key)
     ref = oracle.score_multi(ens, vals, X)
     _, ref_leaves, _ = oracle.score(ens, X)
     for lv in (0, 4):
@@ -123,7 +123,7 @@ def test_vector_valued_leaves(emu, cfg_id, n_trees, n_out, kind):
 def test_coded_documents_with_corner_values(emu):
     """Coded plan: NaN, +-inf, +-0 and values equal to thresholds; the emulator checks every
     staged code of the coding kernel's branch-free descent against a plain count."""
-    cfg = W.CONFIGS[5]
+    cfg = W.WORKLOADS["large_5kx256_f700_1M"]
     ens = W.make_ensemble(cfg, n_trees=40)
     X = W.make_docs(cfg, n_docs=80)
     rng = np.random.default_rng(0)
@@ -193,8 +193,8 @@ def test_tree_order_ignores_node_numbering(emu, seed):
 def test_tree_order_keeps_complete_trees_together(emu):
     """Complete trees of one depth stay contiguous in a mixed model, and a model of complete trees
     is cut into complete-depth tiles only."""
-    rand = W.make_ensemble(W.CONFIGS[2], n_trees=300)
-    comp = W.make_ensemble(W.CONFIGS[4], n_trees=500)
+    rand = W.make_ensemble(W.WORKLOADS["rank_1kx32"], n_trees=300)
+    comp = W.make_ensemble(W.WORKLOADS["shallow_20kx8_1M"], n_trees=500)
     trees = []
     for i in range(800):
         e, t = (comp, i // 2) if i % 8 < 5 and i // 2 < 500 else (rand, i % 300)
@@ -212,7 +212,7 @@ def test_tree_order_shortens_the_lockstep_walk(emu):
     """On the ranking-shaped model, groups of 4 trees taken in the packed order need fewer
     lockstep steps (per 64-document wave, the longest path of any tree in the group) than in the
     input order: the estimate tracks the real path lengths."""
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg, n_docs=64 * 16)
     _, leaves, _ = oracle.score(ens, X)

@@ -68,9 +68,10 @@ def test_valid_models(driver):
     files = []
     ens, X, _ = load_hand_ensemble()
     files.append(_write(d / "hand.bin", ens, X))
-    for cfg_id, n_trees, n_docs in ((1, None, 130), (2, 150, 70), (3, 60, 40), (4, 400, 70), (5, 30, 66)):
-        cfg = W.CONFIGS[cfg_id]
-        files.append(_write(d / f"cfg{cfg_id}.bin", W.make_ensemble(cfg, n_trees=n_trees),
+    for wl, n_trees, n_docs in (("tiny_10x8", None, 130), ("rank_1kx32", 150, 70), ("wide_1kx64_f700", 60, 40),
+                                ("shallow_20kx8_1M", 400, 70), ("large_5kx256_f700_1M", 30, 66)):
+        cfg = W.WORKLOADS[wl]
+        files.append(_write(d / f"{wl}.bin", W.make_ensemble(cfg, n_trees=n_trees),
                             W.make_docs(cfg, n_docs=n_docs)))
     for seed in range(6):
         F = (1, 7, 33, 136, 260, 5)[seed]
@@ -78,7 +79,7 @@ def test_valid_models(driver):
                                 thr_values=_POOL[:7] if seed % 2 else None)
         X = W.random_docs(seed, 97, F, values=_POOL if seed % 2 else None, zero_frac=0.2)
         files.append(_write(d / f"rand{seed}.bin", ens, X))
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=50)
     files.append(_write(d / "vec.bin", ens, W.make_docs(cfg, n_docs=65),
                         values=W.make_leaf_vectors(ens, 3, "dense", seed=1)))

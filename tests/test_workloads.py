@@ -18,9 +18,9 @@ def _depths(fe, le, ri):
     return d
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4, 5])
-def test_config_shapes(cfg_id):
-    cfg = W.CONFIGS[cfg_id]
+@pytest.mark.parametrize("wl", sorted(W.WORKLOADS))
+def test_workload_shapes_and_seeds(wl):
+    cfg = W.WORKLOADS[wl]
     T = min(cfg.n_trees, 200)
     ens = W.make_ensemble(cfg, n_trees=T)
     assert ens.n_trees == T
@@ -54,7 +54,7 @@ def test_config_shapes(cfg_id):
 
 
 def test_determinism_and_prefixes():
-    cfg = W.CONFIGS[2]
+    cfg = W.WORKLOADS["rank_1kx32"]
     a = W.make_ensemble(cfg, n_trees=30)
     b = W.make_ensemble(cfg, n_trees=10)
     c = a.take_trees(10)
@@ -63,11 +63,11 @@ def test_determinism_and_prefixes():
     X1 = W.make_docs(cfg, n_docs=9000)
     X2 = W.make_docs(cfg, n_docs=2500, start=4000)
     assert np.array_equal(X1[4000:6500], X2)
-    assert not np.array_equal(W.make_docs(W.CONFIGS[4], n_docs=10), W.make_docs(W.CONFIGS[1], n_docs=10))
+    assert not np.array_equal(W.make_docs(W.WORKLOADS["shallow_20kx8_1M"], n_docs=10), W.make_docs(W.WORKLOADS["tiny_10x8"], n_docs=10))
 
 
 def test_thresholds_come_from_the_sample():
-    cfg = W.CONFIGS[5]
+    cfg = W.WORKLOADS["large_5kx256_f700_1M"]
     S = W.make_threshold_sample(cfg)
     ens = W.make_ensemble(cfg, n_trees=5)
     internal = ens.feature >= 0
@@ -77,8 +77,8 @@ def test_thresholds_come_from_the_sample():
 
 
 def test_query_groups():
-    g = W.make_query_groups(W.CONFIGS[2])
-    assert g.sum() == W.CONFIGS[2].n_docs
+    g = W.make_query_groups(W.WORKLOADS["rank_1kx32"])
+    assert g.sum() == W.WORKLOADS["rank_1kx32"].n_docs
     assert g[:-1].min() >= 20 and g.max() <= 200
 
 

@@ -85,7 +85,7 @@ class Ensemble:
 class Config:
     """One synthetic workload: ensemble shape, threshold rule, leaf and feature distributions."""
 
-    cfg_id: int
+    seed_key: int  # first spawn key of the workload's random streams
     name: str
     n_trees: int
     n_leaves: int
@@ -101,19 +101,21 @@ class Config:
     notes: str = ""
 
 
-CONFIGS = {
-    1: Config(1, "tiny_10x8", 10, 8, None, False, 136, 1_000, 0.0, "uniform", "uniform", 1.0,
-              notes="10 trees x 8 leaves, 7 uniform leaf splits (unbalanced), U[0,1) features"),
-    2: Config(2, "rank_1kx32", 1_000, 32, 16, False, 136, 100_000, 0.30, "lognormal", "sample", 0.1,
-              query_groups=True,
-              notes="MSLR-shaped: 136 features, 1k trees x 32 leaves, depth <= 16"),
-    3: Config(3, "wide_1kx64_f700", 1_000, 64, 20, False, 700, 50_000, 0.60, "uniform", "sample_nonzero", 0.1,
-              notes="wide features: 700 features, 1k trees x 64 leaves, depth <= 20"),
-    4: Config(4, "shallow_20kx8_1M", 20_000, 8, 3, True, 136, 1_000_000, 0.0, "uniform", "uniform", 0.01,
-              notes="20k complete depth-3 trees, 1M docs"),
-    5: Config(5, "large_5kx256_f700_1M", 5_000, 256, 24, False, 700, 1_000_000, 0.50, "lognormal", "sample", 0.01,
-              notes="5k trees x 256 leaves, depth <= 24, 700 features, 1M docs (model exceeds LDS)"),
-}
+_ALL = (
+    Config(1, "tiny_10x8", 10, 8, None, False, 136, 1_000, 0.0, "uniform", "uniform", 1.0,
+           notes="10 trees x 8 leaves, 7 uniform leaf splits (unbalanced), U[0,1) features"),
+    Config(2, "rank_1kx32", 1_000, 32, 16, False, 136, 100_000, 0.30, "lognormal", "sample", 0.1,
+           query_groups=True,
+           notes="MSLR-shaped: 136 features, 1k trees x 32 leaves, depth <= 16"),
+    Config(3, "wide_1kx64_f700", 1_000, 64, 20, False, 700, 50_000, 0.60, "uniform", "sample_nonzero", 0.1,
+           notes="wide features: 700 features, 1k trees x 64 leaves, depth <= 20"),
+    Config(4, "shallow_20kx8_1M", 20_000, 8, 3, True, 136, 1_000_000, 0.0, "uniform", "uniform", 0.01,
+           notes="20k complete depth-3 trees, 1M docs"),
+    Config(5, "large_5kx256_f700_1M", 5_000, 256, 24, False, 700, 1_000_000, 0.50, "lognormal", "sample", 0.01,
+           notes="5k trees x 256 leaves, depth <= 24, 700 features, 1M docs (model exceeds LDS)"),
+)
+# the five workloads by name
+WORKLOADS = {c.name: c for c in _ALL}
 
 
 # ----------------------------------------------------------------------------------------------
@@ -148,7 +150,7 @@ def make_docs(cfg: Config, n_docs: Optional[int] = None, start: int = 0) -> np.n
         return out
     for k in range(start // X_CHUNK_ROWS, (end - 1) // X_CHUNK_ROWS + 1):
         c0 = k * X_CHUNK_ROWS
-        blk = _feature_block(_rng(cfg.cfg_id, _S_X, k, 0), _rng(cfg.cfg_id, _S_X, k, 1), X_CHUNK_ROWS, F,
+        blk = _feature_block(_rng(cfg.seed_key, _S_X, k, 0), _rng(cfg.seed_key, _S_X, k, 1), X_CHUNK_ROWS, F,
                              cfg.zero_frac, cfg.nonzero)
         lo, hi = max(start, c0), min(end, c0 + X_CHUNK_ROWS)
         out[lo - start:hi - start] = blk[lo - c0:hi - c0]
@@ -158,14 +160,14 @@ def make_docs(cfg: Config, n_docs: Optional[int] = None, start: int = 0) -> np.n
 def make_threshold_sample(cfg: Config) -> np.ndarray:
     """The seeded ``SAMPLE_ROWS x n_features`` sample (same distribution as the documents,
     independent stream) that data-driven thresholds are drawn from."""
-    return _feature_block(_rng(cfg.cfg_id, _S_SAMPLE, 0), _rng(cfg.cfg_id, _S_SAMPLE, 1), SAMPLE_ROWS,
+    return _feature_block(_rng(cfg.seed_key, _S_SAMPLE, 0), _rng(cfg.seed_key, _S_SAMPLE, 1), SAMPLE_ROWS,
                           cfg.n_features, cfg.zero_frac, cfg.nonzero)
 
 
 def make_query_groups(cfg: Config, n_docs: Optional[int] = None) -> np.ndarray:
     """Query-group sizes U{20..200} covering ``n_docs`` documents (the last group truncated)."""
     n = cfg.n_docs if n_docs is None else int(n_docs)
-    rng = _rng(cfg.cfg_id, _S_QUERY)
+    rng = _rng(cfg.seed_key, _S_QUERY)
     sizes = []
     total = 0
     while total < n:
@@ -276,7 +278,7 @@ def make_ensemble(cfg: Config, n_trees: Optional[int] = None) -> Ensemble:
     feats, thrs, lefts, rights, vals = [], [], [], [], []
     offsets = np.zeros(T + 1, dtype=np.int64)
     for t in range(T):
-        rs = _rng(cfg.cfg_id, _S_STRUCT, t)
+        rs = _rng(cfg.seed_key, _S_STRUCT, t)
         if cfg.complete:
             depth = int(cfg.n_leaves).bit_length() - 1
             if (1 << depth) != cfg.n_leaves:
@@ -284,10 +286,10 @@ def make_ensemble(cfg: Config, n_trees: Optional[int] = None) -> Ensemble:
             f, l, r = grow_complete_structure(rs, depth, cfg.n_features)
         else:
             f, l, r = grow_random_structure(rs, cfg.n_leaves, cfg.max_depth, cfg.n_features)
-        thr = _draw_thresholds(cfg, _rng(cfg.cfg_id, _S_THRESH, t), f, sample, nz_cols)
+        thr = _draw_thresholds(cfg, _rng(cfg.seed_key, _S_THRESH, t), f, sample, nz_cols)
         val = np.zeros(f.shape[0], dtype=np.float32)
         leaves = np.nonzero(f < 0)[0]
-        val[leaves] = (_rng(cfg.cfg_id, _S_LEAF, t).normal(0.0, cfg.leaf_sigma, leaves.shape[0])
+        val[leaves] = (_rng(cfg.seed_key, _S_LEAF, t).normal(0.0, cfg.leaf_sigma, leaves.shape[0])
                        .astype(np.float32))
         feats.append(f)
         thrs.append(thr)
