@@ -165,7 +165,7 @@ def test_tree_order_known_answer(emu):
     estimated by the share of the model's thresholds on its feature below its own. A complete
     tree's key is its depth; a deep chain whose root threshold is the lowest of its feature
     sends every document right to a leaf at depth 1 (key 1); complete trees come first among
-    equal keys. Depth-first ordering would put the chain first."""
+    equal keys. Ordering by depth, deepest first, would put the chain first."""
     complete2 = ([0, 0, 0, -1, -1, -1, -1], [0.5, 0.25, 0.75, 0, 0, 0, 0], [1, 3, 5, -1, -1, -1, -1],
                  [2, 4, 6, -1, -1, -1, -1], [0, 0, 0, 1, 2, 3, 4])
     # root (lowest threshold) -> right leaf 2; left: a chain 1 -> 3 -> 5 of depth 4
