@@ -54,7 +54,28 @@ def test_workload_full(T, wl):
     assert_leaves_equal(ids, ref_ids, f"{wl}")
 
 
-def test_config2_latency_batch(T):
+@pytest.mark.parametrize("wl", ["rank_1kx32", "wide_1kx64_f700"])
+def test_workload_full_strict_rule(T, wl):
+    # right iff x > theta: the packer stores the next float above each threshold (and +inf as
+    # "never right"); every score and the leaf ids of the first 8,192 documents
+    cfg = W.WORKLOADS[wl]
+    _say(f"[parity] {wl}, strict rule: {cfg.n_trees} trees, {cfg.n_docs} docs")
+    ens = W.make_ensemble(cfg)
+    X = W.make_docs(cfg)
+    rows = min(cfg.n_docs, 8192)
+    s, ids = _run(T, ens, X, leaves_rows=rows, flags=T.TREE_ENS_RIGHT_IF_GT)
+    ref, _, _ = oracle.score(ens, X, rule=1, want_leaves=False)
+    assert_scores_close(s, ref, f"{wl} strict")
+    _, ref_ids, _ = oracle.score(ens, X[:rows], rule=1)
+    assert_leaves_equal(ids, ref_ids, f"{wl} strict")
+    if wl == "rank_1kx32":
+        # thresholds sampled from feature values (zeros included) tie with document values, so
+        # the two rules send documents to different leaves (wide_1kx64_f700 has no such ties)
+        _, ge_ids, _ = oracle.score(ens, X[:rows], rule=0)
+        assert not np.array_equal(ge_ids, ref_ids)
+
+
+def test_rank_1kx32_latency_batch(T):
     # the 100-document batch: too few documents to fill the GPU, so the trees are split over
     # workgroups and partial sums are reduced by a second kernel
     cfg = W.WORKLOADS["rank_1kx32"]
