@@ -52,6 +52,10 @@ LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
     const int usage_bytes = int((int64_t(n_cols) + 31) / 32 * p.docs_per_block * 4);
     const int usage_room = p.lds_bytes == kLdsPerCu ? (usage_bytes + 15) & ~15 : 0;
     p.tile_bytes = std::min(p.lds_bytes - p.xs_bytes - reserve - usage_room, prefetch * 1024 * 8) & ~15;
+    // One-workgroup plans copy a tile window as whole chunks of 1,024 records (one per thread):
+    // a slot of whole chunks keeps that copy off the zero record and the trace's bitmasks.
+    if (p.lds_bytes == kLdsPerCu)
+        p.tile_bytes = p.tile_bytes / (1024 * 8) * (1024 * 8);
     p.zero_rec = p.xs_bytes + p.tile_bytes;
     p.usage_off = p.lds_bytes == kLdsPerCu ? (p.zero_rec + 8 + 15) & ~15 : kLdsPerCu / 2;
     // Interleave K trees per lane (latency hiding) only when a tile holds at least K rounds of

@@ -436,27 +436,23 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                         }
                     }
                 } else if constexpr (VEC) {
-                    // a leaf's threshold slot holds its table row + 1 (idle slots: row 0, zeros)
-                    float gs[kVecPerLaunch] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    // a leaf's threshold slot holds its table row + 1 (idle slots: row 0, zeros);
+                    // each component added to its double accumulator in tree order
 #pragma unroll
                     for (int i = 0; i < K; ++i) {
                         const float4 v = leaf_vec[int64_t(rec_thr(nd[i]) - 1u) * vec_stride4 + chunk];
-                        gs[0] += v.x;
-                        gs[1] += v.y;
-                        gs[2] += v.z;
-                        gs[3] += v.w;
+                        accv[0] += double(v.x);
+                        accv[1] += double(v.y);
+                        accv[2] += double(v.z);
+                        accv[3] += double(v.w);
                     }
-#pragma unroll
-                    for (int c = 0; c < kVecPerLaunch; ++c)
-                        accv[c] += double(gs[c]);
                 } else if constexpr (!USAGE) {
-                    // K leaf values: exact enough in float, one double add (idle slots hold the
-                    // zero record)
-                    float group_sum = __uint_as_float(rec_thr(nd[0]));
+                    // the K leaf values, each added to the double accumulator in tree order (a
+                    // float sum of the group first can miss the tolerance when a score cancels
+                    // near zero); idle slots hold the zero record
 #pragma unroll
-                    for (int i = 1; i < K; ++i)
-                        group_sum += __uint_as_float(rec_thr(nd[i]));
-                    acc += double(group_sum);
+                    for (int i = 0; i < K; ++i)
+                        acc += double(__uint_as_float(rec_thr(nd[i])));
                 }
             }
         };
@@ -487,6 +483,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     } else {
         // the document rows (loaded after the first two tiles) land before the first barrier
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        // windows are written as whole 1,024-record chunks: the packer sizes the slot of these
+        // plans to whole chunks, so the zero record and the trace's bitmasks after it are safe
         auto write_window = [&](const uint2 (&src)[kWin]) {
 #pragma unroll
             for (int j = 0; j < kWin; ++j)

@@ -75,8 +75,9 @@ const char *emu_message(void) { return g_msg.c_str(); }
 
 // Walk all documents through tiling `level`. Outputs leaf ids [n_docs][n_trees] (input node ids)
 // and fp64 scores [n_docs][n_outputs] (vector-valued leaves read through the leaf-vector table).
-// Returns 0, or 1 with a message naming the first violated invariant, or a negative packer
-// status.
+// plan_out (8 ints): docs per block, trees per lane, record format, coded, tiles at tiling 0,
+// LDS bytes, tile slot bytes, records of the largest tiling-0 image. Returns 0, or 1 with a message naming the first violated
+// invariant, or a negative packer status.
 int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
              const float *threshold, const int32_t *left, const int32_t *right, const float *value,
              int32_t n_outputs, uint32_t flags, const float *X, int64_t n_docs, int32_t n_features,
@@ -97,6 +98,8 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         plan_out[3] = pl.coded;
         plan_out[4] = p.level_begin[1] - p.level_begin[0];
         plan_out[5] = pl.lds_bytes;
+        plan_out[6] = pl.tile_bytes;
+        plan_out[7] = p.level_slot_recs[0];
     }
     const int DL = pl.docs_per_block, K = pl.interleave, E = pl.elem_bytes;
     const int shift = pl.narrow ? 16 : treeens::kWideChildShift;
@@ -143,6 +146,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
     // of whole 1,024-record chunks, at most 8 per tile, with one
     if (pl.lds_bytes == treeens::kLdsPerCu) {
         const int64_t chunks = (slot + 1023) / 1024;
+        // the kernel writes whole chunks: they must fit the prefetch registers and the slot
         if (chunks > treeens::kPrefetchFull / 2 || chunks * 1024 * 8 > pl.tile_bytes)
             return bad("tile window exceeds the registers or the LDS slot");
         const int64_t last = p.level_image_off[level] + int64_t(t1 - t0 - 1) * slot;

@@ -73,3 +73,37 @@ def test_largest_tree_one_tile_holds(T):
     with pytest.raises(T.TreeEnsError) as ei:
         T.TreeEnsemble.from_ensemble(big)
     assert ei.value.code == T.TREE_ENS_E_MODEL
+
+
+# (features, leaves per tree at most, documents per block): float plans with 4, 2 and 1 trees
+# per lane and two threshold-coded plans (the emulator test pins each plan's shape)
+@pytest.mark.parametrize("n_features,max_leaves,dl", [(380, 100, 64), (760, 100, 32), (3000, 40, 8),
+                                                      (1530, 200, 32), (3000, 200, 16)])
+def test_slots_of_whole_chunks(T, n_features, max_leaves, dl):
+    """Near the top of each block-width band the document tile and the trace's bitmasks leave
+    less than 64 KiB for the tile slot of one-workgroup plans, which the packer sizes to whole
+    1,024-record chunks (the unit a window is copied in); large trees fill the last chunk (the
+    emulator test pins each plan). A batch of more blocks than the GPU holds at once runs whole
+    blocks at tiling 0: scores, leaf ids and the feature trace (whose bitmasks follow the slot,
+    as the zero record of idle tree slots does) against the oracle, under the strict rule."""
+    import torch
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf], np.float32)
+    ens = W.random_ensemble(5066, n_trees=160, n_features=n_features, min_leaves=1,
+                            max_leaves=max_leaves, thr_values=pool)
+    n_docs = 300 * dl  # 300 blocks: more than the 256 resident workgroups
+    X = W.random_docs(5066, n_docs, n_features, values=np.append(pool, np.nan).astype(np.float32),
+                      zero_frac=0.2)
+    with T.TreeEnsemble.from_ensemble(ens, T.TREE_ENS_RIGHT_IF_GT) as m:
+        assert m.info()["docs_per_block"] == dl
+        x = dev(X)
+        s = m.predict(x)
+        ids = m.predict_leaves(x)
+        cnt, masks = m.feature_usage(x)
+        torch.cuda.synchronize()
+        s, ids = s.cpu().numpy(), ids.cpu().numpy()
+        cnt, masks = cnt.cpu().numpy(), masks.cpu().numpy().view(np.uint32)
+    ref, ref_ids, _ = oracle.score(ens, X, rule=1)
+    assert_scores_close(s, ref, f"{n_features} features")
+    assert_leaves_equal(ids, ref_ids, f"{n_features} features")
+    ref_cnt, ref_masks = oracle.feature_usage(ens, X, rule=1)
+    assert np.array_equal(masks, ref_masks) and np.array_equal(cnt, ref_cnt), f"{n_features} features: trace"

@@ -77,7 +77,7 @@ def test_invariants_on_the_gpu(T, c):
     ens, X = _make(c)
     rule = c["rule"]
     s, ids = _run(T, ens, X, rule)
-    # doubling every leaf value doubles every score exactly (fp32 group sums, fp64 accumulation
+    # doubling every leaf value doubles every score exactly (fp64 accumulation
     # and the final rounding all commute with an exact power-of-two scaling)
     ens2 = W.Ensemble(ens.tree_offsets, ens.feature, ens.threshold, ens.left, ens.right,
                       (ens.value * 2).astype(np.float32), ens.n_features)

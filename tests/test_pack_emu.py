@@ -46,7 +46,7 @@ def _walk(lib, ens, X, level, flags=0, leaf_values=None):
     X = np.ascontiguousarray(X, np.float32)
     leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
     scores = np.empty((X.shape[0], n_out), np.float64)
-    plan = np.zeros(6, np.int32)
+    plan = np.zeros(8, np.int32)
     rc = lib.emu_walk(ens.n_trees, *[a.ctypes.data for a in arrs], n_out, flags, X.ctypes.data,
                       X.shape[0], X.shape[1], level, leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
     assert rc == 0, lib.emu_message().decode()
@@ -230,3 +230,26 @@ def test_tree_order_shortens_the_lockstep_walk(emu):
 
     order, _ = _order(emu, ens)
     assert steps(order) < 0.9 * steps(np.arange(ens.n_trees))
+
+
+# feature counts near the top of a block-width band of one-workgroup plans, where the document
+# tile and the trace's bitmasks leave less than 64 KiB for the tile slot: (features, leaves per
+# tree at most, documents per block, trees per lane, coded documents)
+BAND_TOP_PLANS = [(380, 100, 64, 4, 0), (760, 100, 32, 2, 0), (3000, 40, 8, 1, 0),
+                  (1530, 200, 32, 1, 1), (3000, 200, 16, 1, 1)]
+
+
+@pytest.mark.parametrize("n_features,max_leaves,dl,k,coded", BAND_TOP_PLANS)
+def test_slots_of_whole_chunks(emu, n_features, max_leaves, dl, k, coded):
+    """The kernel writes a tile window as whole 1,024-record chunks, so the slot of these plans
+    must be a whole number of chunks (a slot of 64,768 bytes once let the last chunk overwrite
+    the zero record and the trace's bitmasks). Large trees fill the last chunk."""
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf], np.float32)
+    ens = W.random_ensemble(5066, n_trees=160, n_features=n_features, min_leaves=1,
+                            max_leaves=max_leaves, thr_values=pool)
+    X = W.random_docs(5066, 70, n_features)
+    plan = _check(emu, ens, X, flags=1, levels=(0, 1))
+    assert (plan[0], plan[1], plan[3]) == (dl, k, coded), plan
+    tile_bytes, slot_recs = int(plan[6]), int(plan[7])
+    assert plan[5] == 160 * 1024 and tile_bytes % 8192 == 0 and tile_bytes < 64 * 1024, plan
+    assert tile_bytes - 8192 < slot_recs * 8 <= tile_bytes, plan  # the last chunk is in use
