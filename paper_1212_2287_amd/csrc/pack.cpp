@@ -496,8 +496,107 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
 
+    // ---- walker packets (two-workgroup plans of 64-document blocks; see pack.hpp) -----------
+    if (plan.lds_bytes == kLdsPerCu / 2 && plan.docs_per_block == 64 && n_trees > 0) {
+        constexpr int32_t W = kPacketWalkers;
+        const int32_t sub = int32_t(int64_t(plan.tile_bytes) / 8 / W / 64 * 64); // records per sub-slot
+        const int32_t n_groups = (n_trees + K - 1) / K;
+        auto group_recs = [&](int32_t g) {
+            const int32_t t0 = g * K, t1 = std::min(n_trees, t0 + K);
+            return int64_t(p.tree_node_off[size_t(t1)]) - int64_t(p.tree_node_off[size_t(t0)]);
+        };
+        auto packet_recs = [&](int32_t ng, int64_t tree_recs) {
+            return int64_t(kPacketHeaderRecs) + int64_t(ng) * K + (int64_t(ng) * K + 3) / 4 + tree_recs;
+        };
+        // per walker: runs (first group, groups) of its consecutive groups that fit a sub-slot
+        std::vector<std::vector<std::pair<int32_t, int32_t>>> runs(static_cast<size_t>(W));
+        bool fits = sub > 0 && sub / 64 <= kPrefetchHalf;
+        for (int32_t w = 0; w < W && fits; w++) {
+            int32_t first = -1, count = 0;
+            int64_t recs = 0;
+            for (int32_t g = w; g < n_groups; g += W) {
+                const int64_t gr = group_recs(g);
+                if (first >= 0 && packet_recs(count + 1, recs + gr) <= sub) {
+                    count++;
+                    recs += gr;
+                    continue;
+                }
+                if (first >= 0)
+                    runs[size_t(w)].push_back({first, count});
+                if (packet_recs(1, gr) > sub) {
+                    fits = false;
+                    break;
+                }
+                first = g;
+                count = 1;
+                recs = gr;
+            }
+            if (fits && first >= 0)
+                runs[size_t(w)].push_back({first, count});
+        }
+        if (fits) {
+            int32_t per = 0;
+            for (const auto &r : runs)
+                per = std::max(per, int32_t(r.size()));
+            p.pk_recs = sub;
+            p.pk_per_walker = per;
+            p.packets.assign(size_t(W) * size_t(per) * size_t(sub), NodeRec{0u, 0u});
+            std::vector<int32_t> most(static_cast<size_t>(per), 0);
+            const NodeRec zero_leaf{zero_record_value(plan, vec), (uint32_t(plan.zero_rec) / 8u) << shift};
+            for (int32_t w = 0; w < W; w++) {
+                const uint32_t base = uint32_t(plan.xs_bytes / 8) + uint32_t(w * sub); // sub-slot in LDS
+                for (size_t q = 0; q < runs[size_t(w)].size(); q++) {
+                    const int32_t g0 = runs[size_t(w)][q].first, ng = runs[size_t(w)][q].second;
+                    NodeRec *img = p.packets.data() + (size_t(w) * size_t(per) + q) * size_t(sub);
+                    p.pk_max_groups = std::max(p.pk_max_groups, ng);
+                    most[q] = std::max(most[q], ng);
+                    int32_t complete = -2; // -2: no tree yet
+                    for (int32_t j = 0; j < ng; j++) {
+                        for (int32_t i = 0; i < K; i++) {
+                            const int32_t t = (g0 + j * W) * K + i;
+                            if (t >= n_trees)
+                                continue;
+                            const int32_t d = int32_t(p.tree_depth[size_t(t)]);
+                            const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
+                            const bool full = nn == (int64_t(2) << d) - 1;
+                            complete = (complete == -2 || complete == d) && full ? d : -1;
+                        }
+                    }
+                    img[0] = NodeRec{uint32_t(ng), uint32_t(complete)};
+                    img[1] = NodeRec{uint32_t(g0), 0u};
+                    const int32_t table = kPacketHeaderRecs + ng * K;
+                    uint16_t *first_rec = reinterpret_cast<uint16_t *>(img + table);
+                    int32_t pos = table + (ng * K + 3) / 4;
+                    for (int32_t j = 0; j < ng; j++) {
+                        for (int32_t i = 0; i < K; i++) {
+                            const int32_t t = (g0 + j * W) * K + i;
+                            NodeRec root = zero_leaf;
+                            if (t < n_trees) {
+                                const uint32_t first = p.tree_node_off[size_t(t)];
+                                const uint32_t nn = p.tree_node_off[size_t(t) + 1] - first;
+                                const uint32_t tree_rec = base + uint32_t(pos);
+                                first_rec[j * K + i] = uint16_t(tree_rec);
+                                for (uint32_t n = 0; n < nn; n++) {
+                                    NodeRec r = p.nodes[first + n];
+                                    r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                                    img[pos + int32_t(n)] = r;
+                                }
+                                root = img[pos];
+                                pos += int32_t(nn);
+                            }
+                            img[kPacketHeaderRecs + j * K + i] = root;
+                        }
+                    }
+                }
+            }
+            for (int32_t m : most)
+                p.pk_total_rounds += m;
+        }
+    }
+
     if (plan.lds_bytes == kLdsPerCu / 2) {
-        const int64_t off = (int64_t(plan.xs_bytes) + int64_t(p.level_slot_recs[0]) * 8 + 15) & ~int64_t(15);
+        const int64_t used = p.pk_recs > 0 ? int64_t(kPacketWalkers) * p.pk_recs : int64_t(p.level_slot_recs[0]);
+        const int64_t off = (int64_t(plan.xs_bytes) + used * 8 + 15) & ~int64_t(15);
         const int64_t mask_bytes = (int64_t(n_cols) + 31) / 32 * plan.docs_per_block * 4;
         if (off + mask_bytes <= plan.zero_rec)
             p.usage_slot_off = int32_t(off);

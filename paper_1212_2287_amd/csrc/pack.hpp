@@ -64,6 +64,21 @@ constexpr int kMaxTileTrees = 1024;
 // kernel locates tile t without a table.
 constexpr int kHeaderFixedWords = 4;
 
+// Walker packets. In two-workgroup plans of 64-document blocks each of the 16 walkers (one wave
+// each) streams its own groups of K trees (g = w, w + 16, w + 32, ...) through a sub-slot of the
+// tile slot of its own, so walkers never wait for one another between tiles. A packet is a run
+// of consecutive groups of one walker that fits the sub-slot, laid out as
+//   record 0   number of groups n in the packet; their common complete depth d, else -1
+//   record 1   index of the packet's first group (its later groups follow at a stride of 16)
+//   records 2.. the K root copies of each group (the zero record for slots past the last tree)
+//   then       the LDS record index of each tree's first record, 16 bits each (for leaf ids),
+//              padded to a whole record
+//   then       the trees' records, child links as absolute LDS record indices of the sub-slot.
+// A walker loads its next packet into registers while it walks the current one. Plans in which
+// one group outgrows a sub-slot keep the shared tiles.
+constexpr int kPacketHeaderRecs = 2;
+constexpr int kPacketWalkers = 16;
+
 // Launch plan fixed at create time from the model's feature range.
 struct LdsPlan {
     int32_t docs_per_block; // documents a workgroup stages (power of two, 8..64)
@@ -134,8 +149,17 @@ struct Packed {
     int32_t level_max_rounds[kTileLevels] = {};
     int64_t total_rounds = 0;
     // feature trace of a two-workgroup plan: LDS byte address of the bitmasks in the tile slot
-    // past the largest tiling-0 image, or -1 when they do not fit before the zero record
+    // past the largest tiling-0 image (past the walkers' sub-slots with packets), or -1 when
+    // they do not fit before the zero record
     int32_t usage_slot_off = -1;
+    // Walker packets (two-workgroup plans of 64-document blocks, see kPacketHeaderRecs): walker
+    // w's packet q is packets[(w * pk_per_walker + q) * pk_recs, ...), linked for its sub-slot
+    // at LDS record xs_bytes / 8 + w * pk_recs. pk_recs == 0: the plan walks shared tiles.
+    int32_t pk_recs = 0;
+    int32_t pk_per_walker = 0;
+    int32_t pk_max_groups = 0;   // groups in the fullest packet
+    int64_t pk_total_rounds = 0; // sum over packet indices of the most groups any walker has there
+    std::vector<NodeRec> packets;
     // vector-valued leaves (n_outputs > 1): a leaf's threshold slot holds 2 + its packed node
     // index instead of a value, and row (thr - 1) of leaf_vec holds its n_outputs values,
     // padded to vec_stride (a multiple of 4) floats; row 0 is zero (the all-zero record's row)

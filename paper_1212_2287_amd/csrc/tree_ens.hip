@@ -61,6 +61,8 @@ constexpr int kNumCus = 256;
 constexpr int kXcds = 8; // accelerator complex dies, each with its own L2
 // s_waitcnt immediate for gfx9: vmcnt(0), expcnt and lgkmcnt left at their maxima (no wait)
 constexpr int kWaitVmcnt0 = 0x0F70;
+// the same with lgkmcnt(0) (LDS and scalar memory) and vmcnt, expcnt at their maxima
+constexpr int kWaitLgkmcnt0 = 0xC07F;
 #ifndef TREE_ENS_PREFETCH_DEPTH
 #define TREE_ENS_PREFETCH_DEPTH 2 // tiles in flight with one workgroup per CU
 #endif
@@ -137,7 +139,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
              const int32_t *__restrict__ tree_orig, int32_t n_trees,
              uint32_t *__restrict__ masks, int32_t mask_words, int32_t usage_off,
              const float4 *__restrict__ leaf_vec, int32_t vec_stride4, int32_t n_out,
-             int32_t chunk, double out_scale) {
+             int32_t chunk, double out_scale, int32_t pk_recs) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
@@ -240,10 +242,26 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         for (int j = 0; j < kWin; ++j)
             dst[j] = src[(j < chunks ? j : 0) * kThreads];
     };
+    // Walker packets (pk_recs > 0, two-workgroup plans of 64-document blocks): walker w's packet
+    // q is images[(w * n_tiles + q) * pk_recs, ...); each lane loads pk_recs / 64 records of it.
+    const int pk_lane = pk_recs / 64;
+    const uint2 *pk_src = images + (int64_t(walker) * n_tiles) * pk_recs + dl;
+    auto fetch_packet = [&](int q) {
+        const uint2 *src = pk_src + int64_t(q) * pk_recs;
+#pragma unroll
+        for (int j = 0; j < kPre; ++j)
+            if (j < pk_lane)
+                pa[j] = src[j * 64];
+    };
     if constexpr (HALF) {
-        cur_recs = t_lo < t_hi ? int(tile_recs[t_lo]) : 0;
-        if (t_lo < t_hi)
-            fetch(t_lo, cur_recs);
+        if (pk_recs > 0) {
+            if (t_lo < t_hi)
+                fetch_packet(t_lo);
+        } else {
+            cur_recs = t_lo < t_hi ? int(tile_recs[t_lo]) : 0;
+            if (t_lo < t_hi)
+                fetch(t_lo, cur_recs);
+        }
     } else {
         if (t_lo < t_hi) {
 #pragma unroll
@@ -322,146 +340,195 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
 
     double acc = 0.0;
     double accv[kVecPerLaunch] = {0.0, 0.0, 0.0, 0.0};
-    // Walk the tile image in the LDS slot.
+    // Walk one group of K trees whose K root copies are the records at rc. tree_of(i) gives the
+    // packed index of the tree in slot i (-1: an idle slot) and, for leaf ids, the LDS record
+    // index of that tree's first record.
+    auto walk_group = [&](const unsigned char *rc, auto complete_tag, int complete_depth, auto &&tree_of) {
+        constexpr bool kComplete = decltype(complete_tag)::value;
+        // the K root records (broadcast reads)
+        uint64_t nd[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            nd[i] = read_record(rc + 8 * i);
+        // One predicated step: feature addresses fa from the records, read the features
+        // xv, compare, child link + bit (the right child follows the left one), read
+        // that record.
+        uint32_t fa[K];
+        std::conditional_t<CODED, uint32_t, float> xv[K];
+        auto read_features = [&]() {
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                fa[i] = and_or(rec_w(nd[i]), col_mask, lane_off);
+                if constexpr (CODED)
+                    xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
+                else
+                    xv[i] = *reinterpret_cast<const float *>(lds + fa[i]);
+                if constexpr (USAGE) {
+                    // column c > 0 holds feature c - 1; column 0 is a leaf's (no
+                    // comparison, nothing recorded)
+                    const uint32_t col = fa[i] >> kColShift;
+                    if (col > 0u)
+                        atomicOr(&umask[((col - 1u) >> 5) * DL + dl], 1u << ((col - 1u) & 31u));
+                }
+            }
+        };
+        auto descend = [&]() {
+            uint32_t addr[K];
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                uint32_t child;
+                const uint32_t w = rec_w(nd[i]), thr = rec_thr(nd[i]);
+                if constexpr (CODED) {
+                    if constexpr (NARROW)
+                        child = narrow_child_coded(w, xv[i], thr);
+                    else
+                        child = (w >> kShift) + (xv[i] >= thr ? 1u : 0u);
+                } else {
+                    if constexpr (NARROW)
+                        child = narrow_child(w, xv[i], __uint_as_float(thr));
+                    else
+                        child = (w >> kShift) + (xv[i] >= __uint_as_float(thr) ? 1u : 0u);
+                }
+                addr[i] = child * 8u;
+            }
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                nd[i] = read_record(lds + addr[i]);
+        };
+        if constexpr (kComplete) {
+            // every path has the same length: no leaf test needed
+            for (int s = 0; s < complete_depth; ++s) {
+                read_features();
+                descend();
+            }
+        } else {
+            // Every lane steps until all lanes of the wave sit on leaves (a leaf's
+            // feature address is the NaN column, below kLeafCol); the record that shows
+            // a lane is at a leaf holds the leaf's value. Every path of a validated tree
+            // reaches a leaf and leaves link to themselves, so the exit is always taken.
+            // The next feature reads are issued before the test, so the test overlaps
+            // their latency (after the last step they read the NaN column: harmless).
+            auto any_internal = [&]() {
+                bool internal = false;
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    internal |= fa[i] >= kLeafCol;
+                return __builtin_amdgcn_ballot_w64(internal) != 0;
+            };
+            // The first step is taken untested: a group whose K roots are all leaves
+            // (single-leaf trees, idle slots) is rare, and a leaf absorbs the extra step.
+            read_features();
+            do {
+                descend();
+                read_features();
+            } while (any_internal());
+            // The exit path "uses" the last feature reads, so the compiler cannot sink
+            // them below the test (where they would serialise with it again).
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                asm volatile("" ::"v"(xv[i]));
+        }
+        if constexpr (LEAVES) {
+            const int64_t doc = doc0 + dl;
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                // a leaf's link is its own LDS record index; minus that of its tree's
+                // first record, it is the leaf's position in the tree
+                const int2 tr = tree_of(i);
+                if (tr.x >= 0 && doc < n_docs) {
+                    const int gt = tr.x;
+                    const uint32_t self = (rec_w(nd[i]) >> kShift) - uint32_t(tr.y);
+                    leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
+                }
+            }
+        } else if constexpr (VEC) {
+            // a leaf's threshold slot holds its table row + 1 (idle slots: row 0, zeros);
+            // each component added to its double accumulator in tree order
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                const float4 v = leaf_vec[int64_t(rec_thr(nd[i]) - 1u) * vec_stride4 + chunk];
+                accv[0] += double(v.x);
+                accv[1] += double(v.y);
+                accv[2] += double(v.z);
+                accv[3] += double(v.w);
+            }
+        } else if constexpr (!USAGE) {
+            // the K leaf values, each added to the double accumulator in tree order (a
+            // float sum of the group first can miss the tolerance when a score cancels
+            // near zero); idle slots hold the zero record
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                acc += double(__uint_as_float(rec_thr(nd[i])));
+        }
+    };
+    // Walk the tile image in the LDS slot: walker w takes groups w, w + n_walkers, ... of K
+    // consecutive trees (the packer sizes tiles to a multiple of n_walkers * K trees where it
+    // can, and pads the header's root copies to a multiple of K with the zero record).
     auto walk_tile = [&]() {
         const uint4 h = *reinterpret_cast<const uint4 *>(hdr);
         const int ntr = __builtin_amdgcn_readfirstlane(int(h.x));
         const int complete_depth = __builtin_amdgcn_readfirstlane(int(h.y));
         const int tree_begin = __builtin_amdgcn_readfirstlane(int(h.z));
-        // Walker w takes groups w, w + n_walkers, ... of K consecutive trees (the packer sizes
-        // tiles to a multiple of n_walkers * K trees where it can, and pads the header's root
-        // copies to a multiple of K with the zero record).
         const int n_groups = (ntr + K - 1) / K;
         // records of the tile's trees start after the fixed header words and the root copies
         const uint32_t rec0 = uint32_t(xs_bytes) / 8u + uint32_t(treeens::kHeaderFixedWords / 2 + n_groups * K);
-        auto walk = [&](auto complete_tag) {
-            constexpr bool kComplete = decltype(complete_tag)::value;
-            for (int g = walker; g < n_groups; g += n_walkers) {
-                // the K root records, copied into the header (broadcast reads)
-                uint64_t nd[K];
-                const unsigned char *rc = lds + xs_bytes + 8 * (treeens::kHeaderFixedWords / 2 + g * K);
-#pragma unroll
-                for (int i = 0; i < K; ++i)
-                    nd[i] = read_record(rc + 8 * i);
-                // One predicated step: feature addresses fa from the records, read the features
-                // xv, compare, child link + bit (the right child follows the left one), read
-                // that record.
-                uint32_t fa[K];
-                std::conditional_t<CODED, uint32_t, float> xv[K];
-                auto read_features = [&]() {
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        fa[i] = and_or(rec_w(nd[i]), col_mask, lane_off);
-                        if constexpr (CODED)
-                            xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
-                        else
-                            xv[i] = *reinterpret_cast<const float *>(lds + fa[i]);
-                        if constexpr (USAGE) {
-                            // column c > 0 holds feature c - 1; column 0 is a leaf's (no
-                            // comparison, nothing recorded)
-                            const uint32_t col = fa[i] >> kColShift;
-                            if (col > 0u)
-                                atomicOr(&umask[((col - 1u) >> 5) * DL + dl], 1u << ((col - 1u) & 31u));
-                        }
-                    }
-                };
-                auto descend = [&]() {
-                    uint32_t addr[K];
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        uint32_t child;
-                        const uint32_t w = rec_w(nd[i]), thr = rec_thr(nd[i]);
-                        if constexpr (CODED) {
-                            if constexpr (NARROW)
-                                child = narrow_child_coded(w, xv[i], thr);
-                            else
-                                child = (w >> kShift) + (xv[i] >= thr ? 1u : 0u);
-                        } else {
-                            if constexpr (NARROW)
-                                child = narrow_child(w, xv[i], __uint_as_float(thr));
-                            else
-                                child = (w >> kShift) + (xv[i] >= __uint_as_float(thr) ? 1u : 0u);
-                        }
-                        addr[i] = child * 8u;
-                    }
-#pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        nd[i] = read_record(lds + addr[i]);
-                };
-                if constexpr (kComplete) {
-                    // every path has the same length: no leaf test needed
-                    for (int s = 0; s < complete_depth; ++s) {
-                        read_features();
-                        descend();
-                    }
-                } else {
-                    // Every lane steps until all lanes of the wave sit on leaves (a leaf's
-                    // feature address is the NaN column, below kLeafCol); the record that shows
-                    // a lane is at a leaf holds the leaf's value. Every path of a validated tree
-                    // reaches a leaf and leaves link to themselves, so the exit is always taken.
-                    // The next feature reads are issued before the test, so the test overlaps
-                    // their latency (after the last step they read the NaN column: harmless).
-                    auto any_internal = [&]() {
-                        bool internal = false;
-#pragma unroll
-                        for (int i = 0; i < K; ++i)
-                            internal |= fa[i] >= kLeafCol;
-                        return __builtin_amdgcn_ballot_w64(internal) != 0;
-                    };
-                    // The first step is taken untested: a group whose K roots are all leaves
-                    // (single-leaf trees, idle slots) is rare, and a leaf absorbs the extra step.
-                    read_features();
-                    do {
-                        descend();
-                        read_features();
-                    } while (any_internal());
-                    // The exit path "uses" the last feature reads, so the compiler cannot sink
-                    // them below the test (where they would serialise with it again).
-#pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        asm volatile("" ::"v"(xv[i]));
-                }
-                if constexpr (LEAVES) {
-                    const int64_t doc = doc0 + dl;
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        // a leaf's link is its own LDS record index; minus that of its tree's
-                        // root, it is the leaf's position in the tree
-                        const int t = g * K + i;
-                        if (t < ntr && doc < n_docs) {
-                            const int gt = tree_begin + t;
-                            const uint32_t root = rec0 + tree_node_off[gt] - tree_node_off[tree_begin];
-                            const uint32_t self = (rec_w(nd[i]) >> kShift) - root;
-                            leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
-                        }
-                    }
-                } else if constexpr (VEC) {
-                    // a leaf's threshold slot holds its table row + 1 (idle slots: row 0, zeros);
-                    // each component added to its double accumulator in tree order
-#pragma unroll
-                    for (int i = 0; i < K; ++i) {
-                        const float4 v = leaf_vec[int64_t(rec_thr(nd[i]) - 1u) * vec_stride4 + chunk];
-                        accv[0] += double(v.x);
-                        accv[1] += double(v.y);
-                        accv[2] += double(v.z);
-                        accv[3] += double(v.w);
-                    }
-                } else if constexpr (!USAGE) {
-                    // the K leaf values, each added to the double accumulator in tree order (a
-                    // float sum of the group first can miss the tolerance when a score cancels
-                    // near zero); idle slots hold the zero record
-#pragma unroll
-                    for (int i = 0; i < K; ++i)
-                        acc += double(__uint_as_float(rec_thr(nd[i])));
-                }
-            }
-        };
-        if (complete_depth >= 0)
-            walk(std::true_type{});
-        else
-            walk(std::false_type{});
+        for (int g = walker; g < n_groups; g += n_walkers) {
+            const unsigned char *rc = lds + xs_bytes + 8 * (treeens::kHeaderFixedWords / 2 + g * K);
+            auto tree_of = [&](int i) {
+                const int t = g * K + i;
+                return t < ntr ? make_int2(tree_begin + t,
+                                           int(rec0 + tree_node_off[tree_begin + t] - tree_node_off[tree_begin]))
+                               : make_int2(-1, 0);
+            };
+            if (complete_depth >= 0)
+                walk_group(rc, std::true_type{}, complete_depth, tree_of);
+            else
+                walk_group(rc, std::false_type{}, complete_depth, tree_of);
+        }
+    };
+    // Walk one of this walker's packets in its sub-slot, which starts at LDS record base: its
+    // groups are first_group, first_group + n_walkers, ...
+    auto walk_packet = [&](uint32_t base) {
+        const uint2 h0 = *reinterpret_cast<const uint2 *>(lds + 8 * base);
+        const uint2 h1 = *reinterpret_cast<const uint2 *>(lds + 8 * (base + 1));
+        const int ng = __builtin_amdgcn_readfirstlane(int(h0.x));
+        const int complete_depth = __builtin_amdgcn_readfirstlane(int(h0.y));
+        const int first_group = __builtin_amdgcn_readfirstlane(int(h1.x));
+        const uint16_t *first_rec =
+            reinterpret_cast<const uint16_t *>(lds + 8 * (base + treeens::kPacketHeaderRecs + ng * K));
+        for (int j = 0; j < ng; ++j) {
+            const unsigned char *rc = lds + 8 * (base + treeens::kPacketHeaderRecs + j * K);
+            auto tree_of = [&](int i) {
+                const int gt = (first_group + j * n_walkers) * K + i;
+                return gt < n_trees ? make_int2(gt, int(first_rec[j * K + i])) : make_int2(-1, 0);
+            };
+            if (complete_depth >= 0)
+                walk_group(rc, std::true_type{}, complete_depth, tree_of);
+            else
+                walk_group(rc, std::false_type{}, complete_depth, tree_of);
+        }
     };
     if constexpr (HALF) {
+        if (pk_recs > 0) {
+            // Each walker streams its own packets through its own sub-slot: no barrier between
+            // packets, so a walker never waits for the slowest one of a tile.
+            const uint32_t my_base = uint32_t(xs_bytes) / 8u + uint32_t(walker * pk_recs);
+            uint2 *my = reinterpret_cast<uint2 *>(lds) + my_base;
+            __syncthreads(); // the document tile and the zero record are written
+            for (int q = t_lo; q < t_hi; ++q) {
+                // this packet's records (and, before the first, the document rows) have landed
+                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+#pragma unroll
+                for (int j = 0; j < kPre; ++j)
+                    if (j < pk_lane)
+                        my[dl + j * 64] = pa[j];
+                // the wave's own writes complete before it reads the packet back
+                __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
+                if (q + 1 < t_hi)
+                    fetch_packet(q + 1);
+                walk_packet(my_base);
+            }
+        } else
         for (int ti = t_lo; ti < t_hi; ++ti) {
             __syncthreads(); // the previous tile is fully walked (and the document tile written)
             // All outstanding global loads (this tile's records, and the document rows before
@@ -678,7 +745,7 @@ using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *,
                          const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
                          float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
                          int32_t, uint32_t *, int32_t, int32_t, const float4 *, int32_t,
-                         int32_t, int32_t, double);
+                         int32_t, int32_t, double, int32_t);
 
 template <int DL, bool HALF, bool NARROW, bool CODED, int MODE>
 ScoreFn pick_k(int k) {
@@ -748,6 +815,13 @@ struct tree_ens {
     int32_t level_slot_recs[treeens::kTileLevels] = {};
     uint2 *d_images = nullptr;      // tile images of every tiling
     uint32_t *d_tile_recs = nullptr; // records of each tile image
+    // walker packets (two-workgroup plans of 64-document blocks): records per sub-slot (0: the
+    // plan walks shared tiles), packets per walker, the planner's rounds, and the images
+    int32_t pk_recs = 0;
+    int32_t pk_per_walker = 0;
+    int32_t pk_max_groups = 0;
+    int64_t pk_total_rounds = 0;
+    uint2 *d_packets = nullptr;
     // leaf-id output: packed tree -> input tree, packed node -> input node id
     uint32_t *d_tree_node_off = nullptr;
     int32_t *d_tree_orig = nullptr;
@@ -790,6 +864,7 @@ namespace {
 
 void free_device(tree_ens *h) {
     (void)hipFree(h->d_images);
+    (void)hipFree(h->d_packets);
     (void)hipFree(h->d_tile_recs);
     (void)hipFree(h->d_tree_node_off);
     (void)hipFree(h->d_tree_orig);
@@ -883,18 +958,26 @@ LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
     constexpr double kItemCost = 0.2;    // staging, prologue and restaging of one workgroup (measured)
     constexpr double kReduceCost = 0.05; // the second kernel
     constexpr double kPerWorkgroup = 1e-6;
-    constexpr double kTileRounds = 0.5;  // switching tiles, in walker rounds
+    constexpr double kTileRounds = 0.5;    // switching tiles, in walker rounds
+    constexpr double kPacketRounds = 0.1;  // switching packets (no barrier), in walker rounds
     const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
     const int64_t slots = int64_t(kNumCus) * wg_per_cu;
-    const double total = double(std::max<int64_t>(h->total_rounds, 1)) +
-                         kTileRounds * double(h->level_begin[1] - h->level_begin[0]);
+    // walker packets: one level, each walker's packets in place of the tiles
+    const bool pk = h->pk_recs > 0;
+    const int n_levels = pk ? 1 : treeens::kTileLevels;
+    auto tiles_at = [&](int level) {
+        return pk ? h->pk_per_walker : h->level_begin[level + 1] - h->level_begin[level];
+    };
+    auto rounds_at = [&](int level) { return pk ? h->pk_max_groups : h->level_max_rounds[level]; };
+    const double switch_rounds = pk ? kPacketRounds : kTileRounds;
+    const double total = double(std::max<int64_t>(pk ? h->pk_total_rounds : h->total_rounds, 1)) +
+                         switch_rounds * double(tiles_at(0));
     double best = 1e300;
     LaunchShape pick;
     auto consider = [&](int level, int64_t head, int sp) {
-        const int nt = h->level_begin[level + 1] - h->level_begin[level];
+        const int nt = tiles_at(level);
         const int64_t tail = n_blocks - head;
-        const double share =
-            double((nt + sp - 1) / sp) * (h->level_max_rounds[level] + kTileRounds) / total;
+        const double share = double((nt + sp - 1) / sp) * (rounds_at(level) + switch_rounds) / total;
         const double cost = double(head / slots) * (1.0 + kItemCost) +
                             double((tail * sp + slots - 1) / slots) * (share + kItemCost) +
                             (sp > 1 ? kReduceCost : 0.0) + kPerWorkgroup * double(head + tail * sp);
@@ -903,19 +986,19 @@ LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
             pick = LaunchShape{level, head, sp};
         }
     };
-    for (int k = 0; k < treeens::kTileLevels; ++k) {
-        const int nt = h->level_begin[k + 1] - h->level_begin[k];
+    for (int k = 0; k < n_levels; ++k) {
+        const int nt = tiles_at(k);
         for (int sp = 1; sp <= std::min(nt, 1024); ++sp)
             consider(k, 0, sp);
     }
     const int64_t rem = n_blocks % slots;
     if (n_blocks > slots && rem > 0) {
-        const int nt = h->level_begin[1] - h->level_begin[0];
+        const int nt = tiles_at(0);
         for (int sp = 2; sp <= std::min<int64_t>(nt, slots / rem); ++sp)
             consider(0, n_blocks - rem, sp);
     }
 #ifdef TREE_ENS_FORCE_SPLITS // measurement builds only
-    pick = LaunchShape{0, 0, std::min(TREE_ENS_FORCE_SPLITS, h->level_begin[1] - h->level_begin[0])};
+    pick = LaunchShape{0, 0, std::min(TREE_ENS_FORCE_SPLITS, tiles_at(0))};
 #endif
     return pick;
 }
@@ -1037,9 +1120,12 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                 return hip_fail(e, "hipMallocAsync(partials)");
         }
     }
-    const uint2 *images = h->d_images + h->level_image_off[level];
-    const uint32_t *tile_recs = h->d_tile_recs + h->level_begin[level];
-    const int n_tiles = h->level_begin[level + 1] - h->level_begin[level];
+    // walker packets (pk_recs > 0) stand in for the tiles: n_tiles is then packets per walker
+    const bool pk = h->pk_recs > 0;
+    const uint2 *images = pk ? h->d_packets : h->d_images + h->level_image_off[level];
+    const uint32_t *tile_recs = h->d_tile_recs + (pk ? 0 : h->level_begin[level]);
+    const int n_tiles = pk ? h->pk_per_walker : h->level_begin[level + 1] - h->level_begin[level];
+    const int32_t slot_recs = pk ? h->pk_recs : h->level_slot_recs[level];
     (void)hipGetLastError();
     // coded models: one pass turns the float features into 16-bit threshold codes
     const void *docs = X;
@@ -1070,12 +1156,12 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const int n_out = MODE == kModeVector ? h->n_outputs : 1;
     for (int chunk = 0; chunk < n_chunks && e == hipSuccess; ++chunk) {
         hipLaunchKernelGGL(fn, dim3(unsigned(n_wgs)), dim3(kThreads), 0, stream, docs, n_docs,
-                           row_stride, h->n_cols, images, h->level_slot_recs[level], tile_recs,
+                           row_stride, h->n_cols, images, slot_recs, tile_recs,
                            n_tiles, int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec,
                            partials, scores, leaf_ids, h->d_orig_id, h->d_tree_node_off,
                            h->d_tree_orig, h->n_trees, masks, mask_words, usage_off,
                            reinterpret_cast<const float4 *>(h->d_leaf_vec), h->vec_stride / 4, n_out,
-                           chunk, scale);
+                           chunk, scale, h->pk_recs);
         e = hipGetLastError();
         if (e == hipSuccess && partials) {
             // the tail blocks' entries, in [doc][component] order
@@ -1180,6 +1266,10 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
     std::memcpy(h->level_max_rounds, p.level_max_rounds, sizeof h->level_max_rounds);
     h->total_rounds = p.total_rounds;
     h->usage_slot_off = p.usage_slot_off;
+    h->pk_recs = p.pk_recs;
+    h->pk_per_walker = p.pk_per_walker;
+    h->pk_max_groups = p.pk_max_groups;
+    h->pk_total_rounds = p.pk_total_rounds;
     std::memcpy(h->level_slot_recs, p.level_slot_recs, sizeof h->level_slot_recs);
     std::vector<uint2> images(p.images.size());
     if (!p.images.empty())
@@ -1188,6 +1278,11 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
         e = upload(&h->d_images, images);
     if (e == hipSuccess)
         e = upload(&h->d_tile_recs, p.tile_recs);
+    if (e == hipSuccess && p.pk_recs > 0) {
+        std::vector<uint2> packets(p.packets.size());
+        std::memcpy(packets.data(), p.packets.data(), p.packets.size() * sizeof(NodeRec));
+        e = upload(&h->d_packets, packets);
+    }
     if (e == hipSuccess)
         e = upload(&h->d_tree_node_off, p.tree_node_off);
     if (e == hipSuccess)

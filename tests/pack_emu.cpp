@@ -11,6 +11,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -75,8 +76,9 @@ const char *emu_message(void) { return g_msg.c_str(); }
 
 // Walk all documents through tiling `level`. Outputs leaf ids [n_docs][n_trees] (input node ids)
 // and fp64 scores [n_docs][n_outputs] (vector-valued leaves read through the leaf-vector table).
-// plan_out (8 ints): docs per block, trees per lane, record format, coded, tiles at tiling 0,
-// LDS bytes, tile slot bytes, records of the largest tiling-0 image. Returns 0, or 1 with a message naming the first violated
+// plan_out (9 ints): docs per block, trees per lane, record format, coded, tiles at tiling 0,
+// LDS bytes, tile slot bytes, records of the largest tiling-0 image, walker sub-slot records
+// (0: shared tiles). Returns 0, or 1 with a message naming the first violated
 // invariant, or a negative packer status.
 int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
              const float *threshold, const int32_t *left, const int32_t *right, const float *value,
@@ -100,6 +102,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         plan_out[5] = pl.lds_bytes;
         plan_out[6] = pl.tile_bytes;
         plan_out[7] = p.level_slot_recs[0];
+        plan_out[8] = p.pk_recs;
     }
     const int DL = pl.docs_per_block, K = pl.interleave, E = pl.elem_bytes;
     const int shift = pl.narrow ? 16 : treeens::kWideChildShift;
@@ -123,13 +126,16 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         // zero record
         if (p.usage_slot_off >= 0) {
             const int64_t mask_bytes = int64_t(p.n_cols + 31) / 32 * DL * 4;
+            // with walker packets the bitmasks follow the sub-slots, else the tiling-0 images
+            const int64_t used = p.pk_recs > 0 ? int64_t(treeens::kPacketWalkers) * p.pk_recs
+                                               : int64_t(p.level_slot_recs[0]);
             if (pl.lds_bytes != treeens::kLdsPerCu / 2 || p.usage_slot_off % 16 ||
-                p.usage_slot_off < int64_t(xs) + int64_t(p.level_slot_recs[0]) * 8 ||
-                p.usage_slot_off + mask_bytes > int64_t(zero))
+                p.usage_slot_off < int64_t(xs) + used * 8 || p.usage_slot_off + mask_bytes > int64_t(zero))
                 return bad("in-slot feature bitmasks overlap a tile image or the zero record");
-            for (int32_t t = p.level_begin[0]; t < p.level_begin[1]; t++)
-                if (int64_t(xs) + int64_t(p.tile_recs[size_t(t)]) * 8 > p.usage_slot_off)
-                    return bad("a tiling-0 image reaches the in-slot feature bitmasks");
+            if (p.pk_recs == 0)
+                for (int32_t t = p.level_begin[0]; t < p.level_begin[1]; t++)
+                    if (int64_t(xs) + int64_t(p.tile_recs[size_t(t)]) * 8 > p.usage_slot_off)
+                        return bad("a tiling-0 image reaches the in-slot feature bitmasks");
         }
     }
     std::vector<uint8_t> lds(size_t(pl.lds_bytes), 0);
@@ -154,6 +160,16 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
             return bad("the last tile's window reads past the images");
     } else if (slot > int64_t(treeens::kPrefetchHalf) * 1024) {
         return bad("tile image exceeds the prefetch registers");
+    }
+    if (p.pk_recs > 0) {
+        // walker packets: whole 64-lane loads that fit the prefetch registers, sub-slots inside
+        // the tile slot, one packet stream per walker
+        if (pl.lds_bytes != treeens::kLdsPerCu / 2 || DL != 64 || p.pk_recs % 64 ||
+            p.pk_recs / 64 > treeens::kPrefetchHalf ||
+            int64_t(treeens::kPacketWalkers) * p.pk_recs * 8 > pl.tile_bytes)
+            return bad("walker sub-slots do not fit the plan");
+        if (p.packets.size() != size_t(treeens::kPacketWalkers) * size_t(p.pk_per_walker) * size_t(p.pk_recs))
+            return bad("packet buffer has the wrong size");
     }
     std::vector<int32_t> seen(size_t(n_trees), 0);
     for (int64_t i = 0; i < n_docs * n_trees; i++)
@@ -186,6 +202,123 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         const treeens::NodeRec z{treeens::zero_record_value(pl, vec), (zero / 8u) << shift};
         std::memcpy(lds.data() + zero, &z, 8);
 
+        // Walk every document of the block through packed tree gt whose root copy is at
+        // root_copy (LDS byte address) and whose first record is LDS record root_idx.
+        auto walk_tree = [&](int gt, uint32_t root_copy, uint32_t root_idx, int complete,
+                             const std::function<bool(uint32_t)> &valid) -> int {
+            const int64_t tree_n = int64_t(p.tree_node_off[size_t(gt) + 1] - p.tree_node_off[size_t(gt)]);
+            for (int dl = 0; dl < DL && doc0 + dl < n_docs; dl++) {
+                const int64_t doc = doc0 + dl;
+                treeens::NodeRec r = rec_at(root_copy);
+                int steps = 0;
+                for (;;) {
+                    const uint32_t fa = (r.w & mask) | uint32_t(dl * E);
+                    if (fa != (r.w & mask) + uint32_t(dl * E))
+                        return bad("column offset and lane offset overlap");
+                    if (fa + uint32_t(E) > xs)
+                        return bad("feature address outside the document tile");
+                    if (complete >= 0 ? steps == complete : fa < leaf_col)
+                        break;
+                    bool right_side;
+                    if (E == 4) {
+                        float x;
+                        std::memcpy(&x, lds.data() + fa, 4);
+                        right_side = x >= as_float(r.thr_bits);
+                    } else {
+                        uint16_t x;
+                        std::memcpy(&x, lds.data() + fa, 2);
+                        right_side = uint32_t(x) >= r.thr_bits;
+                    }
+                    const uint32_t a = ((r.w >> shift) + (right_side ? 1u : 0u)) * 8u;
+                    if (!valid(a))
+                        return bad("child address outside the tile's records");
+                    r = rec_at(a);
+                    if (++steps > p.max_depth + 1)
+                        return bad("walk longer than the deepest tree");
+                }
+                if ((r.w & mask) != 0)
+                    return bad("walk ended on an internal node");
+                {
+                    // one more step from a leaf must come back to the same record
+                    bool right_side;
+                    if (E == 4) {
+                        float x;
+                        std::memcpy(&x, lds.data() + (r.w & mask) + dl * E, 4);
+                        right_side = x >= as_float(r.thr_bits);
+                    } else {
+                        uint16_t x;
+                        std::memcpy(&x, lds.data() + (r.w & mask) + dl * E, 2);
+                        right_side = uint32_t(x) >= r.thr_bits;
+                    }
+                    const uint32_t a = ((r.w >> shift) + (right_side ? 1u : 0u)) * 8u;
+                    if (!valid(a) || std::memcmp(lds.data() + a, &r, 8) != 0)
+                        return bad("a leaf does not absorb a further step");
+                }
+                const int64_t self = int64_t(r.w >> shift) - int64_t(root_idx);
+                if (self < 0 || self >= tree_n)
+                    return bad("leaf outside its tree");
+                const int32_t orig_tree = p.tree_orig[size_t(gt)];
+                leaf_ids[doc * n_trees + orig_tree] = p.orig_id[p.tree_node_off[size_t(gt)] + size_t(self)];
+                if (vec) {
+                    const int64_t row = int64_t(r.thr_bits) - 1;
+                    if (row < 1 || row > int64_t(p.nodes.size()))
+                        return bad("leaf names a row outside the leaf-vector table");
+                    for (int c = 0; c < n_outputs; c++)
+                        scores[doc * n_outputs + c] +=
+                            double(p.leaf_vec[size_t(row) * size_t(p.vec_stride) + size_t(c)]);
+                } else {
+                    scores[doc] += double(as_float(r.thr_bits));
+                }
+            }
+            seen[size_t(p.tree_orig[size_t(gt)])]++;
+            return 0;
+        };
+
+        if (p.pk_recs > 0) {
+            // each walker copies its packets, in order, into its own sub-slot and walks them
+            constexpr int32_t W = treeens::kPacketWalkers;
+            const int32_t sub = p.pk_recs, per = p.pk_per_walker;
+            for (int32_t w = 0; w < W; w++) {
+                const uint32_t lo_b = xs + uint32_t(w * sub) * 8u, hi_b = lo_b + uint32_t(sub) * 8u;
+                for (int32_t q = 0; q < per; q++) {
+                    const treeens::NodeRec *img = p.packets.data() + (size_t(w) * size_t(per) + size_t(q)) * size_t(sub);
+                    std::memcpy(lds.data() + lo_b, img, size_t(sub) * 8);
+                    const treeens::NodeRec h0 = rec_at(lo_b), h1 = rec_at(lo_b + 8);
+                    const int ng = int(h0.thr_bits), complete = int32_t(h0.w), g0 = int(h1.thr_bits);
+                    if (ng == 0)
+                        continue;
+                    const int table = treeens::kPacketHeaderRecs + ng * K;
+                    const int rec_begin = table + (ng * K + 3) / 4;
+                    if (ng < 0 || rec_begin > sub)
+                        return bad("packet header out of range");
+                    const uint32_t rec_lo = lo_b + uint32_t(rec_begin) * 8u;
+                    auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= rec_lo && a + 8 <= hi_b) || a == zero); };
+                    for (int j = 0; j < ng; j++) {
+                        const int g = g0 + j * W;
+                        if (g % W != w)
+                            return bad("a packet holds a group of another walker");
+                        for (int i = 0; i < K; i++) {
+                            const int gt = g * K + i;
+                            const uint32_t root_copy = lo_b + 8u * uint32_t(treeens::kPacketHeaderRecs + j * K + i);
+                            if (gt >= n_trees) {
+                                if (std::memcmp(lds.data() + root_copy, lds.data() + zero, 8) != 0)
+                                    return bad("packet: padding root is not the zero record");
+                                continue;
+                            }
+                            uint16_t first_rec;
+                            std::memcpy(&first_rec, lds.data() + lo_b + uint32_t(table) * 8u + 2u * uint32_t(j * K + i), 2);
+                            const uint32_t root_idx = first_rec;
+                            if (!valid(root_idx * 8u) ||
+                                std::memcmp(lds.data() + root_idx * 8u, lds.data() + root_copy, 8) != 0)
+                                return bad("packet: root copy does not match the tree's root record");
+                            if (const int e = walk_tree(gt, root_copy, root_idx, complete, valid))
+                                return e;
+                        }
+                    }
+                }
+            }
+            continue;
+        }
         for (int32_t t = t0; t < t1; t++) {
             const uint32_t recs = p.tile_recs[size_t(t)];
             if (recs > uint32_t(slot))
@@ -215,71 +348,8 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                 const uint32_t root_idx = rec0 + p.tree_node_off[size_t(gt)] - p.tree_node_off[size_t(tb)];
                 if (!valid(root_idx * 8u) || std::memcmp(lds.data() + root_idx * 8u, lds.data() + root0 + 8u * s, 8) != 0)
                     return bad("root copy does not match the tree's root record");
-                const int64_t tree_n = int64_t(p.tree_node_off[size_t(gt) + 1] - p.tree_node_off[size_t(gt)]);
-                for (int dl = 0; dl < DL && doc0 + dl < n_docs; dl++) {
-                    const int64_t doc = doc0 + dl;
-                    treeens::NodeRec r = rec_at(root0 + 8u * s);
-                    int steps = 0;
-                    for (;;) {
-                        const uint32_t fa = (r.w & mask) | uint32_t(dl * E);
-                        if (fa != (r.w & mask) + uint32_t(dl * E))
-                            return bad("column offset and lane offset overlap");
-                        if (fa + uint32_t(E) > xs)
-                            return bad("feature address outside the document tile");
-                        if (complete >= 0 ? steps == complete : fa < leaf_col)
-                            break;
-                        bool right_side;
-                        if (E == 4) {
-                            float x;
-                            std::memcpy(&x, lds.data() + fa, 4);
-                            right_side = x >= as_float(r.thr_bits);
-                        } else {
-                            uint16_t x;
-                            std::memcpy(&x, lds.data() + fa, 2);
-                            right_side = uint32_t(x) >= r.thr_bits;
-                        }
-                        const uint32_t a = ((r.w >> shift) + (right_side ? 1u : 0u)) * 8u;
-                        if (!valid(a))
-                            return bad("child address outside the tile's records");
-                        r = rec_at(a);
-                        if (++steps > p.max_depth + 1)
-                            return bad("walk longer than the deepest tree");
-                    }
-                    if ((r.w & mask) != 0)
-                        return bad("walk ended on an internal node");
-                    {
-                        // one more step from a leaf must come back to the same record
-                        bool right_side;
-                        if (E == 4) {
-                            float x;
-                            std::memcpy(&x, lds.data() + (r.w & mask) + dl * E, 4);
-                            right_side = x >= as_float(r.thr_bits);
-                        } else {
-                            uint16_t x;
-                            std::memcpy(&x, lds.data() + (r.w & mask) + dl * E, 2);
-                            right_side = uint32_t(x) >= r.thr_bits;
-                        }
-                        const uint32_t a = ((r.w >> shift) + (right_side ? 1u : 0u)) * 8u;
-                        if (!valid(a) || std::memcmp(lds.data() + a, &r, 8) != 0)
-                            return bad("a leaf does not absorb a further step");
-                    }
-                    const int64_t self = int64_t(r.w >> shift) - int64_t(root_idx);
-                    if (self < 0 || self >= tree_n)
-                        return bad("leaf outside its tree");
-                    const int32_t orig_tree = p.tree_orig[size_t(gt)];
-                    leaf_ids[doc * n_trees + orig_tree] = p.orig_id[p.tree_node_off[size_t(gt)] + size_t(self)];
-                    if (vec) {
-                        const int64_t row = int64_t(r.thr_bits) - 1;
-                        if (row < 1 || row > int64_t(p.nodes.size()))
-                            return bad("leaf names a row outside the leaf-vector table");
-                        for (int c = 0; c < n_outputs; c++)
-                            scores[doc * n_outputs + c] +=
-                                double(p.leaf_vec[size_t(row) * size_t(p.vec_stride) + size_t(c)]);
-                    } else {
-                        scores[doc] += double(as_float(r.thr_bits));
-                    }
-                }
-                seen[size_t(p.tree_orig[size_t(gt)])]++;
+                if (const int e = walk_tree(gt, root0 + 8u * s, root_idx, complete, valid))
+                    return e;
             }
         }
     }

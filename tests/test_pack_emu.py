@@ -46,7 +46,7 @@ def _walk(lib, ens, X, level, flags=0, leaf_values=None):
     X = np.ascontiguousarray(X, np.float32)
     leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
     scores = np.empty((X.shape[0], n_out), np.float64)
-    plan = np.zeros(8, np.int32)
+    plan = np.zeros(9, np.int32)
     rc = lib.emu_walk(ens.n_trees, *[a.ctypes.data for a in arrs], n_out, flags, X.ctypes.data,
                       X.shape[0], X.shape[1], level, leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
     assert rc == 0, lib.emu_message().decode()
@@ -253,3 +253,21 @@ def test_slots_of_whole_chunks(emu, n_features, max_leaves, dl, k, coded):
     tile_bytes, slot_recs = int(plan[6]), int(plan[7])
     assert plan[5] == 160 * 1024 and tile_bytes % 8192 == 0 and tile_bytes < 64 * 1024, plan
     assert tile_bytes - 8192 < slot_recs * 8 <= tile_bytes, plan  # the last chunk is in use
+
+
+def test_walker_packets_or_shared_tiles(emu):
+    """Two-workgroup plans of 64-document blocks stream per-walker packets when every group of
+    K trees fits a walker's sub-slot (the ranking and shallow workloads), and keep the shared
+    tiles otherwise (one large tree per group); one-workgroup plans always use tiles. The walk
+    over the packets (every LDS access in the walker's own sub-slot, every tree once per block,
+    leaf ids equal to the oracle's) is what _check runs in both cases."""
+    for wl, packets in (("rank_1kx32", True), ("shallow_20kx8_1M", True), ("wide_1kx64_f700", False)):
+        cfg = W.WORKLOADS[wl]
+        ens = W.make_ensemble(cfg, n_trees=min(cfg.n_trees, 800))
+        plan = _check(emu, ens, W.make_docs(cfg, n_docs=70), levels=(0,))
+        assert (plan[8] > 0) == packets, (wl, plan)
+        if packets:
+            assert plan[8] % 64 == 0 and 16 * plan[8] * 8 <= plan[6], plan
+    big = W.random_ensemble(3, n_trees=30, n_features=136, min_leaves=150, max_leaves=220)
+    plan = _check(emu, big, W.random_docs(3, 70, 136), levels=(0,))
+    assert plan[5] == 80 * 1024 and plan[0] == 64 and plan[8] == 0, plan
