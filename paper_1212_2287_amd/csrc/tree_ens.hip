@@ -347,9 +347,19 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         constexpr bool kComplete = decltype(complete_tag)::value;
         // the K root records (broadcast reads)
         uint64_t nd[K];
+        if constexpr (K % 2 == 0) {
+            // two roots per 16-byte read (a group's roots start 16-byte aligned when K is even)
 #pragma unroll
-        for (int i = 0; i < K; ++i)
-            nd[i] = read_record(rc + 8 * i);
+            for (int i = 0; i < K; i += 2) {
+                const uint4 r2 = *reinterpret_cast<const uint4 *>(rc + 8 * i);
+                nd[i] = uint64_t(r2.x) | uint64_t(r2.y) << 32;
+                nd[i + 1] = uint64_t(r2.z) | uint64_t(r2.w) << 32;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                nd[i] = read_record(rc + 8 * i);
+        }
         // One predicated step: feature addresses fa from the records, read the features
         // xv, compare, child link + bit (the right child follows the left one), read
         // that record.
@@ -415,13 +425,22 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                     internal |= fa[i] >= kLeafCol;
                 return __builtin_amdgcn_ballot_w64(internal) != 0;
             };
-            // The first step is taken untested: a group whose K roots are all leaves
-            // (single-leaf trees, idle slots) is rare, and a leaf absorbs the extra step.
+            // Trees sit in the packed order longest expected lockstep walk first, so the
+            // group's first tree usually ends last: step while its lanes are not all on
+            // leaves (one compare per step), then while any of the K trees is not (the full
+            // test, rarely true by then). The first step is taken untested: a group whose K
+            // roots are all leaves (single-leaf trees, idle slots) is rare, and a leaf absorbs
+            // the extra step.
+            auto lead_internal = [&]() {
+                return __builtin_amdgcn_ballot_w64(fa[0] >= kLeafCol) != 0;
+            };
             read_features();
-            do {
+            for (;;) {
                 descend();
                 read_features();
-            } while (any_internal());
+                if (!lead_internal() && (K == 1 || !any_internal()))
+                    break;
+            }
             // The exit path "uses" the last feature reads, so the compiler cannot sink
             // them below the test (where they would serialise with it again).
 #pragma unroll
@@ -472,19 +491,24 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         const int n_groups = (ntr + K - 1) / K;
         // records of the tile's trees start after the fixed header words and the root copies
         const uint32_t rec0 = uint32_t(xs_bytes) / 8u + uint32_t(treeens::kHeaderFixedWords / 2 + n_groups * K);
-        for (int g = walker; g < n_groups; g += n_walkers) {
-            const unsigned char *rc = lds + xs_bytes + 8 * (treeens::kHeaderFixedWords / 2 + g * K);
-            auto tree_of = [&](int i) {
-                const int t = g * K + i;
-                return t < ntr ? make_int2(tree_begin + t,
-                                           int(rec0 + tree_node_off[tree_begin + t] - tree_node_off[tree_begin]))
-                               : make_int2(-1, 0);
-            };
-            if (complete_depth >= 0)
-                walk_group(rc, std::true_type{}, complete_depth, tree_of);
-            else
-                walk_group(rc, std::false_type{}, complete_depth, tree_of);
-        }
+        auto walk_groups = [&](auto complete_tag) {
+            for (int g = walker; g < n_groups; g += n_walkers) {
+                const unsigned char *rc = lds + xs_bytes + 8 * (treeens::kHeaderFixedWords / 2 + g * K);
+                auto tree_of = [&](int i) {
+                    const int t = g * K + i;
+                    return t < ntr ? make_int2(tree_begin + t,
+                                               int(rec0 + tree_node_off[tree_begin + t] - tree_node_off[tree_begin]))
+                                   : make_int2(-1, 0);
+                };
+                walk_group(rc, complete_tag, complete_depth, tree_of);
+            }
+        };
+        // the branch on the tile's complete depth outside the group loop, so that each loop
+        // keeps its records in the registers it reads them into
+        if (complete_depth >= 0)
+            walk_groups(std::true_type{});
+        else
+            walk_groups(std::false_type{});
     };
     // Walk one of this walker's packets in its sub-slot, which starts at LDS record base: its
     // groups are first_group, first_group + n_walkers, ...
@@ -496,17 +520,21 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         const int first_group = __builtin_amdgcn_readfirstlane(int(h1.x));
         const uint16_t *first_rec =
             reinterpret_cast<const uint16_t *>(lds + 8 * (base + treeens::kPacketHeaderRecs + ng * K));
-        for (int j = 0; j < ng; ++j) {
-            const unsigned char *rc = lds + 8 * (base + treeens::kPacketHeaderRecs + j * K);
-            auto tree_of = [&](int i) {
-                const int gt = (first_group + j * n_walkers) * K + i;
-                return gt < n_trees ? make_int2(gt, int(first_rec[j * K + i])) : make_int2(-1, 0);
-            };
-            if (complete_depth >= 0)
-                walk_group(rc, std::true_type{}, complete_depth, tree_of);
-            else
-                walk_group(rc, std::false_type{}, complete_depth, tree_of);
-        }
+        auto walk_groups = [&](auto complete_tag) {
+            for (int j = 0; j < ng; ++j) {
+                const unsigned char *rc = lds + 8 * (base + treeens::kPacketHeaderRecs + j * K);
+                auto tree_of = [&](int i) {
+                    const int gt = (first_group + j * n_walkers) * K + i;
+                    return gt < n_trees ? make_int2(gt, int(first_rec[j * K + i])) : make_int2(-1, 0);
+                };
+                walk_group(rc, complete_tag, complete_depth, tree_of);
+            }
+        };
+        // as in walk_tile, the branch on the complete depth outside the group loop
+        if (complete_depth >= 0)
+            walk_groups(std::true_type{});
+        else
+            walk_groups(std::false_type{});
     };
     if constexpr (HALF) {
         if (pk_recs > 0) {

@@ -300,6 +300,9 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                         for (int i = 0; i < K; i++) {
                             const int gt = g * K + i;
                             const uint32_t root_copy = lo_b + 8u * uint32_t(treeens::kPacketHeaderRecs + j * K + i);
+                            // the kernel reads two roots per 16-byte read when K is even
+                            if (K % 2 == 0 && i % 2 == 0 && root_copy % 16 != 0)
+                                return bad("packet: a pair of root copies is not 16-byte aligned");
                             if (gt >= n_trees) {
                                 if (std::memcmp(lds.data() + root_copy, lds.data() + zero, 8) != 0)
                                     return bad("packet: padding root is not the zero record");
@@ -339,6 +342,9 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
             auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= lo && a + 8 <= hi) || a == zero); };
             // root copies: records 2.. of the header; padding slots hold the zero record
             const uint32_t root0 = xs + 8u * uint32_t(treeens::kHeaderFixedWords / 2);
+            // the kernel reads two roots per 16-byte read when K is even
+            if (K % 2 == 0 && root0 % 16 != 0)
+                return bad("header: the root copies are not 16-byte aligned");
             for (int s = ntr; s < padded; s++)
                 if (std::memcmp(lds.data() + root0 + 8u * s, lds.data() + zero, 8) != 0)
                     return bad("header: padding root is not the zero record");
