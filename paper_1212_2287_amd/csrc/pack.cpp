@@ -496,10 +496,15 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
 
-    // ---- walker packets (two-workgroup plans of 64-document blocks; see pack.hpp) -----------
-    if (plan.lds_bytes == kLdsPerCu / 2 && plan.docs_per_block == 64 && n_trees > 0) {
+    // ---- walker packets (plans of 64-document blocks; see pack.hpp) ---------------------------
+    if (plan.docs_per_block == 64 && n_trees > 0) {
         constexpr int32_t W = kPacketWalkers;
-        const int32_t sub = int32_t(int64_t(plan.tile_bytes) / 8 / W / 64 * 64); // records per sub-slot
+        const bool half = plan.lds_bytes == kLdsPerCu / 2;
+        // two workgroups per CU: the sub-slots share the tile slot (the zero record after it);
+        // one: they take the LDS past the document tile, then their own zero record
+        const int64_t region = half ? int64_t(plan.tile_bytes) : int64_t(plan.lds_bytes) - plan.xs_bytes - 16;
+        const int32_t sub = int32_t(std::max<int64_t>(region, 0) / 8 / W / 64 * 64); // records per sub-slot
+        const int32_t pk_zero = half ? plan.zero_rec : plan.xs_bytes + W * sub * 8;
         const int32_t n_groups = (n_trees + K - 1) / K;
         auto group_recs = [&](int32_t g) {
             const int32_t t0 = g * K, t1 = std::min(n_trees, t0 + K);
@@ -510,7 +515,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         };
         // per walker: runs (first group, groups) of its consecutive groups that fit a sub-slot
         std::vector<std::vector<std::pair<int32_t, int32_t>>> runs(static_cast<size_t>(W));
-        bool fits = sub > 0 && sub / 64 <= kPrefetchHalf;
+        bool fits = sub > 0 && sub / 64 <= (half ? kPrefetchHalf : kPrefetchFull);
         for (int32_t w = 0; w < W && fits; w++) {
             int32_t first = -1, count = 0;
             int64_t recs = 0;
@@ -539,10 +544,11 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             for (const auto &r : runs)
                 per = std::max(per, int32_t(r.size()));
             p.pk_recs = sub;
+            p.pk_zero_rec = pk_zero;
             p.pk_per_walker = per;
             p.packets.assign(size_t(W) * size_t(per) * size_t(sub), NodeRec{0u, 0u});
             std::vector<int32_t> most(static_cast<size_t>(per), 0);
-            const NodeRec zero_leaf{zero_record_value(plan, vec), (uint32_t(plan.zero_rec) / 8u) << shift};
+            const NodeRec zero_leaf{zero_record_value(plan, vec), (uint32_t(pk_zero) / 8u) << shift};
             for (int32_t w = 0; w < W; w++) {
                 const uint32_t base = uint32_t(plan.xs_bytes / 8) + uint32_t(w * sub); // sub-slot in LDS
                 for (size_t q = 0; q < runs[size_t(w)].size(); q++) {

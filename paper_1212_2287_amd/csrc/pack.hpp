@@ -64,10 +64,13 @@ constexpr int kMaxTileTrees = 1024;
 // kernel locates tile t without a table.
 constexpr int kHeaderFixedWords = 4;
 
-// Walker packets. In two-workgroup plans of 64-document blocks each of the 16 walkers (one wave
-// each) streams its own groups of K trees (g = w, w + 16, w + 32, ...) through a sub-slot of the
-// tile slot of its own, so walkers never wait for one another between tiles. A packet is a run
-// of consecutive groups of one walker that fits the sub-slot, laid out as
+// Walker packets. In plans of 64-document blocks each of the 16 walkers (one wave each) streams
+// its own groups of K trees (g = w, w + 16, w + 32, ...) through a sub-slot of its own, so
+// walkers never wait for one another between tiles. Two-workgroup plans cut the tile slot into
+// the 16 sub-slots; one-workgroup plans cut all of the LDS past the document tile but a zero
+// record of their own (their feature trace, whose bitmasks sit past the shared tiles, keeps
+// walking the shared tiles). A packet is a run of consecutive groups of one walker that fits
+// the sub-slot, laid out as
 //   record 0   number of groups n in the packet; their common complete depth d, else -1
 //   record 1   index of the packet's first group (its later groups follow at a stride of 16)
 //   records 2.. the K root copies of each group (the zero record for slots past the last tree)
@@ -156,6 +159,7 @@ struct Packed {
     // w's packet q is packets[(w * pk_per_walker + q) * pk_recs, ...), linked for its sub-slot
     // at LDS record xs_bytes / 8 + w * pk_recs. pk_recs == 0: the plan walks shared tiles.
     int32_t pk_recs = 0;
+    int32_t pk_zero_rec = 0; // LDS byte address of the zero record the packets' padding links to
     int32_t pk_per_walker = 0;
     int32_t pk_max_groups = 0;   // groups in the fullest packet
     int64_t pk_total_rounds = 0; // sum over packet indices of the most groups any walker has there

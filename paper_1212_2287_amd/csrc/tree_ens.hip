@@ -148,6 +148,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     //                            after the last tile, the cross-walker reduction (1,024 doubles,
     //                            4 x 1,024 with vector-valued leaves)
     //   zero_rec (8 bytes)       all-zero self-linked leaf of value 0, for idle walker slots
+    //                            (walker packets of one-workgroup plans fill the LDS from
+    //                            xs_bytes up to a zero record of their own, passed here)
     //   usage_off                usage modes: word j of document lane dl's feature bitmask at
     //                            [j * DL + dl] (32 feature ids a word); in the slot past the
     //                            largest tile image when it fits there (kModeUsageSlot, two
@@ -222,7 +224,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     //    loaded unconditionally so that the compiler counts the outstanding loads exactly.
     constexpr int kWin = treeens::kPrefetchFull / 2;
     constexpr int kDepth = HALF ? 1 : TREE_ENS_PREFETCH_DEPTH; // tiles in flight
-    constexpr int kPreA = HALF ? kPre : kWin;
+    constexpr int kPreA = kPre; // shared tiles of two-workgroup plans, or walker packets
     uint2 pa[kPreA], win[kDepth][HALF ? 1 : kWin];
     int cur_recs = 0;
     const int chunks = (slot_recs + kThreads - 1) / kThreads;
@@ -242,8 +244,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         for (int j = 0; j < kWin; ++j)
             dst[j] = src[(j < chunks ? j : 0) * kThreads];
     };
-    // Walker packets (pk_recs > 0, two-workgroup plans of 64-document blocks): walker w's packet
-    // q is images[(w * n_tiles + q) * pk_recs, ...); each lane loads pk_recs / 64 records of it.
+    // Walker packets (pk_recs > 0, plans of 64-document blocks): walker w's packet q is
+    // images[(w * n_tiles + q) * pk_recs, ...); each lane loads pk_recs / 64 records of it.
     const int pk_lane = pk_recs / 64;
     const uint2 *pk_src = images + (int64_t(walker) * n_tiles) * pk_recs + dl;
     auto fetch_packet = [&](int q) {
@@ -263,7 +265,10 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 fetch(t_lo, cur_recs);
         }
     } else {
-        if (t_lo < t_hi) {
+        if (pk_recs > 0) {
+            if (t_lo < t_hi)
+                fetch_packet(t_lo);
+        } else if (t_lo < t_hi) {
 #pragma unroll
             for (int d = 0; d < kDepth; ++d)
                 fetch_window(win[d], t_lo + d);
@@ -536,27 +541,30 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         else
             walk_groups(std::false_type{});
     };
-    if constexpr (HALF) {
-        if (pk_recs > 0) {
-            // Each walker streams its own packets through its own sub-slot: no barrier between
-            // packets, so a walker never waits for the slowest one of a tile.
-            const uint32_t my_base = uint32_t(xs_bytes) / 8u + uint32_t(walker * pk_recs);
-            uint2 *my = reinterpret_cast<uint2 *>(lds) + my_base;
-            __syncthreads(); // the document tile and the zero record are written
-            for (int q = t_lo; q < t_hi; ++q) {
-                // this packet's records (and, before the first, the document rows) have landed
-                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    // Each walker streams its own packets through its own sub-slot: no barrier between packets,
+    // so a walker never waits for the slowest one of a tile.
+    auto walk_packets = [&]() {
+        const uint32_t my_base = uint32_t(xs_bytes) / 8u + uint32_t(walker * pk_recs);
+        uint2 *my = reinterpret_cast<uint2 *>(lds) + my_base;
+        __syncthreads(); // the document tile and the zero record are written
+        for (int q = t_lo; q < t_hi; ++q) {
+            // this packet's records (and, before the first, the document rows) have landed
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 #pragma unroll
-                for (int j = 0; j < kPre; ++j)
-                    if (j < pk_lane)
-                        my[dl + j * 64] = pa[j];
-                // the wave's own writes complete before it reads the packet back
-                __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
-                if (q + 1 < t_hi)
-                    fetch_packet(q + 1);
-                walk_packet(my_base);
-            }
-        } else
+            for (int j = 0; j < kPre; ++j)
+                if (j < pk_lane)
+                    my[dl + j * 64] = pa[j];
+            // the wave's own writes complete before it reads the packet back
+            __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
+            if (q + 1 < t_hi)
+                fetch_packet(q + 1);
+            walk_packet(my_base);
+        }
+    };
+    if constexpr (HALF) {
+        if (pk_recs > 0)
+            walk_packets();
+        else
         for (int ti = t_lo; ti < t_hi; ++ti) {
             __syncthreads(); // the previous tile is fully walked (and the document tile written)
             // All outstanding global loads (this tile's records, and the document rows before
@@ -575,6 +583,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 fetch(ti + 1, cur_recs);
             walk_tile();
         }
+    } else if (pk_recs > 0) {
+        walk_packets();
     } else {
         // the document rows (loaded after the first two tiles) land before the first barrier
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
@@ -846,6 +856,7 @@ struct tree_ens {
     // walker packets (two-workgroup plans of 64-document blocks): records per sub-slot (0: the
     // plan walks shared tiles), packets per walker, the planner's rounds, and the images
     int32_t pk_recs = 0;
+    int32_t pk_zero_rec = 0;
     int32_t pk_per_walker = 0;
     int32_t pk_max_groups = 0;
     int64_t pk_total_rounds = 0;
@@ -1148,8 +1159,10 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                 return hip_fail(e, "hipMallocAsync(partials)");
         }
     }
-    // walker packets (pk_recs > 0) stand in for the tiles: n_tiles is then packets per walker
-    const bool pk = h->pk_recs > 0;
+    // walker packets (pk_recs > 0) stand in for the tiles: n_tiles is then packets per walker.
+    // The feature trace of one-workgroup plans keeps the shared tiles: its bitmasks sit past
+    // their zero record, where the packets' sub-slots reach.
+    const bool pk = h->pk_recs > 0 && !(MODE == kModeUsage && h->plan.lds_bytes == treeens::kLdsPerCu);
     const uint2 *images = pk ? h->d_packets : h->d_images + h->level_image_off[level];
     const uint32_t *tile_recs = h->d_tile_recs + (pk ? 0 : h->level_begin[level]);
     const int n_tiles = pk ? h->pk_per_walker : h->level_begin[level + 1] - h->level_begin[level];
@@ -1185,11 +1198,12 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     for (int chunk = 0; chunk < n_chunks && e == hipSuccess; ++chunk) {
         hipLaunchKernelGGL(fn, dim3(unsigned(n_wgs)), dim3(kThreads), 0, stream, docs, n_docs,
                            row_stride, h->n_cols, images, slot_recs, tile_recs,
-                           n_tiles, int32_t(shape.head), splits, h->plan.xs_bytes, h->plan.zero_rec,
+                           n_tiles, int32_t(shape.head), splits, h->plan.xs_bytes,
+                           pk ? h->pk_zero_rec : h->plan.zero_rec,
                            partials, scores, leaf_ids, h->d_orig_id, h->d_tree_node_off,
                            h->d_tree_orig, h->n_trees, masks, mask_words, usage_off,
                            reinterpret_cast<const float4 *>(h->d_leaf_vec), h->vec_stride / 4, n_out,
-                           chunk, scale, h->pk_recs);
+                           chunk, scale, pk ? h->pk_recs : 0);
         e = hipGetLastError();
         if (e == hipSuccess && partials) {
             // the tail blocks' entries, in [doc][component] order
@@ -1295,6 +1309,7 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
     h->total_rounds = p.total_rounds;
     h->usage_slot_off = p.usage_slot_off;
     h->pk_recs = p.pk_recs;
+    h->pk_zero_rec = p.pk_zero_rec;
     h->pk_per_walker = p.pk_per_walker;
     h->pk_max_groups = p.pk_max_groups;
     h->pk_total_rounds = p.pk_total_rounds;

@@ -162,11 +162,16 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         return bad("tile image exceeds the prefetch registers");
     }
     if (p.pk_recs > 0) {
-        // walker packets: whole 64-lane loads that fit the prefetch registers, sub-slots inside
-        // the tile slot, one packet stream per walker
-        if (pl.lds_bytes != treeens::kLdsPerCu / 2 || DL != 64 || p.pk_recs % 64 ||
-            p.pk_recs / 64 > treeens::kPrefetchHalf ||
-            int64_t(treeens::kPacketWalkers) * p.pk_recs * 8 > pl.tile_bytes)
+        // walker packets: whole 64-lane loads that fit the prefetch registers, one packet stream
+        // per walker; two-workgroup plans: sub-slots inside the tile slot, before the plan's zero
+        // record; one-workgroup plans: sub-slots up to the packets' own zero record
+        const bool half = pl.lds_bytes == treeens::kLdsPerCu / 2;
+        const int64_t sub_end = int64_t(xs) + int64_t(treeens::kPacketWalkers) * p.pk_recs * 8;
+        if (DL != 64 || p.pk_recs % 64 ||
+            p.pk_recs / 64 > (half ? treeens::kPrefetchHalf : treeens::kPrefetchFull) ||
+            (half ? (p.pk_zero_rec != int32_t(zero) || sub_end > int64_t(xs) + pl.tile_bytes)
+                  : (p.pk_zero_rec % 8 || sub_end > p.pk_zero_rec ||
+                     int64_t(p.pk_zero_rec) + 8 > pl.lds_bytes)))
             return bad("walker sub-slots do not fit the plan");
         if (p.packets.size() != size_t(treeens::kPacketWalkers) * size_t(p.pk_per_walker) * size_t(p.pk_recs))
             return bad("packet buffer has the wrong size");
@@ -275,9 +280,13 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         };
 
         if (p.pk_recs > 0) {
-            // each walker copies its packets, in order, into its own sub-slot and walks them
+            // each walker copies its packets, in order, into its own sub-slot and walks them;
+            // padding links to the packets' zero record (the plan's own in two-workgroup plans)
             constexpr int32_t W = treeens::kPacketWalkers;
             const int32_t sub = p.pk_recs, per = p.pk_per_walker;
+            const uint32_t pzero = uint32_t(p.pk_zero_rec);
+            const treeens::NodeRec zp{treeens::zero_record_value(pl, vec), (pzero / 8u) << shift};
+            std::memcpy(lds.data() + pzero, &zp, 8);
             for (int32_t w = 0; w < W; w++) {
                 const uint32_t lo_b = xs + uint32_t(w * sub) * 8u, hi_b = lo_b + uint32_t(sub) * 8u;
                 for (int32_t q = 0; q < per; q++) {
@@ -292,7 +301,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                     if (ng < 0 || rec_begin > sub)
                         return bad("packet header out of range");
                     const uint32_t rec_lo = lo_b + uint32_t(rec_begin) * 8u;
-                    auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= rec_lo && a + 8 <= hi_b) || a == zero); };
+                    auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= rec_lo && a + 8 <= hi_b) || a == pzero); };
                     for (int j = 0; j < ng; j++) {
                         const int g = g0 + j * W;
                         if (g % W != w)
@@ -304,7 +313,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                             if (K % 2 == 0 && i % 2 == 0 && root_copy % 16 != 0)
                                 return bad("packet: a pair of root copies is not 16-byte aligned");
                             if (gt >= n_trees) {
-                                if (std::memcmp(lds.data() + root_copy, lds.data() + zero, 8) != 0)
+                                if (std::memcmp(lds.data() + root_copy, lds.data() + pzero, 8) != 0)
                                     return bad("packet: padding root is not the zero record");
                                 continue;
                             }
