@@ -496,48 +496,64 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
 
-    // ---- walker packets (plans of 64-document blocks; see pack.hpp) ---------------------------
-    if (plan.docs_per_block == 64 && n_trees > 0) {
-        constexpr int32_t W = kPacketWalkers;
+    // ---- walker packets (plans of 64- or 32-document blocks; see pack.hpp) -----------------------
+    if ((plan.docs_per_block == 64 || plan.docs_per_block == 32) && n_trees > 0) {
+        constexpr int32_t W = kPacketWalkers;       // waves, one packet stream each
+        const int32_t P = 64 / plan.docs_per_block; // walkers per wave
+        const int32_t HW = W * P;                   // walkers
         const bool half = plan.lds_bytes == kLdsPerCu / 2;
         // two workgroups per CU: the sub-slots share the tile slot (the zero record after it);
         // one: they take the LDS past the document tile, then their own zero record
         const int64_t region = half ? int64_t(plan.tile_bytes) : int64_t(plan.lds_bytes) - plan.xs_bytes - 16;
         const int32_t sub = int32_t(std::max<int64_t>(region, 0) / 8 / W / 64 * 64); // records per sub-slot
+        const int32_t part = sub / P; // records of one walker's part of a packet
         const int32_t pk_zero = half ? plan.zero_rec : plan.xs_bytes + W * sub * 8;
         const int32_t n_groups = (n_trees + K - 1) / K;
+        // walker h of wave v (walker index v * P + h) takes groups v * P + h + r * HW, r = 0, 1, ...
+        auto group_of = [&](int32_t v, int32_t h, int32_t r) { return v * P + h + r * HW; };
         auto group_recs = [&](int32_t g) {
+            if (g >= n_groups)
+                return int64_t(0); // past the last group: zero roots, no records
             const int32_t t0 = g * K, t1 = std::min(n_trees, t0 + K);
             return int64_t(p.tree_node_off[size_t(t1)]) - int64_t(p.tree_node_off[size_t(t0)]);
         };
         auto packet_recs = [&](int32_t ng, int64_t tree_recs) {
             return int64_t(kPacketHeaderRecs) + int64_t(ng) * K + (int64_t(ng) * K + 3) / 4 + tree_recs;
         };
-        // per walker: runs (first group, groups) of its consecutive groups that fit a sub-slot
+        // per wave: runs (first round, rounds) of consecutive rounds whose groups fit every
+        // walker's part of the sub-slot; all walkers of a wave step through the same rounds
         std::vector<std::vector<std::pair<int32_t, int32_t>>> runs(static_cast<size_t>(W));
-        bool fits = sub > 0 && sub / 64 <= (half ? kPrefetchHalf : kPrefetchFull);
-        for (int32_t w = 0; w < W && fits; w++) {
+        bool fits = sub > 0 && part % 2 == 0 && sub / 64 <= (half ? kPrefetchHalf : kPrefetchFull);
+        for (int32_t v = 0; v < W && fits; v++) {
+            int32_t rounds = 0;
+            while (group_of(v, 0, rounds) < n_groups)
+                rounds++;
             int32_t first = -1, count = 0;
-            int64_t recs = 0;
-            for (int32_t g = w; g < n_groups; g += W) {
-                const int64_t gr = group_recs(g);
-                if (first >= 0 && packet_recs(count + 1, recs + gr) <= sub) {
+            std::vector<int64_t> recs(static_cast<size_t>(P), 0);
+            for (int32_t r = 0; r < rounds; r++) {
+                bool more = first >= 0;
+                for (int32_t h = 0; h < P && more; h++)
+                    more = packet_recs(count + 1, recs[size_t(h)] + group_recs(group_of(v, h, r))) <= part;
+                if (more) {
                     count++;
-                    recs += gr;
+                    for (int32_t h = 0; h < P; h++)
+                        recs[size_t(h)] += group_recs(group_of(v, h, r));
                     continue;
                 }
                 if (first >= 0)
-                    runs[size_t(w)].push_back({first, count});
-                if (packet_recs(1, gr) > sub) {
-                    fits = false;
+                    runs[size_t(v)].push_back({first, count});
+                for (int32_t h = 0; h < P; h++)
+                    if (packet_recs(1, group_recs(group_of(v, h, r))) > part)
+                        fits = false;
+                if (!fits)
                     break;
-                }
-                first = g;
+                first = r;
                 count = 1;
-                recs = gr;
+                for (int32_t h = 0; h < P; h++)
+                    recs[size_t(h)] = group_recs(group_of(v, h, r));
             }
             if (fits && first >= 0)
-                runs[size_t(w)].push_back({first, count});
+                runs[size_t(v)].push_back({first, count});
         }
         if (fits) {
             int32_t per = 0;
@@ -549,48 +565,53 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             p.packets.assign(size_t(W) * size_t(per) * size_t(sub), NodeRec{0u, 0u});
             std::vector<int32_t> most(static_cast<size_t>(per), 0);
             const NodeRec zero_leaf{zero_record_value(plan, vec), (uint32_t(pk_zero) / 8u) << shift};
-            for (int32_t w = 0; w < W; w++) {
-                const uint32_t base = uint32_t(plan.xs_bytes / 8) + uint32_t(w * sub); // sub-slot in LDS
-                for (size_t q = 0; q < runs[size_t(w)].size(); q++) {
-                    const int32_t g0 = runs[size_t(w)][q].first, ng = runs[size_t(w)][q].second;
-                    NodeRec *img = p.packets.data() + (size_t(w) * size_t(per) + q) * size_t(sub);
+            for (int32_t v = 0; v < W; v++) {
+                for (size_t q = 0; q < runs[size_t(v)].size(); q++) {
+                    const int32_t r0 = runs[size_t(v)][q].first, ng = runs[size_t(v)][q].second;
                     p.pk_max_groups = std::max(p.pk_max_groups, ng);
                     most[q] = std::max(most[q], ng);
+                    // the common complete depth of every tree of the packet, else -1
                     int32_t complete = -2; // -2: no tree yet
-                    for (int32_t j = 0; j < ng; j++) {
-                        for (int32_t i = 0; i < K; i++) {
-                            const int32_t t = (g0 + j * W) * K + i;
-                            if (t >= n_trees)
-                                continue;
-                            const int32_t d = int32_t(p.tree_depth[size_t(t)]);
-                            const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
-                            const bool full = nn == (int64_t(2) << d) - 1;
-                            complete = (complete == -2 || complete == d) && full ? d : -1;
+                    for (int32_t h = 0; h < P; h++) {
+                        for (int32_t j = 0; j < ng; j++) {
+                            for (int32_t i = 0; i < K; i++) {
+                                const int32_t t = group_of(v, h, r0 + j) * K + i;
+                                if (t >= n_trees)
+                                    continue;
+                                const int32_t d = int32_t(p.tree_depth[size_t(t)]);
+                                const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
+                                const bool full = nn == (int64_t(2) << d) - 1;
+                                complete = (complete == -2 || complete == d) && full ? d : -1;
+                            }
                         }
                     }
-                    img[0] = NodeRec{uint32_t(ng), uint32_t(complete)};
-                    img[1] = NodeRec{uint32_t(g0), 0u};
-                    const int32_t table = kPacketHeaderRecs + ng * K;
-                    uint16_t *first_rec = reinterpret_cast<uint16_t *>(img + table);
-                    int32_t pos = table + (ng * K + 3) / 4;
-                    for (int32_t j = 0; j < ng; j++) {
-                        for (int32_t i = 0; i < K; i++) {
-                            const int32_t t = (g0 + j * W) * K + i;
-                            NodeRec root = zero_leaf;
-                            if (t < n_trees) {
-                                const uint32_t first = p.tree_node_off[size_t(t)];
-                                const uint32_t nn = p.tree_node_off[size_t(t) + 1] - first;
-                                const uint32_t tree_rec = base + uint32_t(pos);
-                                first_rec[j * K + i] = uint16_t(tree_rec);
-                                for (uint32_t n = 0; n < nn; n++) {
-                                    NodeRec r = p.nodes[first + n];
-                                    r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
-                                    img[pos + int32_t(n)] = r;
+                    for (int32_t h = 0; h < P; h++) {
+                        const uint32_t base = uint32_t(plan.xs_bytes / 8) + uint32_t(v * sub + h * part); // in LDS
+                        NodeRec *img = p.packets.data() + (size_t(v) * size_t(per) + q) * size_t(sub) + size_t(h * part);
+                        img[0] = NodeRec{uint32_t(ng), uint32_t(complete)};
+                        img[1] = NodeRec{uint32_t(group_of(v, h, r0)), 0u};
+                        const int32_t table = kPacketHeaderRecs + ng * K;
+                        uint16_t *first_rec = reinterpret_cast<uint16_t *>(img + table);
+                        int32_t pos = table + (ng * K + 3) / 4;
+                        for (int32_t j = 0; j < ng; j++) {
+                            for (int32_t i = 0; i < K; i++) {
+                                const int32_t t = group_of(v, h, r0 + j) * K + i;
+                                NodeRec root = zero_leaf;
+                                if (t < n_trees) {
+                                    const uint32_t first = p.tree_node_off[size_t(t)];
+                                    const uint32_t nn = p.tree_node_off[size_t(t) + 1] - first;
+                                    const uint32_t tree_rec = base + uint32_t(pos);
+                                    first_rec[j * K + i] = uint16_t(tree_rec);
+                                    for (uint32_t n = 0; n < nn; n++) {
+                                        NodeRec r = p.nodes[first + n];
+                                        r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                                        img[pos + int32_t(n)] = r;
+                                    }
+                                    root = img[pos];
+                                    pos += int32_t(nn);
                                 }
-                                root = img[pos];
-                                pos += int32_t(nn);
+                                img[kPacketHeaderRecs + j * K + i] = root;
                             }
-                            img[kPacketHeaderRecs + j * K + i] = root;
                         }
                     }
                 }

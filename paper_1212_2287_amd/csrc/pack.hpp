@@ -64,21 +64,24 @@ constexpr int kMaxTileTrees = 1024;
 // kernel locates tile t without a table.
 constexpr int kHeaderFixedWords = 4;
 
-// Walker packets. In plans of 64-document blocks each of the 16 walkers (one wave each) streams
-// its own groups of K trees (g = w, w + 16, w + 32, ...) through a sub-slot of its own, so
-// walkers never wait for one another between tiles. Two-workgroup plans cut the tile slot into
-// the 16 sub-slots; one-workgroup plans cut all of the LDS past the document tile but a zero
-// record of their own (their feature trace, whose bitmasks sit past the shared tiles, keeps
-// walking the shared tiles). A packet is a run of consecutive groups of one walker that fits
-// the sub-slot, laid out as
-//   record 0   number of groups n in the packet; their common complete depth d, else -1
-//   record 1   index of the packet's first group (its later groups follow at a stride of 16)
+// Walker packets. In plans of 64- or 32-document blocks each of the 16 waves streams packets
+// through a sub-slot of its own, so walkers never wait for one another between tiles. Walker h
+// of wave v (one walker per wave for 64-document blocks, two half-waves for 32; walker index
+// v * P + h of HW = 16 * P) owns groups of K trees g = v * P + h + r * HW, r = 0, 1, ... (rounds).
+// Two-workgroup plans cut the tile slot into the 16 sub-slots; one-workgroup plans cut all of
+// the LDS past the document tile but a zero record of their own (their feature trace, whose
+// bitmasks sit past the shared tiles, keeps walking the shared tiles). A packet is a run of
+// consecutive rounds of one wave that fits the sub-slot, in P equal parts, one per walker,
+// each laid out as
+//   record 0   number of groups n in the packet (the same in every part); the complete depth d
+//              common to every tree of the packet, else -1
+//   record 1   index of the walker's first group in the packet (later ones follow at stride HW)
 //   records 2.. the K root copies of each group (the zero record for slots past the last tree)
 //   then       the LDS record index of each tree's first record, 16 bits each (for leaf ids),
 //              padded to a whole record
-//   then       the trees' records, child links as absolute LDS record indices of the sub-slot.
-// A walker loads its next packet into registers while it walks the current one. Plans in which
-// one group outgrows a sub-slot keep the shared tiles.
+//   then       the trees' records, child links as absolute LDS record indices of the part.
+// A wave loads its next packet into registers while it walks the current one. Plans in which
+// one group outgrows a part keep the shared tiles.
 constexpr int kPacketHeaderRecs = 2;
 constexpr int kPacketWalkers = 16;
 
@@ -155,9 +158,9 @@ struct Packed {
     // past the largest tiling-0 image (past the walkers' sub-slots with packets), or -1 when
     // they do not fit before the zero record
     int32_t usage_slot_off = -1;
-    // Walker packets (two-workgroup plans of 64-document blocks, see kPacketHeaderRecs): walker
-    // w's packet q is packets[(w * pk_per_walker + q) * pk_recs, ...), linked for its sub-slot
-    // at LDS record xs_bytes / 8 + w * pk_recs. pk_recs == 0: the plan walks shared tiles.
+    // Walker packets (see kPacketHeaderRecs): wave
+    // v's packet q is packets[(v * pk_per_walker + q) * pk_recs, ...), linked for its sub-slot
+    // at LDS record xs_bytes / 8 + v * pk_recs. pk_recs == 0: the plan walks shared tiles.
     int32_t pk_recs = 0;
     int32_t pk_zero_rec = 0; // LDS byte address of the zero record the packets' padding links to
     int32_t pk_per_walker = 0;

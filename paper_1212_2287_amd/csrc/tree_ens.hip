@@ -244,10 +244,12 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         for (int j = 0; j < kWin; ++j)
             dst[j] = src[(j < chunks ? j : 0) * kThreads];
     };
-    // Walker packets (pk_recs > 0, plans of 64-document blocks): walker w's packet q is
-    // images[(w * n_tiles + q) * pk_recs, ...); each lane loads pk_recs / 64 records of it.
+    // Walker packets (pk_recs > 0, plans of 64- or 32-document blocks): wave v's packet q is
+    // images[(v * n_tiles + q) * pk_recs, ...), one part of pk_recs * DL / 64 records for each
+    // of its walkers; each lane loads pk_recs / 64 records of it.
+    const int lane = tid & 63, wave = tid >> 6;
     const int pk_lane = pk_recs / 64;
-    const uint2 *pk_src = images + (int64_t(walker) * n_tiles) * pk_recs + dl;
+    const uint2 *pk_src = images + (int64_t(wave) * n_tiles) * pk_recs + lane;
     auto fetch_packet = [&](int q) {
         const uint2 *src = pk_src + int64_t(q) * pk_recs;
 #pragma unroll
@@ -522,7 +524,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         const uint2 h1 = *reinterpret_cast<const uint2 *>(lds + 8 * (base + 1));
         const int ng = __builtin_amdgcn_readfirstlane(int(h0.x));
         const int complete_depth = __builtin_amdgcn_readfirstlane(int(h0.y));
-        const int first_group = __builtin_amdgcn_readfirstlane(int(h1.x));
+        // group count and complete depth are common to the walkers of a wave; first groups not
+        const int first_group = DL == 64 ? __builtin_amdgcn_readfirstlane(int(h1.x)) : int(h1.x);
         const uint16_t *first_rec =
             reinterpret_cast<const uint16_t *>(lds + 8 * (base + treeens::kPacketHeaderRecs + ng * K));
         auto walk_groups = [&](auto complete_tag) {
@@ -544,8 +547,10 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // Each walker streams its own packets through its own sub-slot: no barrier between packets,
     // so a walker never waits for the slowest one of a tile.
     auto walk_packets = [&]() {
-        const uint32_t my_base = uint32_t(xs_bytes) / 8u + uint32_t(walker * pk_recs);
+        const uint32_t my_base = uint32_t(xs_bytes) / 8u + uint32_t(wave * pk_recs);
         uint2 *my = reinterpret_cast<uint2 *>(lds) + my_base;
+        // this walker's part of the wave's sub-slot
+        const uint32_t part_base = my_base + uint32_t(DL == 64 ? 0 : (lane / DL) * (pk_recs * DL / 64));
         __syncthreads(); // the document tile and the zero record are written
         for (int q = t_lo; q < t_hi; ++q) {
             // this packet's records (and, before the first, the document rows) have landed
@@ -553,12 +558,12 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
 #pragma unroll
             for (int j = 0; j < kPre; ++j)
                 if (j < pk_lane)
-                    my[dl + j * 64] = pa[j];
+                    my[lane + j * 64] = pa[j];
             // the wave's own writes complete before it reads the packet back
             __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
             if (q + 1 < t_hi)
                 fetch_packet(q + 1);
-            walk_packet(my_base);
+            walk_packet(part_base);
         }
     };
     if constexpr (HALF) {

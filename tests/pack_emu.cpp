@@ -167,7 +167,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         // record; one-workgroup plans: sub-slots up to the packets' own zero record
         const bool half = pl.lds_bytes == treeens::kLdsPerCu / 2;
         const int64_t sub_end = int64_t(xs) + int64_t(treeens::kPacketWalkers) * p.pk_recs * 8;
-        if (DL != 64 || p.pk_recs % 64 ||
+        if ((DL != 64 && DL != 32) || p.pk_recs % 64 ||
             p.pk_recs / 64 > (half ? treeens::kPrefetchHalf : treeens::kPrefetchFull) ||
             (half ? (p.pk_zero_rec != int32_t(zero) || sub_end > int64_t(xs) + pl.tile_bytes)
                   : (p.pk_zero_rec % 8 || sub_end > p.pk_zero_rec ||
@@ -287,44 +287,54 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
             const uint32_t pzero = uint32_t(p.pk_zero_rec);
             const treeens::NodeRec zp{treeens::zero_record_value(pl, vec), (pzero / 8u) << shift};
             std::memcpy(lds.data() + pzero, &zp, 8);
+            // P walkers per wave (two half-waves for 32-document blocks), each with its own part
+            const int32_t P = 64 / DL, HW = W * P, part = sub / P;
+            if (sub % P || part % 2)
+                return bad("packet parts are not whole, 16-byte aligned halves");
             for (int32_t w = 0; w < W; w++) {
-                const uint32_t lo_b = xs + uint32_t(w * sub) * 8u, hi_b = lo_b + uint32_t(sub) * 8u;
                 for (int32_t q = 0; q < per; q++) {
                     const treeens::NodeRec *img = p.packets.data() + (size_t(w) * size_t(per) + size_t(q)) * size_t(sub);
-                    std::memcpy(lds.data() + lo_b, img, size_t(sub) * 8);
-                    const treeens::NodeRec h0 = rec_at(lo_b), h1 = rec_at(lo_b + 8);
-                    const int ng = int(h0.thr_bits), complete = int32_t(h0.w), g0 = int(h1.thr_bits);
-                    if (ng == 0)
-                        continue;
-                    const int table = treeens::kPacketHeaderRecs + ng * K;
-                    const int rec_begin = table + (ng * K + 3) / 4;
-                    if (ng < 0 || rec_begin > sub)
-                        return bad("packet header out of range");
-                    const uint32_t rec_lo = lo_b + uint32_t(rec_begin) * 8u;
-                    auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= rec_lo && a + 8 <= hi_b) || a == pzero); };
-                    for (int j = 0; j < ng; j++) {
-                        const int g = g0 + j * W;
-                        if (g % W != w)
-                            return bad("a packet holds a group of another walker");
-                        for (int i = 0; i < K; i++) {
-                            const int gt = g * K + i;
-                            const uint32_t root_copy = lo_b + 8u * uint32_t(treeens::kPacketHeaderRecs + j * K + i);
-                            // the kernel reads two roots per 16-byte read when K is even
-                            if (K % 2 == 0 && i % 2 == 0 && root_copy % 16 != 0)
-                                return bad("packet: a pair of root copies is not 16-byte aligned");
-                            if (gt >= n_trees) {
-                                if (std::memcmp(lds.data() + root_copy, lds.data() + pzero, 8) != 0)
-                                    return bad("packet: padding root is not the zero record");
-                                continue;
+                    std::memcpy(lds.data() + xs + uint32_t(w * sub) * 8u, img, size_t(sub) * 8);
+                    const treeens::NodeRec c0 = rec_at(xs + uint32_t(w * sub) * 8u);
+                    for (int32_t h = 0; h < P; h++) {
+                        const uint32_t lo_b = xs + uint32_t(w * sub + h * part) * 8u, hi_b = lo_b + uint32_t(part) * 8u;
+                        const treeens::NodeRec h0 = rec_at(lo_b), h1 = rec_at(lo_b + 8);
+                        const int ng = int(h0.thr_bits), complete = int32_t(h0.w), g0 = int(h1.thr_bits);
+                        // the kernel takes the group count and complete depth from any lane
+                        if (h0.thr_bits != c0.thr_bits || h0.w != c0.w)
+                            return bad("packet parts disagree on the group count or complete depth");
+                        if (ng == 0)
+                            continue;
+                        const int table = treeens::kPacketHeaderRecs + ng * K;
+                        const int rec_begin = table + (ng * K + 3) / 4;
+                        if (ng < 0 || rec_begin > part)
+                            return bad("packet header out of range");
+                        const uint32_t rec_lo = lo_b + uint32_t(rec_begin) * 8u;
+                        auto valid = [&](uint32_t a) { return a % 8 == 0 && ((a >= rec_lo && a + 8 <= hi_b) || a == pzero); };
+                        for (int j = 0; j < ng; j++) {
+                            const int g = g0 + j * HW;
+                            if (g % HW != w * P + h)
+                                return bad("a packet holds a group of another walker");
+                            for (int i = 0; i < K; i++) {
+                                const int gt = g * K + i;
+                                const uint32_t root_copy = lo_b + 8u * uint32_t(treeens::kPacketHeaderRecs + j * K + i);
+                                // the kernel reads two roots per 16-byte read when K is even
+                                if (K % 2 == 0 && i % 2 == 0 && root_copy % 16 != 0)
+                                    return bad("packet: a pair of root copies is not 16-byte aligned");
+                                if (gt >= n_trees) {
+                                    if (std::memcmp(lds.data() + root_copy, lds.data() + pzero, 8) != 0)
+                                        return bad("packet: padding root is not the zero record");
+                                    continue;
+                                }
+                                uint16_t first_rec;
+                                std::memcpy(&first_rec, lds.data() + lo_b + uint32_t(table) * 8u + 2u * uint32_t(j * K + i), 2);
+                                const uint32_t root_idx = first_rec;
+                                if (!valid(root_idx * 8u) ||
+                                    std::memcmp(lds.data() + root_idx * 8u, lds.data() + root_copy, 8) != 0)
+                                    return bad("packet: root copy does not match the tree's root record");
+                                if (const int e = walk_tree(gt, root_copy, root_idx, complete, valid))
+                                    return e;
                             }
-                            uint16_t first_rec;
-                            std::memcpy(&first_rec, lds.data() + lo_b + uint32_t(table) * 8u + 2u * uint32_t(j * K + i), 2);
-                            const uint32_t root_idx = first_rec;
-                            if (!valid(root_idx * 8u) ||
-                                std::memcmp(lds.data() + root_idx * 8u, lds.data() + root_copy, 8) != 0)
-                                return bad("packet: root copy does not match the tree's root record");
-                            if (const int e = walk_tree(gt, root_copy, root_idx, complete, valid))
-                                return e;
                         }
                     }
                 }

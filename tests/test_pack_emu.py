@@ -256,15 +256,16 @@ def test_slots_of_whole_chunks(emu, n_features, max_leaves, dl, k, coded):
 
 
 def test_walker_packets_or_shared_tiles(emu):
-    """Plans of 64-document blocks stream per-walker packets when every group of K trees fits a
-    walker's sub-slot (the ranking and shallow workloads in two-workgroup plans, the large
-    700-feature workload's 511-node trees in a one-workgroup plan, whose sub-slots take all of
-    the LDS past the document tile), and keep the shared tiles otherwise (a group larger than a
-    sub-slot, or 32-document blocks). The walk over the packets (every LDS access in the
-    walker's own sub-slot or on the packets' zero record, every tree once per block, leaf ids
-    equal to the oracle's) is what _check runs in both cases."""
+    """Plans of 64- and 32-document blocks stream per-wave packets when every group of K trees
+    fits a walker's part of a sub-slot (the ranking and shallow workloads in two-workgroup
+    plans; the large 700-feature workload's 511-node trees and the wide workload's two
+    half-wave walkers per wave in one-workgroup plans, whose sub-slots take all of the LDS past
+    the document tile), and keep the shared tiles otherwise (a group larger than a part). The
+    walk over the packets (every LDS access in the walker's own part or on the packets' zero
+    record, every tree once per block, leaf ids equal to the oracle's) is what _check runs in
+    both cases."""
     for wl, packets in (("rank_1kx32", True), ("shallow_20kx8_1M", True), ("large_5kx256_f700_1M", True),
-                        ("wide_1kx64_f700", False)):
+                        ("wide_1kx64_f700", True)):
         cfg = W.WORKLOADS[wl]
         ens = W.make_ensemble(cfg, n_trees=min(cfg.n_trees, 800 if wl != "large_5kx256_f700_1M" else 120))
         plan = _check(emu, ens, W.make_docs(cfg, n_docs=70), levels=(0,))
@@ -272,8 +273,8 @@ def test_walker_packets_or_shared_tiles(emu):
         if packets and plan[5] == 80 * 1024:
             assert plan[8] % 64 == 0 and 16 * plan[8] * 8 <= plan[6], plan
         elif packets:
-            # coded 64-document tile of 701 columns (89,728 B); 16 sub-slots of 576 records
-            assert plan[5] == 160 * 1024 and plan[3] == 1 and plan[8] == 576, plan
+            # a 701-column tile of 64 codes or 32 floats (89,728 B); 16 sub-slots of 576 records
+            assert plan[5] == 160 * 1024 and plan[0] * (2 if plan[3] else 4) == 128 and plan[8] == 576, plan
     # one-workgroup plan of 64-document blocks whose trees outgrow a 576-record sub-slot
     wide = W.random_ensemble(5, n_trees=24, n_features=300, min_leaves=300, max_leaves=320)
     plan = _check(emu, wide, W.random_docs(5, 70, 300), levels=(0,))
