@@ -193,7 +193,8 @@ int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int
  *   min_features   1 + the largest feature id any node reads (0 if there is none).
  *   max_depth      edges on the longest root-to-leaf path over all trees.
  *   packed_bytes   bytes of node records (8 per node); the device also holds the tile images
- *                  built from them (one set per tiling granularity).
+ *                  built from them (one set per tiling granularity) and, for models whose
+ *                  groups of trees fit, the per-wave packets (one more copy of the records).
  *   n_tiles        LDS tiles the trees are streamed in for a large batch.
  *   docs_per_block documents a workgroup stages in LDS (a power of two from 8 to 64).
  */

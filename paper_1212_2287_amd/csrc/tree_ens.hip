@@ -858,8 +858,9 @@ struct tree_ens {
     int32_t level_slot_recs[treeens::kTileLevels] = {};
     uint2 *d_images = nullptr;      // tile images of every tiling
     uint32_t *d_tile_recs = nullptr; // records of each tile image
-    // walker packets (two-workgroup plans of 64-document blocks): records per sub-slot (0: the
-    // plan walks shared tiles), packets per walker, the planner's rounds, and the images
+    // walker packets (plans of 64- and 32-document blocks): records per sub-slot (0: the plan
+    // walks shared tiles), the packets' zero record, packets per wave, the planner's rounds,
+    // and the images
     int32_t pk_recs = 0;
     int32_t pk_zero_rec = 0;
     int32_t pk_per_walker = 0;
