@@ -64,6 +64,18 @@ def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
     return plans[0]
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_random_wide_models(emu, seed):
+    """Wide documents: one-workgroup plans of 64-, 32- and 16-document blocks, float and
+    threshold-coded, with walker packets (one or two walkers per wave) or shared tiles."""
+    rng = np.random.default_rng(100 + seed)
+    n_feat = int(rng.choice([200, 300, 700, 1100]))
+    ens = W.random_ensemble(100 + seed, n_trees=int(rng.integers(1, 200)), n_features=n_feat,
+                            min_leaves=1, max_leaves=int(rng.choice([8, 64, 200, 300])))
+    X = W.random_docs(100 + seed, n_docs=int(rng.integers(1, 80)), n_features=n_feat)
+    _check(emu, ens, X, flags=seed % 2, levels=(0,))
+
+
 def test_hand_ensemble_both_rules(emu):
     ens, X, _ = load_hand_ensemble()
     for flags in (0, 1):
