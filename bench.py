@@ -102,20 +102,41 @@ def count_visits(model, ens, Xd, max_docs=None):
     return total * (Xd.shape[0] / n), n < Xd.shape[0]
 
 
+def step_stats(samples_s):
+    """Median, mean and the 95% confidence interval of the mean (Student's t) of per-step
+    times, in ms (the paper reports means of repeated trials with 95% intervals)."""
+    n = len(samples_s)
+    ms = [v * 1e3 for v in samples_s]
+    mean = statistics.fmean(ms)
+    half = 0.0
+    if n > 1:
+        try:
+            from scipy.stats import t as student_t
+            q = float(student_t.ppf(0.975, n - 1))
+        except ImportError:  # normal quantile as a fallback
+            q = 1.96
+        half = q * statistics.stdev(ms) / n ** 0.5
+    return {"n": n, "median_ms": statistics.median(ms), "mean_ms": mean, "ci95_ms": half,
+            "min_ms": min(ms), "max_ms": max(ms)}
+
+
 def time_steps(model, Xd, out, steps, warmup):
+    """Host wall time per step over the timed region, mean kernel time per step from HIP events
+    on the launch stream, and the per-step event times (an event between consecutive steps)."""
     import torch
     for _ in range(warmup):
         model.predict(Xd, out)
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     t0 = time.perf_counter()
-    ev0.record()
-    for _ in range(steps):
+    evs[0].record()
+    for i in range(steps):
         model.predict(Xd, out)
-    ev1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return wall / steps, ev0.elapsed_time(ev1) / 1e3 / steps
+    per = [evs[i].elapsed_time(evs[i + 1]) / 1e3 for i in range(steps)]
+    return wall / steps, evs[0].elapsed_time(evs[steps]) / 1e3 / steps, per
 
 
 def roofline(kernel_s, lds_bytes, hbm_bytes, traffic):
@@ -157,7 +178,7 @@ def measure_workload(T, W, wl, steps, warmup, n_docs=None, visits_sample=None):
     Xd = torch.from_numpy(X).to("cuda")
     out = torch.empty(cfg.n_docs, dtype=torch.float32, device="cuda")
     del X
-    wall_s, kern_s = time_steps(model, Xd, out, steps, warmup)
+    wall_s, kern_s, per_step = time_steps(model, Xd, out, steps, warmup)
     doc_trees = cfg.n_docs * cfg.n_trees
     visits, sampled = count_visits(model, ens, Xd, visits_sample)
     lds_bytes = visits * 8 + doc_trees * 4
@@ -166,7 +187,8 @@ def measure_workload(T, W, wl, steps, warmup, n_docs=None, visits_sample=None):
     rec = {"workload": cfg.name, "n_trees": cfg.n_trees, "n_leaves": cfg.n_leaves,
            "n_features": cfg.n_features, "n_docs": cfg.n_docs,
            "value": doc_trees / wall_s, "ms_per_step": wall_s * 1e3, "kernel_ms": kern_s * 1e3,
-           "ns_per_doc": wall_s * 1e9 / cfg.n_docs, "visits": int(visits), "visits_sampled": sampled,
+           "ns_per_doc": wall_s * 1e9 / cfg.n_docs, "step_stats": step_stats(per_step),
+           "visits": int(visits), "visits_sampled": sampled,
            "roofline": rl, "roofline_hbm": rl_hbm, "roofline_lds_issue": rl_issue,
            "model": model.info()}
     log(f"{wl}: {rec['ms_per_step']:.3f} ms/step, {rec['value']:.3e} doc*tree/s, "
@@ -174,7 +196,7 @@ def measure_workload(T, W, wl, steps, warmup, n_docs=None, visits_sample=None):
     return rec, model, ens, Xd, out
 
 
-def latency_100(model, Xd, reps=300):
+def latency_100(model, Xd, reps=1000):
     import torch
     x = Xd[:100].contiguous()
     out = torch.empty(100, dtype=torch.float32, device="cuda")
@@ -346,7 +368,12 @@ def cpu_baseline(W, wl, budget_s=10.0):
     cfg = W.WORKLOADS[wl]
     ens = W.make_ensemble(cfg)
     X = W.make_docs(cfg)
-    threads = min(16, len(os.sched_getaffinity(0)))
+    # every host CPU the process may use, capped by the thread budget the machine's
+    # environment grants (OMP_NUM_THREADS, set to one GPU's share of the host on shared boxes)
+    host_cpus = os.cpu_count() or 1
+    threads = min(host_cpus, len(os.sched_getaffinity(0)))
+    if os.environ.get("OMP_NUM_THREADS", "").isdigit() and int(os.environ["OMP_NUM_THREADS"]) > 0:
+        threads = min(threads, int(os.environ["OMP_NUM_THREADS"]))
     oracle.score(ens, X[:1000], threads=threads, want_leaves=False)
     runs = []
     t_start = time.perf_counter()
@@ -364,7 +391,7 @@ def cpu_baseline(W, wl, budget_s=10.0):
                       f"(median), plain C oracle (branching walk, fp64 sum), OpenMP",
             "ns_per_doc": sec * 1e9 / cfg.n_docs,
             "single_thread_ns_per_doc_tree": single * 1e9 / (n1 * cfg.n_trees),
-            "cpu_model": _cpu_model()}
+            "cpu_model": _cpu_model(), "host_cpus": host_cpus}
 
 
 def pmc_probe(T, W) -> int:
@@ -446,6 +473,15 @@ def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) 
 
 
 def _cpu_model() -> str:
+    """The host CPU's model name as lscpu reports it (else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.strip().startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         with open("/proc/cpuinfo") as fh:
             for line in fh:

@@ -28,7 +28,7 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found; the gfx950 library cannot be built")
 
 
-def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
+def build(out: str = LIB, verbose: bool = False) -> str:
     """Compile the packer and the code generator (host C++) and the kernels + C ABI (HIP) into
     one shared library (linked with hiprtc for the model-specialised kernels)."""
     tmp = out + ".tmp"
@@ -37,10 +37,10 @@ def build(out: str = LIB, defines: tuple = (), verbose: bool = False) -> str:
     objs = []
     for name in ("pack", "codegen"):
         o = f"{out}.{name}.o"
-        run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", *[f"-D{d}" for d in defines], "-c",
+        run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Werror", "-c",
              os.path.join(CSRC, f"{name}.cpp"), "-o", o])
         objs.append(o)
-    run([_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], "-I", INCLUDE, "-I", CSRC, "-shared",
+    run([_hipcc(), *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-shared",
          os.path.join(CSRC, "tree_ens.hip"), os.path.join(CSRC, "topk.hip"), "-x", "none", *objs,
          "-lhiprtc", "-o", tmp])
     os.replace(tmp, out)

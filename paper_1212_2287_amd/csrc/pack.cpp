@@ -25,6 +25,11 @@ float strict_to_inclusive(float theta) {
     return std::nextafter(theta, INFINITY);
 }
 
+// A tree of n nodes whose longest root-to-leaf path has d edges is complete (every leaf at depth
+// d) exactly when n = 2^(d+1) - 1. Deep trees (d up to the node count) never are, and the shift
+// must not overflow.
+bool is_complete(int64_t n, int64_t d) { return d < 62 && n == (int64_t(2) << d) - 1; }
+
 // avg_tree_bytes: mean packed size of a tree, to pick how many trees a lane walks at once.
 // elem_bytes: 4 for float features, 2 for codes.
 LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
@@ -63,9 +68,6 @@ LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
     const double fit = avg_tree_bytes > 0 ? p.tile_bytes / avg_tree_bytes : 1e9;
     const int walkers = 1024 / p.docs_per_block;
     p.interleave = fit >= 4.0 * walkers ? 4 : fit >= 2.0 * walkers ? 2 : 1;
-#ifdef TREE_ENS_INTERLEAVE // measurement builds only: force the trees-per-lane interleave
-    p.interleave = TREE_ENS_INTERLEAVE;
-#endif
     return p;
 }
 
@@ -196,9 +198,6 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     // float tile cannot hold one tree for each walker, most walkers would idle.
     bool coded = plan.docs_per_block > 0 && plan.docs_per_block < 64 &&
                  avg_tree_bytes * (1024 / plan.docs_per_block) > plan.tile_bytes;
-#ifdef TREE_ENS_CODED // measurement builds only: force the choice
-    coded = TREE_ENS_CODED != 0;
-#endif
     auto canon = [&](float th) {
         float v = strict ? strict_to_inclusive(th) : th;
         return v == 0.0f ? 0.0f : v; // fold -0.0 into +0.0 (equal under every comparison)
@@ -270,7 +269,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         for (int32_t t = 0; t < n_trees; t++) {
             const int64_t a = tree_offsets[t];
             const int64_t n = tree_offsets[t + 1] - a;
-            complete_tree[size_t(t)] = n == (int64_t(2) << depth_of[size_t(t)]) - 1;
+            complete_tree[size_t(t)] = is_complete(n, depth_of[size_t(t)]);
             reach.assign(size_t(n), 0.0);
             level.assign(size_t(n), 0);
             at_depth.assign(size_t(depth_of[size_t(t)]) + 1, 0.0);
@@ -425,7 +424,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                 const int64_t nn = int64_t(p.tree_node_off[size_t(te) + 1] - p.tree_node_off[size_t(te)]);
                 const int32_t d = int32_t(p.tree_depth[size_t(te)]);
                 dmax = std::max(dmax, d);
-                const bool full = nn == (int64_t(2) << d) - 1; // complete binary tree of depth d
+                const bool full = is_complete(nn, d);
                 complete = (complete == -2 || complete == d) && full ? d : -1;
                 te++;
             }
@@ -580,7 +579,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                                     continue;
                                 const int32_t d = int32_t(p.tree_depth[size_t(t)]);
                                 const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
-                                const bool full = nn == (int64_t(2) << d) - 1;
+                                const bool full = is_complete(nn, d);
                                 complete = (complete == -2 || complete == d) && full ? d : -1;
                             }
                         }

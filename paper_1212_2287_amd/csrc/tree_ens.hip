@@ -63,9 +63,7 @@ constexpr int kXcds = 8; // accelerator complex dies, each with its own L2
 constexpr int kWaitVmcnt0 = 0x0F70;
 // the same with lgkmcnt(0) (LDS and scalar memory) and vmcnt, expcnt at their maxima
 constexpr int kWaitLgkmcnt0 = 0xC07F;
-#ifndef TREE_ENS_PREFETCH_DEPTH
-#define TREE_ENS_PREFETCH_DEPTH 2 // tiles in flight with one workgroup per CU
-#endif
+constexpr int kPrefetchDepth = 2; // tiles in flight with one workgroup per CU
 constexpr int kThreads = 1024; // workgroup size of the scoring kernel (16 waves)
 // what a launch of the scoring kernel produces
 constexpr int kModeScore = 0;  // scores
@@ -223,7 +221,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     //    kWin x kThreads records (the packer caps these tiles at that size and pads the images),
     //    loaded unconditionally so that the compiler counts the outstanding loads exactly.
     constexpr int kWin = treeens::kPrefetchFull / 2;
-    constexpr int kDepth = HALF ? 1 : TREE_ENS_PREFETCH_DEPTH; // tiles in flight
+    constexpr int kDepth = HALF ? 1 : kPrefetchDepth; // tiles in flight
     constexpr int kPreA = kPre; // shared tiles of two-workgroup plans, or walker packets
     uint2 pa[kPreA], win[kDepth][HALF ? 1 : kWin];
     int cur_recs = 0;
@@ -1042,9 +1040,6 @@ LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
         for (int sp = 2; sp <= std::min<int64_t>(nt, slots / rem); ++sp)
             consider(0, n_blocks - rem, sp);
     }
-#ifdef TREE_ENS_FORCE_SPLITS // measurement builds only
-    pick = LaunchShape{0, 0, std::min(TREE_ENS_FORCE_SPLITS, tiles_at(0))};
-#endif
     return pick;
 }
 

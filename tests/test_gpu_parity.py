@@ -86,6 +86,9 @@ def test_rank_1kx32_latency_batch(T):
     assert_leaves_equal(ids, ref_ids, "rank_1kx32, 100 docs")
 
 
+LEAF_CHUNK = 131_072  # documents per leaf-id launch: whole rounds of workgroups, no splits
+
+
 @pytest.mark.parametrize("wl", ["shallow_20kx8_1M", "large_5kx256_f700_1M"])
 def test_workload_1M_sampled(T, wl):
     import torch
@@ -99,15 +102,32 @@ def test_workload_1M_sampled(T, wl):
     with T.TreeEnsemble.from_ensemble(ens) as m:
         Xd = dev(X)
         s = m.predict(Xd)
-        lo = cfg.n_docs - 2048  # leaf ids for a slice that ends at the last (ragged) block
-        ids = m.predict_leaves(Xd[lo:].contiguous())
         torch.cuda.synchronize()
         s = s.cpu().numpy()
-        ids = ids.cpu().numpy()
+        # leaf ids of the seeded sample: every document's leaves are computed by launches of
+        # LEAF_CHUNK documents (the path in which each workgroup walks every tree of its block)
+        # and the sample's rows are kept
+        ids = np.empty((sample.size, cfg.n_trees), np.int32)
+        for a in range(0, cfg.n_docs, LEAF_CHUNK):
+            b = min(cfg.n_docs, a + LEAF_CHUNK)
+            sel = np.nonzero((sample >= a) & (sample < b))[0]
+            if sel.size == 0:
+                continue
+            _say(f"[parity] {wl}: leaf ids of docs {a}..{b}")
+            chunk = m.predict_leaves(Xd[a:b].contiguous())
+            rows = torch.from_numpy(sample[sel] - a).to(chunk.device)
+            ids[sel] = chunk.index_select(0, rows).cpu().numpy()
+            del chunk
+        # the last 4,096 documents in one launch: a small batch, its blocks split over the tiles
+        lo = cfg.n_docs - 4096
+        tail_ids = m.predict_leaves(Xd[lo:].contiguous())
+        torch.cuda.synchronize()
+        tail_ids = tail_ids.cpu().numpy()
         del Xd
     _say(f"[parity] {wl}: oracle on the sample")
-    ref, _, _ = oracle.score(ens, X[sample], want_leaves=False)
+    ref, ref_ids, _ = oracle.score(ens, X[sample])
     assert_scores_close(s[sample], ref, f"{wl} sample")
-    _, ref_ids, _ = oracle.score(ens, X[lo:])
-    assert_leaves_equal(ids, ref_ids, f"{wl} last 2048 docs")
+    assert_leaves_equal(ids, ref_ids, f"{wl} sample leaf ids")
+    _, ref_tail, _ = oracle.score(ens, X[lo:])
+    assert_leaves_equal(tail_ids, ref_tail, f"{wl} last 4096 docs")
     assert np.all(np.isfinite(s))

@@ -220,6 +220,39 @@ def test_tree_order_keeps_complete_trees_together(emu):
     assert tiles.size > 1 and (tiles == 3).all()
 
 
+def _deep_tree(n_internal, depth):
+    """A tree of n_internal splits whose longest path has `depth` edges: a chain of `depth`
+    splits down the right children, then the remaining splits on leaves near the root."""
+    fe, th, le, ri = [-1], [0.0], [-1], [-1]
+    level = [0]
+
+    def split(n):
+        le[n], ri[n], fe[n], th[n] = len(fe), len(fe) + 1, 0, 0.5
+        for _ in range(2):
+            fe.append(-1), th.append(0.0), le.append(-1), ri.append(-1), level.append(level[n] + 1)
+
+    node = 0
+    for _ in range(depth):
+        split(node)
+        node = ri[node]
+    for _ in range(n_internal - depth):
+        split(next(i for i in range(len(fe)) if fe[i] < 0 and level[i] < depth - 1))
+    return fe, th, le, ri, [1.0 if f < 0 else 0.0 for f in fe]
+
+
+def test_deep_tree_of_complete_size_is_not_complete(emu):
+    """255 nodes is the size of a complete tree of depth 7; a tree of 255 nodes and depth 71 is
+    not complete (the check must not shift by the depth: 2 << 71 wraps to 2 << 7 on x86), so its
+    tile keeps the leaf-tested walk, and its leaves still match the oracle."""
+    tree = _deep_tree(127, 71)
+    assert len(tree[0]) == 255
+    ens = _stack([tree, tree], 1)
+    _, tiles = _order(emu, ens)
+    assert tiles.size >= 1 and (tiles == -1).all(), tiles
+    X = np.array([[0.75], [0.25], [0.5], [np.nan]], np.float32)
+    _check(emu, ens, X, levels=(0,))
+
+
 def test_tree_order_shortens_the_lockstep_walk(emu):
     """On the ranking-shaped model, groups of 4 trees taken in the packed order need fewer
     lockstep steps (per 64-document wave, the longest path of any tree in the group) than in the
