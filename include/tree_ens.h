@@ -122,7 +122,10 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
  * the handle (calls on different streams are ordered by an event while they share it), or, if
  * larger, to a stream-ordered allocation (hipMallocAsync / hipFreeAsync on `stream`). Models
  * with threshold-coded features also take a stream-ordered buffer of n_docs x min_features
- * 16-bit codes for the duration of the call.
+ * 16-bit codes for the duration of the call. A call made while `stream` is being captured into
+ * a HIP graph takes neither: it gets a device buffer of its own for its partial sums and codes,
+ * allocated when it is captured and kept by the handle until tree_ens_destroy, so the graph's
+ * replays never share scratch with other calls of the handle, eager or captured.
  */
 int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
                      int32_t n_features, float *scores);

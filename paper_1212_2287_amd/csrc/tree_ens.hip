@@ -883,14 +883,19 @@ struct tree_ens {
     // kernel specialised for the model (TREE_ENS_CODEGEN), used by tree_ens_predict
     hipModule_t cg_module = nullptr;
     hipFunction_t cg_fn = nullptr;
-    // Small batches: partial sums of the tile splits, reused by every call (no allocation per
-    // call). Calls from different streams are ordered with an event, so they never share the
-    // scratch at the same time.
+    // Small batches: partial sums of the tile splits, reused by every eager call (no
+    // allocation per call). Eager calls from different streams are ordered with an event, so
+    // they never share the scratch at the same time.
     double *d_scratch = nullptr;
     hipEvent_t scratch_done = nullptr;
     mutable std::mutex scratch_mu;
     mutable hipStream_t scratch_stream = nullptr;
     mutable bool scratch_used = false;
+    // Calls captured into a HIP graph take none of the above (a replay is ordered with nothing
+    // the handle records): each captured call gets a buffer of its own for its partial sums and
+    // threshold codes, allocated when it is captured and kept until destroy.
+    mutable std::mutex capture_mu;
+    mutable std::vector<void *> capture_bufs;
     // launch shape of the last batch size seen (callers usually repeat one batch size)
     mutable std::mutex shape_mu;
     mutable int64_t shape_blocks = -1;
@@ -919,6 +924,8 @@ void free_device(tree_ens *h) {
     (void)hipFree(h->d_scratch);
     if (h->scratch_done)
         (void)hipEventDestroy(h->scratch_done);
+    for (void *b : h->capture_bufs)
+        (void)hipFree(b);
     if (h->cg_module)
         (void)hipModuleUnload(h->cg_module);
 }
@@ -1127,39 +1134,86 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
             h->shape_splits = shape.splits;
         }
     }
+    {
+        // grid of the chosen shape: every tail block split into the shape's splits, plus the
+        // padding to whole XCD columns
+        const int64_t tail_blocks = n_blocks - shape.head;
+        const int64_t tail_slots = shape.head > 0 ? (tail_blocks + kXcds - 1) / kXcds * kXcds : tail_blocks;
+        if (shape.head + tail_slots * shape.splits > 0x7fffffff)
+            return fail(TREE_ENS_E_ARG, "too many documents for one launch");
+    }
+    ScoreFn fn = pick_kernel<MODE>(h->plan);
+    if (!fn)
+        return fail(TREE_ENS_E_ARG, "unsupported document block size");
+    hipError_t e = hipSuccess;
+    // scratch of this call: split partial sums (score modes with splits) and threshold codes
+    // (coded models), each 256-byte aligned
+    auto align256 = [](size_t b) { return (b + 255) & ~size_t(255); };
+    const size_t codes_bytes = h->plan.coded ? align256(size_t(n_docs) * size_t(h->n_cols) * sizeof(uint16_t)) : 0;
+    auto partial_bytes = [&](const LaunchShape &sh) {
+        return kScores && sh.splits > 1
+                   ? align256(size_t(sh.splits) * size_t(n_docs - sh.head * dl) * size_t(comps) * sizeof(double))
+                   : size_t(0);
+    };
+    double *partials = nullptr;
+    uint16_t *codes = nullptr;
+    bool shared_scratch = false; // partials in the handle's event-ordered buffer
+    bool async_alloc = false;    // partials and codes from hipMallocAsync, freed on the stream
+    void *async_buf = nullptr;
+    std::unique_lock<std::mutex> scratch_lock;
+    {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(stream, &cap) != hipSuccess)
+            cap = hipStreamCaptureStatusNone;
+        (void)hipGetLastError();
+        const size_t need = codes_bytes + partial_bytes(shape);
+        if (cap == hipStreamCaptureStatusActive) {
+            // a buffer of this call's own, kept by the handle: replays of the graph never share
+            // it with eager calls or other graphs (allocated outside the stream's order, so the
+            // capture mode is relaxed for the allocation)
+            if (need > 0) {
+                void *buf = nullptr;
+                hipStreamCaptureMode mode = hipStreamCaptureModeRelaxed;
+                (void)hipThreadExchangeStreamCaptureMode(&mode);
+                e = hipMalloc(&buf, need);
+                (void)hipThreadExchangeStreamCaptureMode(&mode);
+                if (e != hipSuccess)
+                    return hip_fail(e, "hipMalloc(scratch of a captured call)");
+                std::lock_guard<std::mutex> lock(h->capture_mu);
+                h->capture_bufs.push_back(buf);
+                codes = h->plan.coded ? static_cast<uint16_t *>(buf) : nullptr;
+                partials = partial_bytes(shape)
+                               ? reinterpret_cast<double *>(static_cast<unsigned char *>(buf) + codes_bytes)
+                               : nullptr;
+            }
+        } else {
+            const size_t pb = partial_bytes(shape);
+            if (pb > 0 && pb <= kScratchDoubles * sizeof(double) && codes_bytes == 0) {
+                scratch_lock = std::unique_lock<std::mutex>(h->scratch_mu);
+                if (h->scratch_used && h->scratch_stream != stream) {
+                    e = hipStreamWaitEvent(stream, h->scratch_done, 0);
+                    if (e != hipSuccess)
+                        return hip_fail(e, "hipStreamWaitEvent");
+                }
+                partials = h->d_scratch;
+                shared_scratch = true;
+            } else if (need > 0) {
+                e = hipMallocAsync(&async_buf, need, stream);
+                if (e != hipSuccess)
+                    return hip_fail(e, "hipMallocAsync(scratch)");
+                async_alloc = true;
+                codes = h->plan.coded ? static_cast<uint16_t *>(async_buf) : nullptr;
+                partials = pb ? reinterpret_cast<double *>(static_cast<unsigned char *>(async_buf) + codes_bytes)
+                              : nullptr;
+            }
+        }
+    }
     const int level = shape.level, splits = shape.splits;
     const int64_t tail_docs = n_docs - shape.head * dl;
     // tail blocks after a head are laid out in whole XCD columns (see the kernel)
     const int64_t tail_blocks = n_blocks - shape.head;
     const int64_t tail_slots = shape.head > 0 ? (tail_blocks + kXcds - 1) / kXcds * kXcds : tail_blocks;
     const int64_t n_wgs = shape.head + tail_slots * splits;
-    if (n_wgs > 0x7fffffff)
-        return fail(TREE_ENS_E_ARG, "too many documents for one launch");
-    ScoreFn fn = pick_kernel<MODE>(h->plan);
-    if (!fn)
-        return fail(TREE_ENS_E_ARG, "unsupported document block size");
-    hipError_t e = hipSuccess;
-    double *partials = nullptr;
-    bool own_scratch = false; // partials live in the handle's scratch
-    std::unique_lock<std::mutex> scratch_lock;
-    if (kScores && splits > 1) {
-        const size_t n_partials = size_t(splits) * size_t(tail_docs) * size_t(comps);
-        if (n_partials <= kScratchDoubles) {
-            scratch_lock = std::unique_lock<std::mutex>(h->scratch_mu);
-            if (h->scratch_used && h->scratch_stream != stream) {
-                e = hipStreamWaitEvent(stream, h->scratch_done, 0);
-                if (e != hipSuccess)
-                    return hip_fail(e, "hipStreamWaitEvent");
-            }
-            partials = h->d_scratch;
-            own_scratch = true;
-        } else {
-            e = hipMallocAsync(reinterpret_cast<void **>(&partials), n_partials * sizeof(double),
-                               stream);
-            if (e != hipSuccess)
-                return hip_fail(e, "hipMallocAsync(partials)");
-        }
-    }
     // walker packets (pk_recs > 0) stand in for the tiles: n_tiles is then packets per walker.
     // The feature trace of one-workgroup plans keeps the shared tiles: its bitmasks sit past
     // their zero record, where the packets' sub-slots reach.
@@ -1172,15 +1226,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     // coded models: one pass turns the float features into 16-bit threshold codes
     const void *docs = X;
     int32_t row_stride = n_features;
-    uint16_t *codes = nullptr;
     if (h->plan.coded) {
-        e = hipMallocAsync(reinterpret_cast<void **>(&codes),
-                           size_t(n_docs) * size_t(h->n_cols) * sizeof(uint16_t), stream);
-        if (e != hipSuccess) {
-            if (partials)
-                (void)hipFreeAsync(partials, stream);
-            return hip_fail(e, "hipMallocAsync(codes)");
-        }
         // documents per coding workgroup: enough workgroups to fill the GPU twice over, but
         // each one long enough to pay for loading its chunk's thresholds into LDS
         int64_t per_wg = 256;
@@ -1220,19 +1266,14 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
             e = hipGetLastError();
         }
     }
-    if (own_scratch) {
-        // the next call from another stream waits for this one's reduction
+    if (shared_scratch) {
+        // the next eager call from another stream waits for this one's reduction
         if (e == hipSuccess)
             e = hipEventRecord(h->scratch_done, stream);
         h->scratch_stream = stream;
         h->scratch_used = true;
-    } else if (partials) {
-        hipError_t e2 = hipFreeAsync(partials, stream);
-        if (e == hipSuccess)
-            e = e2;
-    }
-    if (codes) {
-        hipError_t e2 = hipFreeAsync(codes, stream);
+    } else if (async_alloc) {
+        hipError_t e2 = hipFreeAsync(async_buf, stream);
         if (e == hipSuccess)
             e = e2;
     }
