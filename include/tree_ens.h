@@ -131,6 +131,25 @@ int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t 
                      int32_t n_features, float *scores);
 
 /*
+ * tree_ens_predict_noalloc -- tree_ens_predict for callers that cannot allocate device memory
+ * during the call (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc). Arguments, results and errors as tree_ens_predict; the same kernels run.
+ *
+ * The call allocates nothing: no hipMalloc, hipMallocAsync or hipFree, no allocating library
+ * routine. Its scratch (the fp64 partial sums of document blocks split over several workgroups,
+ * and the 16-bit threshold codes of coded models) lives in one static device array of 16 MiB
+ * that the library holds on each device it runs on until the process ends. A batch whose split
+ * partial sums would not fit is launched without splits (every workgroup walks all trees of its
+ * block; the scores are the same within the documented tolerance); a batch whose threshold
+ * codes (n_docs x min_features x 2 bytes) exceed 16 MiB is refused with TREE_ENS_E_ARG.
+ * Every call on a device shares that device's array and leaves its contents behind: calls of
+ * this function that overlap in time on one device (different streams, or graph replays next to
+ * eager calls) race on it and must be ordered by the caller.
+ */
+int tree_ens_predict_noalloc(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                             int32_t n_features, float *scores);
+
+/*
  * tree_ens_predict_leaves -- the leaf each (document, tree) pair reaches, by the same walk.
  *
  *   leaf_ids  device, int32 [n_docs][n_trees] row-major: the tree-local id, in the caller's

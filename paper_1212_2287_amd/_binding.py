@@ -70,6 +70,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tree_ens_outputs.argtypes = [P, P, P]
     lib.tree_ens_predict.restype = ctypes.c_int
     lib.tree_ens_predict.argtypes = [P, P, P, i64, i32, P]
+    lib.tree_ens_predict_noalloc.restype = ctypes.c_int
+    lib.tree_ens_predict_noalloc.argtypes = [P, P, P, i64, i32, P]
     lib.tree_ens_predict_leaves.restype = ctypes.c_int
     lib.tree_ens_predict_leaves.argtypes = [P, P, P, i64, i32, P]
     lib.tree_ens_topk.restype = ctypes.c_int
@@ -194,7 +196,7 @@ def _check_docs(X):
         raise TypeError("X must be a contiguous float32 [n_docs, n_features] tensor")
 
 
-def tree_ens_predict(h, X, scores=None, stream=None, n_outputs=None):
+def tree_ens_predict(h, X, scores=None, stream=None, n_outputs=None, _noalloc=False):
     """Scores of the documents ``X`` (device float32 [n_docs, n_features]) as float32 [n_docs]
     (or [n_docs, n_outputs] for a handle with several outputs), enqueued on ``stream``
     (default: torch's current stream for X's device)."""
@@ -210,10 +212,19 @@ def tree_ens_predict(h, X, scores=None, stream=None, n_outputs=None):
             not scores.is_contiguous() or scores.device != X.device:
         raise TypeError("scores must be a contiguous float32 tensor of n_docs * n_outputs entries "
                         "on X's device")
-    rc = load_library().tree_ens_predict(h, _stream_of(X, stream), X.data_ptr() if n_docs else None,
-                                         n_docs, n_feat, scores.data_ptr() if n_docs else None)
-    _check(rc, "tree_ens_predict")
+    fn = "tree_ens_predict_noalloc" if _noalloc else "tree_ens_predict"
+    rc = getattr(load_library(), fn)(h, _stream_of(X, stream), X.data_ptr() if n_docs else None,
+                                     n_docs, n_feat, scores.data_ptr() if n_docs else None)
+    _check(rc, fn)
     return scores
+
+
+def tree_ens_predict_noalloc(h, X, scores, stream=None, n_outputs=None):
+    """tree_ens_predict through the allocation-free entry point: ``scores`` must be given (a
+    device float32 tensor of n_docs * n_outputs entries); the library allocates nothing."""
+    if scores is None:
+        raise TypeError("tree_ens_predict_noalloc needs a preallocated scores tensor")
+    return tree_ens_predict(h, X, scores, stream, n_outputs, _noalloc=True)
 
 
 def tree_ens_predict_leaves(h, X, leaf_ids=None, stream=None):
@@ -380,6 +391,9 @@ class TreeEnsemble:
 
     def predict(self, X, out=None, stream=None):
         return tree_ens_predict(self.handle, X, out, stream, self.n_outputs)
+
+    def predict_noalloc(self, X, out, stream=None):
+        return tree_ens_predict_noalloc(self.handle, X, out, stream, self.n_outputs)
 
     def predict_leaves(self, X, out=None, stream=None):
         return tree_ens_predict_leaves(self.handle, X, out, stream)

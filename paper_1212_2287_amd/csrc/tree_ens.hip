@@ -906,6 +906,34 @@ struct tree_ens {
 
 namespace {
 constexpr size_t kScratchDoubles = size_t(1) << 17; // 1 MiB of split partials
+
+// Scratch of the allocation-free entry point (tree_ens_predict_noalloc): split partial sums and
+// threshold codes in one static array, which every device the library runs on holds until the
+// process ends. In host code `scratch` is only a stand-in for the symbol: its device address
+// comes from hipGetSymbolAddress, once per device, and only that address reaches a kernel or a
+// copy.
+constexpr size_t kStaticScratchBytes = size_t(16) << 20; // 16 MiB
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+unsigned char *g_static_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device` (the current device), looked up on the first use.
+int static_scratch(int device, unsigned char **out) {
+    if (device < 0 || device >= kMaxDevices)
+        return fail(TREE_ENS_E_DEVICE, "device index beyond the allocation-free scratch table");
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    if (!g_static_ptr[device]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)");
+        g_static_ptr[device] = static_cast<unsigned char *>(p);
+    }
+    *out = g_static_ptr[device];
+    return TREE_ENS_OK;
+}
 } // namespace
 
 namespace {
@@ -1091,10 +1119,17 @@ int check_predict_args(const tree_ens *h, const float *X, int64_t n_docs, int32_
 // four outputs); kModeLeaves writes leaf_ids [n_docs][n_trees]; kModeUsage writes per-document
 // feature counts into leaf_ids and, if masks is not NULL, the bitmasks (rows of mask_words
 // words).
+// Where a call's scratch (split partial sums, threshold codes) comes from.
+enum class ScratchSource {
+    kHandle, // the handle's shared buffer or stream-ordered allocations (eager calls), a buffer
+             // of the call's own kept by the handle (calls captured into a graph)
+    kStatic, // the library's static device array only (tree_ens_predict_noalloc)
+};
+
 template <int MODE>
 int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_t n_docs,
                    int32_t n_features, float *scores, int32_t *leaf_ids, uint32_t *masks = nullptr,
-                   int32_t mask_words = 0) {
+                   int32_t mask_words = 0, ScratchSource source = ScratchSource::kHandle) {
     constexpr bool kScores = MODE == kModeScore || MODE == kModeVector; // split partial sums
     // entries per document in the partial sums, and launches (four outputs each)
     const int comps = MODE == kModeVector ? kVecPerLaunch : 1;
@@ -1135,8 +1170,9 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         }
     }
     {
-        // grid of the chosen shape: every tail block split into the shape's splits, plus the
-        // padding to whole XCD columns
+        // grid of the chosen shape (the no-split shape the allocation-free path may fall back
+        // to is never larger): every tail block split into the shape's splits, plus the padding
+        // to whole XCD columns
         const int64_t tail_blocks = n_blocks - shape.head;
         const int64_t tail_slots = shape.head > 0 ? (tail_blocks + kXcds - 1) / kXcds * kXcds : tail_blocks;
         if (shape.head + tail_slots * shape.splits > 0x7fffffff)
@@ -1161,7 +1197,23 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     bool async_alloc = false;    // partials and codes from hipMallocAsync, freed on the stream
     void *async_buf = nullptr;
     std::unique_lock<std::mutex> scratch_lock;
-    {
+    if (source == ScratchSource::kStatic) {
+        // the static array only: a shape whose partials do not fit takes no splits (every
+        // workgroup walks all tiles of its block); codes that do not fit are an error
+        if (codes_bytes > kStaticScratchBytes)
+            return fail(TREE_ENS_E_ARG,
+                        "the batch's threshold codes (" + std::to_string(codes_bytes) +
+                            " bytes) exceed the allocation-free scratch of " +
+                            std::to_string(kStaticScratchBytes) + " bytes");
+        if (codes_bytes + partial_bytes(shape) > kStaticScratchBytes)
+            shape = LaunchShape{0, n_blocks, 1};
+        unsigned char *base = nullptr;
+        const int rc = static_scratch(h->device, &base);
+        if (rc != TREE_ENS_OK)
+            return rc;
+        codes = h->plan.coded ? reinterpret_cast<uint16_t *>(base) : nullptr;
+        partials = partial_bytes(shape) ? reinterpret_cast<double *>(base + codes_bytes) : nullptr;
+    } else {
         hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
         if (hipStreamIsCapturing(stream, &cap) != hipSuccess)
             cap = hipStreamCaptureStatusNone;
@@ -1440,6 +1492,25 @@ int tree_ens_predict(const tree_ens_t *h, void *stream, const float *X, int64_t 
         return e == hipSuccess ? TREE_ENS_OK : hip_fail(e, "specialised kernel launch");
     }
     return launch_predict<kModeScore>(h, s, X, n_docs, n_features, scores, nullptr);
+}
+
+int tree_ens_predict_noalloc(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
+                             int32_t n_features, float *scores) {
+    g_err.clear();
+    int rc = check_predict_args(h, X, n_docs, n_features, scores);
+    if (rc != TREE_ENS_OK || n_docs == 0)
+        return rc;
+    DeviceGuard g(h->device);
+    if (g.err != hipSuccess)
+        return hip_fail(g.err, "hipSetDevice");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (h->n_trees == 0 || h->cg_fn)
+        return tree_ens_predict(h, stream, X, n_docs, n_features, scores); // no scratch used
+    if (h->n_outputs > 1)
+        return launch_predict<kModeVector>(h, s, X, n_docs, n_features, scores, nullptr, nullptr, 0,
+                                           ScratchSource::kStatic);
+    return launch_predict<kModeScore>(h, s, X, n_docs, n_features, scores, nullptr, nullptr, 0,
+                                      ScratchSource::kStatic);
 }
 
 int tree_ens_predict_leaves(const tree_ens_t *h, void *stream, const float *X, int64_t n_docs,
