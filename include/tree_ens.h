@@ -32,7 +32,7 @@ typedef struct tree_ens tree_ens_t;
 #define TREE_ENS_E_ARG (-1)    /* a null pointer where one is required, a negative count, a
                                   misaligned pointer, or unknown flag bits */
 #define TREE_ENS_E_MODEL (-2)  /* the flat arrays do not describe an ensemble of trees (see
-                                  tree_ens_create), or a tree is too large for one LDS tile */
+                                  tree_ens_create), or a tree has more than 65,535 nodes */
 #define TREE_ENS_E_SHAPE (-3)  /* the documents carry fewer features than the model reads */
 #define TREE_ENS_E_DEVICE (-4) /* a HIP call failed (no device, launch or copy error) */
 #define TREE_ENS_E_NOMEM (-5)  /* host or device allocation failed */
@@ -70,8 +70,10 @@ typedef struct tree_ens tree_ens_t;
  * All arrays are host memory, read during the call only; the caller keeps ownership. Node ids
  * need not be in any particular order. TREE_ENS_E_MODEL is returned when a child id is out of
  * range or names the root, a node has two parents, a node is unreachable from the root, a
- * threshold is NaN, a feature id is below -1, a tree has more nodes than one LDS tile holds
- * (reported in the message), or a feature id exceeds the LDS document-tile limit. Validation
+ * threshold is NaN, a feature id is below -1, a tree has more than 65,535 nodes (32,768
+ * leaves), or a feature id exceeds the LDS document-tile limit. Trees too large for one LDS
+ * tile (a few thousand leaves, depending on the feature count) are accepted: they are walked
+ * from device memory (their records stay in L2) instead of being staged in LDS, more slowly. Validation
  * happens before any HIP call, so model errors are reported on a host without a GPU. The
  * handle owns the device copy and is immutable; it may be used from several streams at once.
  */
@@ -217,7 +219,8 @@ int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int
  *   packed_bytes   bytes of node records (8 per node); the device also holds the tile images
  *                  built from them (one set per tiling granularity) and, for models whose
  *                  groups of trees fit, the per-wave packets (one more copy of the records).
- *   n_tiles        LDS tiles the trees are streamed in for a large batch.
+ *   n_tiles        LDS tiles the tiled trees are streamed in for a large batch (trees too
+ *                  large for one tile are walked from device memory and not counted).
  *   docs_per_block documents a workgroup stages in LDS (a power of two from 8 to 64).
  */
 int tree_ens_info(const tree_ens_t *h, int32_t *n_trees, int32_t *min_features,

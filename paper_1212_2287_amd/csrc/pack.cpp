@@ -187,62 +187,93 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     }
 
     const int32_t n_cols = max_fid + 1;
-    const double avg_tree_bytes = n_trees > 0 ? 8.0 * double(n_nodes) / n_trees : 0.0;
-    LdsPlan plan = plan_lds(n_cols, avg_tree_bytes, 4);
-
-    // ---- coded features: per-feature sorted distinct thresholds -----------------------------
-    // Used when float features would leave fewer than 64 documents per block and every
-    // feature's thresholds fit one coding workgroup and 16-bit codes.
-    std::vector<std::vector<float>> thr_of;
-    // Coding pays when float documents leave too few per block for the model's trees: when a
-    // float tile cannot hold one tree for each walker, most walkers would idle.
-    bool coded = plan.docs_per_block > 0 && plan.docs_per_block < 64 &&
-                 avg_tree_bytes * (1024 / plan.docs_per_block) > plan.tile_bytes;
     auto canon = [&](float th) {
         float v = strict ? strict_to_inclusive(th) : th;
         return v == 0.0f ? 0.0f : v; // fold -0.0 into +0.0 (equal under every comparison)
     };
-    if (coded) {
-        thr_of.assign(size_t(n_cols), {});
-        for (int64_t i = 0; i < n_nodes && coded; i++) {
-            if (feature[i] < 0)
-                continue;
-            const float v = canon(threshold[i]);
-            if (!std::isnan(v))
-                thr_of[size_t(feature[i])].push_back(v);
+
+    // ---- coded features: per-feature sorted distinct thresholds -----------------------------
+    // Possible when every feature's thresholds fit one coding workgroup and 16-bit codes; used
+    // when float documents leave too few per block for the model's trees (below).
+    std::vector<std::vector<float>> thr_of;
+    int code_ok = -1; // -1: not computed yet
+    auto can_code = [&]() {
+        if (code_ok < 0) {
+            code_ok = 1;
+            thr_of.assign(size_t(n_cols), {});
+            for (int64_t i = 0; i < n_nodes; i++) {
+                if (feature[i] < 0)
+                    continue;
+                const float v = canon(threshold[i]);
+                if (!std::isnan(v))
+                    thr_of[size_t(feature[i])].push_back(v);
+            }
+            for (auto &tv : thr_of) {
+                std::sort(tv.begin(), tv.end());
+                tv.erase(std::unique(tv.begin(), tv.end()), tv.end());
+                if (tv.size() > kMaxCode || tv.size() > size_t(kCodeTableFloats))
+                    code_ok = 0;
+            }
         }
-        for (auto &tv : thr_of) {
-            std::sort(tv.begin(), tv.end());
-            tv.erase(std::unique(tv.begin(), tv.end()), tv.end());
-            if (tv.size() > kMaxCode || tv.size() > size_t(kCodeTableFloats))
-                coded = false;
-        }
+        return code_ok == 1;
+    };
+
+    // ---- LDS plan and the trees too large for one tile ---------------------------------------
+    // A tree whose records (plus a tile's header and K root copies) exceed the plan's tile slot
+    // is a "big" tree: it stays out of the tiles and is walked from device memory. The plan
+    // depends on the mean size of the tiled trees, and the slot size on the plan, so the two are
+    // settled together (a few rounds at most; the last plan's slot decides).
+    std::vector<uint8_t> is_big(size_t(n_trees), 0);
+    LdsPlan plan{};
+    bool coded = false;
+    int64_t max_nodes_per_tree = 0;
+    for (int round = 0; round < 4; round++) {
+        int64_t small_nodes = 0, n_small_trees = 0;
+        for (int32_t t = 0; t < n_trees; t++)
+            if (!is_big[size_t(t)]) {
+                small_nodes += tree_offsets[t + 1] - tree_offsets[t];
+                n_small_trees++;
+            }
+        const double avg_tree_bytes = n_small_trees > 0 ? 8.0 * double(small_nodes) / double(n_small_trees) : 0.0;
+        plan = plan_lds(n_cols, avg_tree_bytes, 4);
+        // Coding pays when float documents leave too few per block for the model's trees: when
+        // a float tile cannot hold one tree for each walker, most walkers would idle.
+        coded = plan.docs_per_block > 0 && plan.docs_per_block < 64 &&
+                avg_tree_bytes * (1024 / plan.docs_per_block) > plan.tile_bytes && can_code();
         if (coded)
             plan = plan_lds(n_cols, avg_tree_bytes, 2);
+        if (plan.docs_per_block == 0)
+            break;
+        // a one-tree tile holds the fixed header words and the root copies (padded to K records)
+        max_nodes_per_tree = plan.tile_bytes / int64_t(sizeof(NodeRec)) - (kHeaderFixedWords / 2 + plan.interleave);
+        bool changed = false;
+        for (int32_t t = 0; t < n_trees; t++) {
+            const uint8_t big = tree_offsets[t + 1] - tree_offsets[t] > max_nodes_per_tree;
+            changed |= big != is_big[size_t(t)];
+            is_big[size_t(t)] = big;
+        }
+        if (!changed)
+            break;
     }
     if (plan.docs_per_block == 0) {
         err = "feature id " + std::to_string(max_fid) + " is beyond the LDS document-tile limit (" +
               std::to_string(kXsMaxBytes / (8 * 4) - 2) + ")";
         return kErrModel;
     }
-    // a one-tree tile holds the fixed header words and the root copies (padded to K records)
-    const int64_t header1 = kHeaderFixedWords / 2 + plan.interleave;
-    const int64_t max_nodes_per_tree = plan.tile_bytes / int64_t(sizeof(NodeRec)) - header1;
+    // the final plan's slot decides which trees are tiled
     int64_t largest_tree = 0;
-    for (int32_t t = 0; t < n_trees; t++)
-        largest_tree = std::max<int64_t>(largest_tree, tree_offsets[t + 1] - tree_offsets[t]);
+    int32_t n_small = 0;
+    for (int32_t t = 0; t < n_trees; t++) {
+        const int64_t n = tree_offsets[t + 1] - tree_offsets[t];
+        is_big[size_t(t)] = n > max_nodes_per_tree;
+        if (!is_big[size_t(t)]) {
+            largest_tree = std::max(largest_tree, n);
+            n_small++;
+        }
+    }
     // the narrow format needs column offsets below 64 KiB and links below 2^16 (absolute LDS
     // record indices are below 160 KiB / 8 = 20480; tree-relative ones below the tree's size)
     plan.narrow = (plan.xs_bytes <= 65536 && largest_tree <= kNarrowMaxTreeNodes) ? 1 : 0;
-    for (int32_t t = 0; t < n_trees; t++) {
-        const int64_t n = tree_offsets[t + 1] - tree_offsets[t];
-        if (n > max_nodes_per_tree) {
-            err = "tree " + std::to_string(t) + " has " + std::to_string(n) +
-                  " nodes; one LDS tile holds at most " + std::to_string(max_nodes_per_tree) +
-                  " at this feature count";
-            return kErrModel;
-        }
-    }
 
     // ---- tree order: expected lockstep length ----------------------------------------------
     // A wave steps through a tree until the longest of its 64 documents' paths ends, so the trees
@@ -320,22 +351,27 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     p.tree_orig.resize(size_t(n_trees));
     std::iota(p.tree_orig.begin(), p.tree_orig.end(), 0);
     std::stable_sort(p.tree_orig.begin(), p.tree_orig.end(), [&](int32_t x, int32_t y) {
+        if (is_big[size_t(x)] != is_big[size_t(y)])
+            return is_big[size_t(x)] < is_big[size_t(y)]; // tiled trees first, big ones last
         if (lock_key[size_t(x)] != lock_key[size_t(y)])
             return lock_key[size_t(x)] > lock_key[size_t(y)];
         if (complete_tree[size_t(x)] != complete_tree[size_t(y)])
             return complete_tree[size_t(x)] > complete_tree[size_t(y)];
         return depth_of[size_t(x)] > depth_of[size_t(y)];
     });
+    p.n_small = n_small;
     p.nodes.reserve(size_t(n_nodes));
     p.orig_id.reserve(size_t(n_nodes));
     p.tree_node_off.resize(size_t(n_trees) + 1, 0);
     p.tree_depth.resize(size_t(n_trees), 0);
     std::vector<int32_t> new_id;
-    auto link = [&](uint32_t child) {
-        return plan.narrow ? child << 16 : child << kWideChildShift;
-    };
     for (int32_t pt = 0; pt < n_trees; pt++) {
         const int32_t t = p.tree_orig[size_t(pt)];
+        // big trees (packed last) take the big-tree record format (see kBigLinkShift)
+        const bool big_tree = pt >= n_small;
+        auto link = [&](uint32_t child) {
+            return big_tree ? child << kBigLinkShift : plan.narrow ? child << 16 : child << kWideChildShift;
+        };
         const int64_t a = tree_offsets[t];
         const int64_t n = tree_offsets[t + 1] - a;
         // breadth-first numbering in which the two children of a node take adjacent slots
@@ -372,8 +408,9 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                                                : uint32_t(std::lower_bound(tv.begin(), tv.end(), v) -
                                                           tv.begin()) + 1u;
                 }
-                const uint32_t col = uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) *
-                                     uint32_t(plan.elem_bytes);
+                const uint32_t col = big_tree ? uint32_t(feature[a + i] + 1)
+                                              : uint32_t(feature[a + i] + 1) * uint32_t(plan.docs_per_block) *
+                                                    uint32_t(plan.elem_bytes);
                 r.w = link(uint32_t(new_id[size_t(left[a + i])])) | col;
             } else if (vec) {
                 // never 0: a coded leaf (code 0 >= thr is false) stays put as well
@@ -407,16 +444,16 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         p.level_begin[k] = int32_t(p.tiles.size());
         const int64_t budget = std::max<int64_t>(plan.tile_bytes >> k, 16);
         int32_t tb = 0;
-        while (tb < n_trees) {
+        while (tb < n_small) {
             int32_t fit = 0;
-            for (int64_t recs = 0; tb + fit < n_trees && fit < kMaxTileTrees; fit++) {
+            for (int64_t recs = 0; tb + fit < n_small && fit < kMaxTileTrees; fit++) {
                 const int64_t nn = int64_t(p.tree_node_off[size_t(tb + fit) + 1] -
                                            p.tree_node_off[size_t(tb + fit)]);
                 if (fit > 0 && (header_recs(fit + 1) + recs + nn) * 8 > budget)
                     break;
                 recs += nn;
             }
-            const int32_t limit = (fit > round && tb + fit < n_trees) ? fit / round * round : fit;
+            const int32_t limit = (fit > round && tb + fit < n_small) ? fit / round * round : fit;
             int32_t te = tb;
             int32_t dmax = 0;
             int32_t complete = -2; // -2: no tree yet
@@ -496,7 +533,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
     }
 
     // ---- walker packets (plans of 64- or 32-document blocks; see pack.hpp) -----------------------
-    if ((plan.docs_per_block == 64 || plan.docs_per_block == 32) && n_trees > 0) {
+    if ((plan.docs_per_block == 64 || plan.docs_per_block == 32) && n_small > 0) {
         constexpr int32_t W = kPacketWalkers;       // waves, one packet stream each
         const int32_t P = 64 / plan.docs_per_block; // walkers per wave
         const int32_t HW = W * P;                   // walkers
@@ -507,13 +544,13 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         const int32_t sub = int32_t(std::max<int64_t>(region, 0) / 8 / W / 64 * 64); // records per sub-slot
         const int32_t part = sub / P; // records of one walker's part of a packet
         const int32_t pk_zero = half ? plan.zero_rec : plan.xs_bytes + W * sub * 8;
-        const int32_t n_groups = (n_trees + K - 1) / K;
+        const int32_t n_groups = (n_small + K - 1) / K;
         // walker h of wave v (walker index v * P + h) takes groups v * P + h + r * HW, r = 0, 1, ...
         auto group_of = [&](int32_t v, int32_t h, int32_t r) { return v * P + h + r * HW; };
         auto group_recs = [&](int32_t g) {
             if (g >= n_groups)
                 return int64_t(0); // past the last group: zero roots, no records
-            const int32_t t0 = g * K, t1 = std::min(n_trees, t0 + K);
+            const int32_t t0 = g * K, t1 = std::min(n_small, t0 + K);
             return int64_t(p.tree_node_off[size_t(t1)]) - int64_t(p.tree_node_off[size_t(t0)]);
         };
         auto packet_recs = [&](int32_t ng, int64_t tree_recs) {
@@ -575,7 +612,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                         for (int32_t j = 0; j < ng; j++) {
                             for (int32_t i = 0; i < K; i++) {
                                 const int32_t t = group_of(v, h, r0 + j) * K + i;
-                                if (t >= n_trees)
+                                if (t >= n_small)
                                     continue;
                                 const int32_t d = int32_t(p.tree_depth[size_t(t)]);
                                 const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
@@ -596,7 +633,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                             for (int32_t i = 0; i < K; i++) {
                                 const int32_t t = group_of(v, h, r0 + j) * K + i;
                                 NodeRec root = zero_leaf;
-                                if (t < n_trees) {
+                                if (t < n_small) {
                                     const uint32_t first = p.tree_node_off[size_t(t)];
                                     const uint32_t nn = p.tree_node_off[size_t(t) + 1] - first;
                                     const uint32_t tree_rec = base + uint32_t(pos);

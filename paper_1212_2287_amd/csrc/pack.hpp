@@ -37,8 +37,19 @@ static_assert(sizeof(NodeRec) == 8, "node record must be 8 bytes");
 constexpr int kWideChildShift = 17;
 constexpr uint32_t kNarrowColMask = 0xffffu;
 constexpr uint32_t kWideColMask = (1u << kWideChildShift) - 1; // column offsets < 128 KiB
-constexpr int kMaxTreeNodes = 1 << (32 - kWideChildShift);    // 32768 nodes per tree
 constexpr int kNarrowMaxTreeNodes = 1 << 16;                    // 16-bit child index
+// Largest tree accepted (nodes): 32,768 leaves.
+constexpr int kMaxTreeNodes = 65535;
+
+// Big trees: a tree whose records do not fit one LDS tile slot (with the tile's header and K
+// root copies) is not tiled. It is packed after all tiled trees, in its own record format, and
+// the scoring kernel walks it from device memory (the records stay in L2), reading the
+// documents' features from the staged LDS tile as for every other tree:
+//   w = (tree-relative left child << kBigLinkShift) | column index (f + 1; 0 for a leaf)
+// with thr as in NodeRec. The right child follows the left one, a leaf links to itself, and
+// column 0 is the NaN (or code 0) column, so leaves absorb further steps here too.
+constexpr int kBigLinkShift = 16;
+constexpr uint32_t kBigColMask = 0xffffu;
 
 // A run of whole trees [tree_begin, tree_end) (packed order) staged into LDS together.
 struct Tile {
@@ -135,6 +146,7 @@ constexpr int kUsageHalfBytes = ((kTwoWgXsBytes / (64 * 4) - 1 + 31) / 32) * 64 
 
 struct Packed {
     int32_t n_trees = 0;
+    int32_t n_small = 0;   // trees [0, n_small) are tiled; [n_small, n_trees) are big trees
     int32_t n_cols = 0;    // 1 + largest feature id read (0 if none)
     int32_t max_depth = 0; // over all trees
     LdsPlan plan{};

@@ -137,7 +137,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
              const int32_t *__restrict__ tree_orig, int32_t n_trees,
              uint32_t *__restrict__ masks, int32_t mask_words, int32_t usage_off,
              const float4 *__restrict__ leaf_vec, int32_t vec_stride4, int32_t n_out,
-             int32_t chunk, double out_scale, int32_t pk_recs) {
+             int32_t chunk, double out_scale, int32_t pk_recs, const uint2 *__restrict__ big,
+             int32_t n_small, uint32_t big_off0) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
@@ -531,7 +532,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 const unsigned char *rc = lds + 8 * (base + treeens::kPacketHeaderRecs + j * K);
                 auto tree_of = [&](int i) {
                     const int gt = (first_group + j * n_walkers) * K + i;
-                    return gt < n_trees ? make_int2(gt, int(first_rec[j * K + i])) : make_int2(-1, 0);
+                    return gt < n_small ? make_int2(gt, int(first_rec[j * K + i])) : make_int2(-1, 0);
                 };
                 walk_group(rc, complete_tag, complete_depth, tree_of);
             }
@@ -608,6 +609,51 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 fetch_window(win[d], ti + d + kDepth);
                 if (d == 0 || ti + d < t_hi)
                     walk_tile();
+            }
+        }
+    }
+    // Big trees (too large for a tile; packed after the tiled ones): walked from device memory,
+    // one tree per walker at a time, the records staying in L2. A record is {thr, w} with
+    // w = (tree-relative left child << 16) | column index; the features come from the LDS
+    // document tile as for every other tree, and leaves absorb further steps (column 0). Big
+    // tree b goes to split b % n_splits and, within it, to walker (b / n_splits) % n_walkers.
+    if (n_small < n_trees) {
+        __syncthreads(); // the document tile is written (no tile may have been walked)
+        const int n_big = n_trees - n_small;
+        for (int b = split + n_splits * walker; b < n_big; b += n_splits * n_walkers) {
+            const int gt = n_small + b;
+            const uint2 *tr = big + (tree_node_off[gt] - big_off0);
+            uint2 r = tr[0];
+            for (;;) {
+                const uint32_t fa = ((r.y & treeens::kBigColMask) << kColShift) | lane_off;
+                const Elem x = *reinterpret_cast<const Elem *>(lds + fa);
+                if constexpr (USAGE) {
+                    const uint32_t col = r.y & treeens::kBigColMask;
+                    if (col > 0u)
+                        atomicOr(&umask[((col - 1u) >> 5) * DL + dl], 1u << ((col - 1u) & 31u));
+                }
+                if (__builtin_amdgcn_ballot_w64(fa >= kLeafCol) == 0)
+                    break;
+                bool right;
+                if constexpr (CODED)
+                    right = uint32_t(x) >= r.x;
+                else
+                    right = x >= __uint_as_float(r.x);
+                r = tr[(r.y >> treeens::kBigLinkShift) + (right ? 1u : 0u)];
+            }
+            if constexpr (LEAVES) {
+                const int64_t doc = doc0 + dl;
+                if (doc < n_docs)
+                    leaf_ids[doc * n_trees + tree_orig[gt]] =
+                        orig_id[tree_node_off[gt] + (r.y >> treeens::kBigLinkShift)];
+            } else if constexpr (VEC) {
+                const float4 v = leaf_vec[int64_t(r.x - 1u) * vec_stride4 + chunk];
+                accv[0] += double(v.x);
+                accv[1] += double(v.y);
+                accv[2] += double(v.z);
+                accv[3] += double(v.w);
+            } else if constexpr (!USAGE) {
+                acc += double(__uint_as_float(r.x));
             }
         }
     }
@@ -786,7 +832,7 @@ using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *,
                          const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
                          float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
                          int32_t, uint32_t *, int32_t, int32_t, const float4 *, int32_t,
-                         int32_t, int32_t, double, int32_t);
+                         int32_t, int32_t, double, int32_t, const uint2 *, int32_t, uint32_t);
 
 template <int DL, bool HALF, bool NARROW, bool CODED, int MODE>
 ScoreFn pick_k(int k) {
@@ -865,6 +911,11 @@ struct tree_ens {
     int32_t pk_max_groups = 0;
     int64_t pk_total_rounds = 0;
     uint2 *d_packets = nullptr;
+    // big trees (packed indices [n_small, n_trees)): their records in the big-tree format, the
+    // first at packed node offset big_off0
+    int32_t n_small = 0;
+    uint32_t big_off0 = 0;
+    uint2 *d_big = nullptr;
     // leaf-id output: packed tree -> input tree, packed node -> input node id
     uint32_t *d_tree_node_off = nullptr;
     int32_t *d_tree_orig = nullptr;
@@ -941,6 +992,7 @@ namespace {
 void free_device(tree_ens *h) {
     (void)hipFree(h->d_images);
     (void)hipFree(h->d_packets);
+    (void)hipFree(h->d_big);
     (void)hipFree(h->d_tile_recs);
     (void)hipFree(h->d_tree_node_off);
     (void)hipFree(h->d_tree_orig);
@@ -1302,7 +1354,8 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                            partials, scores, leaf_ids, h->d_orig_id, h->d_tree_node_off,
                            h->d_tree_orig, h->n_trees, masks, mask_words, usage_off,
                            reinterpret_cast<const float4 *>(h->d_leaf_vec), h->vec_stride / 4, n_out,
-                           chunk, scale, pk ? h->pk_recs : 0);
+                           chunk, scale, pk ? h->pk_recs : 0, h->d_big, h->n_small,
+                           h->big_off0);
         e = hipGetLastError();
         if (e == hipSuccess && partials) {
             // the tail blocks' entries, in [doc][component] order
@@ -1419,6 +1472,13 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
         std::vector<uint2> packets(p.packets.size());
         std::memcpy(packets.data(), p.packets.data(), p.packets.size() * sizeof(NodeRec));
         e = upload(&h->d_packets, packets);
+    }
+    h->n_small = p.n_small;
+    h->big_off0 = p.tree_node_off[size_t(p.n_small)];
+    if (e == hipSuccess && p.n_small < p.n_trees) {
+        std::vector<uint2> big(p.nodes.size() - h->big_off0);
+        std::memcpy(big.data(), p.nodes.data() + h->big_off0, big.size() * sizeof(NodeRec));
+        e = upload(&h->d_big, big);
     }
     if (e == hipSuccess)
         e = upload(&h->d_tree_node_off, p.tree_node_off);

@@ -76,9 +76,9 @@ const char *emu_message(void) { return g_msg.c_str(); }
 
 // Walk all documents through tiling `level`. Outputs leaf ids [n_docs][n_trees] (input node ids)
 // and fp64 scores [n_docs][n_outputs] (vector-valued leaves read through the leaf-vector table).
-// plan_out (9 ints): docs per block, trees per lane, record format, coded, tiles at tiling 0,
+// plan_out (10 ints): docs per block, trees per lane, record format, coded, tiles at tiling 0,
 // LDS bytes, tile slot bytes, records of the largest tiling-0 image, walker sub-slot records
-// (0: shared tiles). Returns 0, or 1 with a message naming the first violated
+// (0: shared tiles), tiled trees (the rest are big trees walked from device memory). Returns 0, or 1 with a message naming the first violated
 // invariant, or a negative packer status.
 int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
              const float *threshold, const int32_t *left, const int32_t *right, const float *value,
@@ -103,6 +103,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
         plan_out[6] = pl.tile_bytes;
         plan_out[7] = p.level_slot_recs[0];
         plan_out[8] = p.pk_recs;
+        plan_out[9] = p.n_small;
     }
     const int DL = pl.docs_per_block, K = pl.interleave, E = pl.elem_bytes;
     const int shift = pl.narrow ? 16 : treeens::kWideChildShift;
@@ -279,6 +280,66 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
             return 0;
         };
 
+        // big trees: records read from the packed array in the big-tree format (tree-relative
+        // links, column indices), features from the LDS document tile
+        for (int32_t gt = p.n_small; gt < n_trees; gt++) {
+            const uint32_t first = p.tree_node_off[size_t(gt)];
+            const int64_t tree_n = int64_t(p.tree_node_off[size_t(gt) + 1]) - int64_t(first);
+            for (int dl = 0; dl < DL && doc0 + dl < n_docs; dl++) {
+                const int64_t doc = doc0 + dl;
+                int64_t cur = 0;
+                int steps = 0;
+                auto step = [&](int64_t at, bool *internal) -> int64_t {
+                    const treeens::NodeRec r = p.nodes[size_t(first) + size_t(at)];
+                    const uint32_t col = r.w & treeens::kBigColMask;
+                    if (col > uint32_t(p.n_cols))
+                        return -2;
+                    const uint32_t fa = col * uint32_t(DL * E) + uint32_t(dl * E);
+                    *internal = fa >= leaf_col;
+                    bool right_side;
+                    if (E == 4) {
+                        float x;
+                        std::memcpy(&x, lds.data() + fa, 4);
+                        right_side = x >= as_float(r.thr_bits);
+                    } else {
+                        uint16_t x;
+                        std::memcpy(&x, lds.data() + fa, 2);
+                        right_side = uint32_t(x) >= r.thr_bits;
+                    }
+                    return int64_t(r.w >> treeens::kBigLinkShift) + (right_side ? 1 : 0);
+                };
+                for (;;) {
+                    bool internal = false;
+                    const int64_t nxt = step(cur, &internal);
+                    if (nxt == -2)
+                        return bad("big tree: column index beyond the document tile");
+                    if (!internal) {
+                        if (nxt != cur)
+                            return bad("big tree: a leaf does not absorb a further step");
+                        break;
+                    }
+                    if (nxt < 0 || nxt >= tree_n)
+                        return bad("big tree: child outside the tree's records");
+                    cur = nxt;
+                    if (++steps > p.max_depth + 1)
+                        return bad("big tree: walk longer than the deepest tree");
+                }
+                const treeens::NodeRec r = p.nodes[size_t(first) + size_t(cur)];
+                leaf_ids[doc * n_trees + p.tree_orig[size_t(gt)]] = p.orig_id[size_t(first) + size_t(cur)];
+                if (vec) {
+                    const int64_t row = int64_t(r.thr_bits) - 1;
+                    if (row < 1 || row > int64_t(p.nodes.size()))
+                        return bad("big tree: leaf names a row outside the leaf-vector table");
+                    for (int c = 0; c < n_outputs; c++)
+                        scores[doc * n_outputs + c] +=
+                            double(p.leaf_vec[size_t(row) * size_t(p.vec_stride) + size_t(c)]);
+                } else {
+                    scores[doc] += double(as_float(r.thr_bits));
+                }
+            }
+            seen[size_t(p.tree_orig[size_t(gt)])]++;
+        }
+
         if (p.pk_recs > 0) {
             // each walker copies its packets, in order, into its own sub-slot and walks them;
             // padding links to the packets' zero record (the plan's own in two-workgroup plans)
@@ -321,7 +382,7 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                                 // the kernel reads two roots per 16-byte read when K is even
                                 if (K % 2 == 0 && i % 2 == 0 && root_copy % 16 != 0)
                                     return bad("packet: a pair of root copies is not 16-byte aligned");
-                                if (gt >= n_trees) {
+                                if (gt >= p.n_small) {
                                     if (std::memcmp(lds.data() + root_copy, lds.data() + pzero, 8) != 0)
                                         return bad("packet: padding root is not the zero record");
                                     continue;

@@ -93,7 +93,7 @@ int check_file(const char *path) {
         const int cg = treeens::codegen_source(n_trees, off.data(), feature.data(), threshold.data(),
                                                left.data(), right.data(), value.data(), uint32_t(rule), src, err);
         for (int level = 0; level < treeens::kTileLevels; level++) {
-            int32_t plan[9] = {};
+            int32_t plan[10] = {};
             const int erc = emu_walk(n_trees, off.data(), feature.data(), threshold.data(), left.data(),
                                      right.data(), value.data(), n_outputs, uint32_t(rule), X.data(), n_docs,
                                      n_features, level, e_leaves.data(), e_scores.data(), plan);

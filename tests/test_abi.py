@@ -76,14 +76,15 @@ def test_model_errors_are_reported_without_a_device():
 
 
 def test_oversized_tree_is_rejected():
-    # one tree with more nodes than an LDS tile holds at 136 features
-    n_leaves = 7000
+    # 65,535 nodes (32,768 leaves) is the largest tree accepted; a tree of 32,769 leaves is
+    # refused during validation, before any device call
+    n_leaves = 32769
     fe, le, ri = W.grow_random_structure(np.random.default_rng(0), n_leaves, None, 136)
     n = fe.shape[0]
     ens = W.Ensemble(np.array([0, n], np.int64), fe, np.zeros(n, np.float32), le, ri, np.zeros(n, np.float32), 136)
     with pytest.raises(T.TreeEnsError) as ei:
         _create(ens)
-    assert ei.value.code == T.TREE_ENS_E_MODEL and "LDS tile" in ei.value.message
+    assert ei.value.code == T.TREE_ENS_E_MODEL and "65535 nodes" in ei.value.message
 
 
 def test_valid_model_reaches_the_device_step():

@@ -1,6 +1,6 @@
 """Maximum sizes on the GPU: every document-block width the LDS plans choose (64, 32, 16 and 8
 documents per block, float and threshold-coded rows) up to the largest feature id accepted,
-and the largest single tree one LDS tile holds, against the oracle (scores within tolerance,
+the largest single tree one LDS tile holds and the smallest one it does not, against the oracle (scores within tolerance,
 leaf ids bit-exact)."""
 from __future__ import annotations
 
@@ -64,15 +64,17 @@ def test_coded_rows_for_wide_features_and_large_trees(T, n_cols, dl):
 
 
 def test_largest_tree_one_tile_holds(T):
-    # 2,923 leaves (5,845 nodes) is the largest tree accepted at 136 features; one more leaf
-    # is refused at create
+    # 2,923 leaves (5,845 nodes) is the largest tree one tile holds at 136 features (it is
+    # tiled); one more leaf makes it a big tree, walked from device memory
     ens = W.random_ensemble(1, n_trees=1, n_features=136, min_leaves=2923, max_leaves=2923)
     X = W.make_docs(W.WORKLOADS["rank_1kx32"], n_docs=3000)
-    _check(T, ens, X, "largest tree")
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        assert m.info()["n_tiles"] == 1
+    _check(T, ens, X, "largest tiled tree")
     big = W.random_ensemble(1, n_trees=1, n_features=136, min_leaves=2924, max_leaves=2924)
-    with pytest.raises(T.TreeEnsError) as ei:
-        T.TreeEnsemble.from_ensemble(big)
-    assert ei.value.code == T.TREE_ENS_E_MODEL
+    with T.TreeEnsemble.from_ensemble(big) as m:
+        assert m.info()["n_tiles"] == 0
+    _check(T, big, X, "smallest big tree")
 
 
 # (features, leaves per tree at most, documents per block): float plans with 4, 2 and 1 trees

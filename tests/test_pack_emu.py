@@ -46,7 +46,7 @@ def _walk(lib, ens, X, level, flags=0, leaf_values=None):
     X = np.ascontiguousarray(X, np.float32)
     leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
     scores = np.empty((X.shape[0], n_out), np.float64)
-    plan = np.zeros(9, np.int32)
+    plan = np.zeros(10, np.int32)
     rc = lib.emu_walk(ens.n_trees, *[a.ctypes.data for a in arrs], n_out, flags, X.ctypes.data,
                       X.shape[0], X.shape[1], level, leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
     assert rc == 0, lib.emu_message().decode()
@@ -328,3 +328,69 @@ def test_walker_packets_or_shared_tiles(emu):
     big = W.random_ensemble(3, n_trees=30, n_features=136, min_leaves=150, max_leaves=220)
     plan = _check(emu, big, W.random_docs(3, 70, 136), levels=(0,))
     assert plan[5] == 80 * 1024 and plan[0] == 64 and plan[8] == 0, plan
+
+
+def _big_model(seed, n_feat, n_small, small_leaves, big_leaves):
+    """n_small trees of up to small_leaves leaves followed by trees of the given leaf counts
+    (too large for one LDS tile), in one ensemble."""
+    parts = []
+    if n_small:
+        parts.append(W.random_ensemble(seed, n_trees=n_small, n_features=n_feat, min_leaves=1,
+                                       max_leaves=small_leaves))
+    for i, L in enumerate(big_leaves):
+        parts.append(W.random_ensemble(seed * 10 + i, n_trees=1, n_features=n_feat, min_leaves=L, max_leaves=L))
+    trees = [e.tree(t) for e in parts for t in range(e.n_trees)]
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(len(trees))  # big trees anywhere in the input order
+    return _stack([trees[i] for i in order], n_feat)
+
+
+@pytest.mark.parametrize("n_feat,n_small,big_leaves,coded", [
+    (136, 40, [3000, 8192], 0),      # two-workgroup plan: a 45 KiB slot holds 2,923 leaves at most
+    (136, 0, [8192, 32768], 0),      # only big trees: no tile at all
+    (700, 30, [4500, 8192], 0),      # one-workgroup plan of 32 float documents
+    (700, 300, [300, 8192], 1),      # threshold-coded documents
+])
+def test_big_trees_walked_from_device_memory(emu, n_feat, n_small, big_leaves, coded):
+    """Trees larger than one LDS tile (up to 65,535 nodes) are packed after the tiled ones in
+    the big-tree format and walked from the packed array: every child link stays inside its
+    tree, leaves absorb a further step, and the leaf ids equal the oracle's, under both rules."""
+    ens = _big_model(7 + n_small, n_feat, n_small, 400 if coded else 40, big_leaves)
+    X = W.random_docs(9, 70, n_feat, zero_frac=0.2)
+    for flags in (0, 1):
+        plan = _check(emu, ens, X, flags=flags, levels=(0, 4))
+        # a tree is big when its records, the tile header and K root copies exceed the slot
+        cap = int(plan[6]) // 8 - 2 - int(plan[1])
+        sizes = np.diff(ens.tree_offsets)
+        assert plan[9] == int((sizes <= cap).sum()) and (sizes > cap).sum() >= 1, (plan, cap)
+        assert plan[3] == coded, plan
+
+
+def test_big_trees_with_vector_leaves(emu):
+    ens = _big_model(3, 136, 20, 30, [8192])
+    X = W.random_docs(4, 65, 136)
+    vals = W.make_leaf_vectors(ens, 5, "dense", seed=2)
+    ref = oracle.score_multi(ens, vals, X)
+    _, ref_leaves, _ = oracle.score(ens, X)
+    leaves, scores, plan = _walk(emu, ens, X, 0, leaf_values=vals)
+    assert plan[9] == 20
+    np.testing.assert_array_equal(leaves, ref_leaves)
+    np.testing.assert_allclose(scores, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_tree_size_limit(emu):
+    """65,535 nodes (32,768 leaves) is the largest tree accepted; one more leaf is refused."""
+    ok = W.random_ensemble(11, n_trees=1, n_features=5, min_leaves=32768, max_leaves=32768)
+    X = W.random_docs(11, 10, 5)
+    plan = _check(emu, ok, X, levels=(0,))
+    assert plan[9] == 0
+    too_big = W.random_ensemble(12, n_trees=1, n_features=5, min_leaves=32769, max_leaves=32769)
+    arrs = [np.ascontiguousarray(too_big.tree_offsets, np.int64), np.ascontiguousarray(too_big.feature, np.int32),
+            np.ascontiguousarray(too_big.threshold, np.float32), np.ascontiguousarray(too_big.left, np.int32),
+            np.ascontiguousarray(too_big.right, np.int32), np.ascontiguousarray(too_big.value, np.float32)]
+    leaves = np.empty((10, 1), np.int32)
+    scores = np.empty((10, 1), np.float64)
+    plan = np.zeros(10, np.int32)
+    rc = emu.emu_walk(1, *[a.ctypes.data for a in arrs], 1, 0, X.ctypes.data, 10, 5, 0,
+                      leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
+    assert rc == -2 and b"65535" in emu.emu_message()
