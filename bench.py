@@ -394,11 +394,11 @@ def cpu_baseline(W, wl, budget_s=10.0):
             "cpu_model": _cpu_model(), "host_cpus": host_cpus}
 
 
-def pmc_probe(T, W) -> int:
-    """Copy the feature matrix once (reads and writes exactly its bytes: the calibration for the
-    FETCH_SIZE / WRITE_SIZE counters), then score it three times."""
+def pmc_probe(T, W, workload: str = HEADLINE) -> int:
+    """Copy the workload's feature matrix once (reads and writes exactly its bytes: the
+    calibration for the FETCH_SIZE / WRITE_SIZE counters), then score it three times."""
     import torch
-    cfg = W.WORKLOADS[HEADLINE]
+    cfg = W.WORKLOADS[workload]
     ens = W.make_ensemble(cfg)
     Xd = torch.from_numpy(W.make_docs(cfg)).to("cuda")
     copy = torch.empty_like(Xd)
@@ -414,14 +414,16 @@ def pmc_probe(T, W) -> int:
     return 0
 
 
-def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) -> int:
+def write_traffic(fetch_csv: str, write_csv: str, workload: str = HEADLINE,
+                  out_path: str = TRAFFIC_FILE) -> int:
     """Per-launch HBM traffic of the scoring kernel from two rocprofv3 --pmc runs of
-    --pmc-probe (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what the same
-    counter reads for the probe's plain device copy of the feature matrix (a kernel that reads
-    and writes exactly that many bytes). Runs on the host; writes profiles/hbm_traffic.json."""
+    --pmc-probe WORKLOAD (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what
+    the same counter reads for the probe's plain device copy of the feature matrix (a kernel
+    that reads and writes exactly that many bytes). Runs on the host; adds the workload's entry
+    to profiles/hbm_traffic.json (entries taken on another kernel source are dropped)."""
     import csv
     import workloads as W
-    cfg = W.WORKLOADS[HEADLINE]
+    cfg = W.WORKLOADS[workload]
     copy_bytes = cfg.n_docs * cfg.n_features * 4
 
     def per_kernel(path, counter):
@@ -446,25 +448,29 @@ def write_traffic(fetch_csv: str, write_csv: str, out_path: str = TRAFFIC_FILE) 
     read_b = f_score * 1024.0 * f_factor
     write_b = w_score * 1024.0 * w_factor
     fetch_dir, write_dir = os.path.dirname(fetch_csv), os.path.dirname(write_csv)
-    rec = {
-        "kernel_hash": kernel_hash(),
-        "note": (f"HBM bytes per launch of the scoring kernel on {cfg.name} ({cfg.n_docs} docs), mean "
-                 f"of {n_f} (FETCH_SIZE) and {n_w} (WRITE_SIZE) dispatches, each counter scaled by "
-                 f"its reading on a plain device copy of {copy_bytes} bytes (FETCH_SIZE {f_copy:.1f} "
-                 f"KiB, WRITE_SIZE {w_copy:.1f} KiB for {copy_bytes / 1024:.1f} KiB moved)."),
+    try:
+        with open(out_path) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        rec = {}
+    if rec.get("kernel_hash") != kernel_hash():
+        rec = {"kernel_hash": kernel_hash(), "workloads": {}}
+    rec["note"] = ("HBM bytes per launch of the scoring kernel, mean over the probe's dispatches; "
+                   "FETCH_SIZE and WRITE_SIZE each scaled by their reading on a plain device copy "
+                   "of the workload's feature matrix (a kernel that moves exactly its bytes).")
+    rec["workloads"][cfg.name] = {
+        "fetch_kib_raw": f_score, "write_kib_raw": w_score, "dispatches": [n_f, n_w],
+        "calibration": {"copy_bytes": copy_bytes, "fetch_kib": f_copy, "write_kib": w_copy,
+                        "fetch_factor": f_factor, "write_factor": w_factor},
+        "hbm_read_bytes_per_launch": int(round(read_b)),
+        "hbm_write_bytes_per_launch": int(round(write_b)),
+        "hbm_bytes_per_launch": int(round(read_b + write_b)),
+        "algorithmic_hbm_bytes": cfg.n_docs * cfg.n_features * 4 + cfg.n_docs * 4,
         "commands": [
-            f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o fetch -- python -u bench.py --pmc-probe",
-            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o write -- python -u bench.py --pmc-probe",
-            f"python bench.py --write-traffic {fetch_csv} {write_csv}",
+            f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o fetch -- python3 -u bench.py --pmc-probe {cfg.name}",
+            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o write -- python3 -u bench.py --pmc-probe {cfg.name}",
+            f"python bench.py --write-traffic {fetch_csv} {write_csv} {cfg.name}",
         ],
-        "calibration": {"fetch_factor": f_factor, "write_factor": w_factor},
-        "workloads": {cfg.name: {
-            "fetch_kib_raw": f_score, "write_kib_raw": w_score,
-            "hbm_read_bytes_per_launch": int(round(read_b)),
-            "hbm_write_bytes_per_launch": int(round(write_b)),
-            "hbm_bytes_per_launch": int(round(read_b + write_b)),
-            "algorithmic_hbm_bytes": cfg.n_docs * cfg.n_features * 4 + cfg.n_docs * 4,
-        }},
     }
     with open(out_path, "w") as fh:
         json.dump(rec, fh, indent=1)
@@ -499,15 +505,18 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--no-extra", action="store_true", help="only the headline workload")
-    ap.add_argument("--pmc-probe", action="store_true",
-                    help="for rocprofv3 --pmc runs: one device copy of the headline workload's "
-                         "feature matrix (a kernel of known traffic, for calibration) followed by "
-                         "3 predicts; prints nothing else")
-    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="host only: turn the counter CSVs of the two --pmc-probe runs into "
+    ap.add_argument("--pmc-probe", nargs="?", const=HEADLINE, default=None, metavar="WORKLOAD",
+                    help="for rocprofv3 --pmc runs: one device copy of the workload's feature "
+                         "matrix (a kernel of known traffic, for calibration) followed by 3 "
+                         "predicts of the whole workload (default: the headline one)")
+    ap.add_argument("--write-traffic", nargs="+", metavar="ARG",
+                    help="host only: FETCH_CSV WRITE_CSV [WORKLOAD]: turn the counter CSVs of the "
+                         "two --pmc-probe runs of a workload into its entry of "
                          "profiles/hbm_traffic.json")
     args = ap.parse_args()
     if args.write_traffic:
+        if len(args.write_traffic) not in (2, 3):
+            ap.error("--write-traffic takes FETCH_CSV WRITE_CSV [WORKLOAD]")
         return write_traffic(*args.write_traffic)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -523,7 +532,7 @@ def main() -> int:
         return 2
 
     if args.pmc_probe:
-        return pmc_probe(T, W)
+        return pmc_probe(T, W, args.pmc_probe)
     rec, model, ens, Xd, out = measure_workload(T, W, HEADLINE, args.steps, args.warmup)
     lat = latency_100(model, Xd)
     log(f"100-doc batch: median {lat['median_us']:.1f} us, device {lat['device_us_per_call']:.1f} us/call")

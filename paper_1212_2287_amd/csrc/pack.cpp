@@ -30,6 +30,21 @@ float strict_to_inclusive(float theta) {
 // must not overflow.
 bool is_complete(int64_t n, int64_t d) { return d < 62 && n == (int64_t(2) << d) - 1; }
 
+// Leaf records of tiles and packets whose trees are all complete of one depth: the walk there
+// takes a fixed number of steps and never tests a leaf, so a leaf record needs neither its
+// column nor its link and holds the leaf value as a double (the 8 bytes of the record), which
+// the kernel adds to its fp64 sum without a conversion. Internal records are unchanged.
+NodeRec complete_leaf(NodeRec r, uint32_t col_mask) {
+    if ((r.w & col_mask) != 0)
+        return r; // internal node (its column offset is never 0)
+    float v;
+    std::memcpy(&v, &r.thr_bits, 4);
+    const double d = double(v);
+    uint64_t b;
+    std::memcpy(&b, &d, 8);
+    return NodeRec{uint32_t(b), uint32_t(b >> 32)};
+}
+
 // avg_tree_bytes: mean packed size of a tree, to pick how many trees a lane walks at once.
 // elem_bytes: 4 for float features, 2 for codes.
 LdsPlan plan_lds(int32_t n_cols, double avg_tree_bytes, int elem_bytes) {
@@ -465,6 +480,10 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                 complete = (complete == -2 || complete == d) && full ? d : -1;
                 te++;
             }
+            // a tile whose last group has idle slots (the zero record) is walked as a general
+            // one: complete walks add every slot's leaf record as a double
+            if ((te - tb) % K != 0)
+                complete = -1;
             p.tiles.push_back(Tile{tb, te, dmax, int32_t(p.tree_node_off[size_t(tb)]), complete});
             tb = te;
         }
@@ -510,6 +529,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             img[1] = NodeRec{uint32_t(tl.tree_begin),
                              i + 1 < n_level ? p.tile_recs[size_t(p.level_begin[k] + i + 1)] : 0u};
             const NodeRec zero_leaf{zero_record_value(plan, vec), (zero_addr / 8u) << shift};
+            const bool f64_leaves = tl.complete_depth >= 0 && !vec;
             for (int32_t t = 0; t < hrecs - kHeaderFixedWords / 2; t++) {
                 NodeRec r = zero_leaf;
                 if (t < ntr) {
@@ -517,6 +537,8 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                     const uint32_t tree_rec = rec0 + first - uint32_t(tl.node_begin);
                     r = p.nodes[first];
                     r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                    if (f64_leaves)
+                        r = complete_leaf(r, col_mask);
                 }
                 img[kHeaderFixedWords / 2 + t] = r;
             }
@@ -526,6 +548,8 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                 for (uint32_t n = first; n < p.tree_node_off[size_t(t) + 1]; n++) {
                     NodeRec r = p.nodes[n];
                     r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                    if (f64_leaves)
+                        r = complete_leaf(r, col_mask);
                     img[hrecs + int64_t(n - uint32_t(tl.node_begin))] = r;
                 }
             }
@@ -591,10 +615,13 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             if (fits && first >= 0)
                 runs[size_t(v)].push_back({first, count});
         }
+        int32_t per = 0;
+        for (const auto &r : runs)
+            per = std::max(per, int32_t(r.size()));
+        // the kernel addresses packets with 32-bit byte offsets
+        if (int64_t(W) * per * sub * int64_t(sizeof(NodeRec)) >= (int64_t(1) << 31))
+            fits = false;
         if (fits) {
-            int32_t per = 0;
-            for (const auto &r : runs)
-                per = std::max(per, int32_t(r.size()));
             p.pk_recs = sub;
             p.pk_zero_rec = pk_zero;
             p.pk_per_walker = per;
@@ -608,12 +635,15 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                     most[q] = std::max(most[q], ng);
                     // the common complete depth of every tree of the packet, else -1
                     int32_t complete = -2; // -2: no tree yet
+                    bool idle = false;
                     for (int32_t h = 0; h < P; h++) {
                         for (int32_t j = 0; j < ng; j++) {
                             for (int32_t i = 0; i < K; i++) {
                                 const int32_t t = group_of(v, h, r0 + j) * K + i;
-                                if (t >= n_small)
+                                if (t >= n_small) {
+                                    idle = true; // an idle slot: the packet is walked as general
                                     continue;
+                                }
                                 const int32_t d = int32_t(p.tree_depth[size_t(t)]);
                                 const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
                                 const bool full = is_complete(nn, d);
@@ -621,6 +651,8 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                             }
                         }
                     }
+                    if (idle)
+                        complete = -1;
                     for (int32_t h = 0; h < P; h++) {
                         const uint32_t base = uint32_t(plan.xs_bytes / 8) + uint32_t(v * sub + h * part); // in LDS
                         NodeRec *img = p.packets.data() + (size_t(v) * size_t(per) + q) * size_t(sub) + size_t(h * part);
@@ -641,6 +673,8 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
                                     for (uint32_t n = 0; n < nn; n++) {
                                         NodeRec r = p.nodes[first + n];
                                         r.w = ((tree_rec + (r.w >> shift)) << shift) | (r.w & col_mask);
+                                        if (complete >= 0 && !vec)
+                                            r = complete_leaf(r, col_mask);
                                         img[pos + int32_t(n)] = r;
                                     }
                                     root = img[pos];

@@ -246,15 +246,24 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // Walker packets (pk_recs > 0, plans of 64- or 32-document blocks): wave v's packet q is
     // images[(v * n_tiles + q) * pk_recs, ...), one part of pk_recs * DL / 64 records for each
     // of its walkers; each lane loads pk_recs / 64 records of it.
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int pk_lane = pk_recs / 64;
-    const uint2 *pk_src = images + (int64_t(wave) * n_tiles) * pk_recs + lane;
+    // The loads are raw buffer loads: the packet's offset in a scalar register, each lane's
+    // record offset in a vector register and the record's position in the instruction's
+    // immediate, so no address arithmetic runs per packet (the packer keeps the packets below
+    // 2 GiB).
+    const __amdgpu_buffer_rsrc_t pk_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint2 *>(images), 0, 0x7fffffff, 0x00020000);
+    const int pk_lane_off = lane * 8;
     auto fetch_packet = [&](int q) {
-        const uint2 *src = pk_src + int64_t(q) * pk_recs;
+        const int soff = (wave * n_tiles + q) * pk_recs * 8;
 #pragma unroll
-        for (int j = 0; j < kPre; ++j)
-            if (j < pk_lane)
-                pa[j] = src[j * 64];
+        for (int j = 0; j < kPre; ++j) {
+            if (j < pk_lane) {
+                const auto v = __builtin_amdgcn_raw_buffer_load_b64(pk_rsrc, pk_lane_off + j * 512, soff, 0);
+                pa[j] = make_uint2(v[0], v[1]);
+            }
+        }
     };
     if constexpr (HALF) {
         if (pk_recs > 0) {
@@ -388,8 +397,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 }
             }
         };
+        uint32_t addr[K]; // byte addresses of the records read by the last step
         auto descend = [&]() {
-            uint32_t addr[K];
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 uint32_t child;
@@ -462,7 +471,11 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 const int2 tr = tree_of(i);
                 if (tr.x >= 0 && doc < n_docs) {
                     const int gt = tr.x;
-                    const uint32_t self = (rec_w(nd[i]) >> kShift) - uint32_t(tr.y);
+                    // complete trees: the leaf's record index is the address the last step
+                    // read (their leaf records carry no link); else the leaf's own link
+                    const uint32_t rec = kComplete ? (complete_depth > 0 ? addr[i] / 8u : uint32_t(tr.y))
+                                                   : rec_w(nd[i]) >> kShift;
+                    const uint32_t self = rec - uint32_t(tr.y);
                     leaf_ids[doc * n_trees + tree_orig[gt]] = orig_id[tree_node_off[gt] + self];
                 }
             }
@@ -480,10 +493,15 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         } else if constexpr (!USAGE) {
             // the K leaf values, each added to the double accumulator in tree order (a
             // float sum of the group first can miss the tolerance when a score cancels
-            // near zero); idle slots hold the zero record
+            // near zero); idle slots hold the zero record. Complete trees' leaf records hold
+            // the value as a double (tiles and packets with an idle slot are never complete).
 #pragma unroll
-            for (int i = 0; i < K; ++i)
-                acc += double(__uint_as_float(rec_thr(nd[i])));
+            for (int i = 0; i < K; ++i) {
+                if constexpr (kComplete)
+                    acc += __longlong_as_double(static_cast<long long>(nd[i]));
+                else
+                    acc += double(__uint_as_float(rec_thr(nd[i])));
+            }
         }
     };
     // Walk the tile image in the LDS slot: walker w takes groups w, w + n_walkers, ... of K

@@ -217,13 +217,17 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                 const int64_t doc = doc0 + dl;
                 treeens::NodeRec r = rec_at(root_copy);
                 int steps = 0;
+                uint32_t last = root_idx * 8u; // LDS byte address of the record r came from
                 for (;;) {
+                    // complete trees: a fixed number of steps (their leaf records hold a double)
+                    if (complete >= 0 && steps == complete)
+                        break;
                     const uint32_t fa = (r.w & mask) | uint32_t(dl * E);
                     if (fa != (r.w & mask) + uint32_t(dl * E))
                         return bad("column offset and lane offset overlap");
                     if (fa + uint32_t(E) > xs)
                         return bad("feature address outside the document tile");
-                    if (complete >= 0 ? steps == complete : fa < leaf_col)
+                    if (complete < 0 && fa < leaf_col)
                         break;
                     bool right_side;
                     if (E == 4) {
@@ -239,8 +243,30 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                     if (!valid(a))
                         return bad("child address outside the tile's records");
                     r = rec_at(a);
+                    last = a;
                     if (++steps > p.max_depth + 1)
                         return bad("walk longer than the deepest tree");
+                }
+                if (complete >= 0) {
+                    // the record reached must be a leaf of the tree, stored as its value in double
+                    const int64_t self = int64_t(last / 8u) - int64_t(root_idx);
+                    if (self < 0 || self >= tree_n)
+                        return bad("complete walk ended outside its tree");
+                    const treeens::NodeRec orig = p.nodes[p.tree_node_off[size_t(gt)] + size_t(self)];
+                    const bool vec_model = n_outputs > 1;
+                    if ((orig.w & mask) != 0)
+                        return bad("complete walk ended on an internal node");
+                    if (!vec_model) {
+                        const double want = double(as_float(orig.thr_bits));
+                        double got;
+                        std::memcpy(&got, &r, 8);
+                        if (std::memcmp(&got, &want, 8) != 0)
+                            return bad("complete tree's leaf record does not hold its value as a double");
+                        leaf_ids[doc * n_trees + p.tree_orig[size_t(gt)]] =
+                            p.orig_id[p.tree_node_off[size_t(gt)] + size_t(self)];
+                        scores[doc] += got;
+                        continue;
+                    }
                 }
                 if ((r.w & mask) != 0)
                     return bad("walk ended on an internal node");
@@ -383,6 +409,8 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
                                 if (K % 2 == 0 && i % 2 == 0 && root_copy % 16 != 0)
                                     return bad("packet: a pair of root copies is not 16-byte aligned");
                                 if (gt >= p.n_small) {
+                                    if (complete >= 0)
+                                        return bad("packet: a complete packet has an idle slot");
                                     if (std::memcmp(lds.data() + root_copy, lds.data() + pzero, 8) != 0)
                                         return bad("packet: padding root is not the zero record");
                                     continue;
@@ -428,6 +456,8 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
             for (int s = ntr; s < padded; s++)
                 if (std::memcmp(lds.data() + root0 + 8u * s, lds.data() + zero, 8) != 0)
                     return bad("header: padding root is not the zero record");
+            if (complete >= 0 && padded != ntr)
+                return bad("header: a complete tile has an idle slot");
             const uint32_t rec0 = xs / 8u + hdr_bytes / 8u; // LDS index of the first tree record
             for (int s = 0; s < ntr; s++) {
                 const int gt = tb + s;

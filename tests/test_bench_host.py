@@ -41,16 +41,27 @@ def test_write_traffic_scales_by_the_copy(tmp_path, monkeypatch):
     _csv(tmp_path / "w.csv", "WRITE_SIZE", [("__amd_rocclr_copyBuffer", copy_kib),
                                              ("score_kernel<64, 4, true, true, false, 0>", 600.0)])
     out = tmp_path / "traffic.json"
-    assert bench.write_traffic(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), str(out)) == 0
+    assert bench.write_traffic(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "rank_1kx32", str(out)) == 0
     rec = json.loads(out.read_text())
     ent = rec["workloads"]["rank_1kx32"]
-    assert rec["calibration"]["fetch_factor"] == pytest.approx(2.0)
+    assert ent["calibration"]["fetch_factor"] == pytest.approx(2.0)
     assert ent["hbm_read_bytes_per_launch"] == round(31000.0 * 1024 * 2)
     assert ent["hbm_write_bytes_per_launch"] == round(600.0 * 1024)
     assert rec["kernel_hash"] == bench.kernel_hash()
     # the stored figure is used only while the kernel sources hash the same
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(out))
     assert bench.load_traffic("rank_1kx32") == ent["hbm_bytes_per_launch"]
+    # a second workload's entry is added beside the first
+    copy5 = 1_000_000 * 700 * 4 / 1024
+    _csv(tmp_path / "f5.csv", "FETCH_SIZE", [("__amd_rocclr_copyBuffer", copy5 / 2),
+                                              ("score_kernel<64, 1, false, false, true, 0>", 1e6)])
+    _csv(tmp_path / "w5.csv", "WRITE_SIZE", [("__amd_rocclr_copyBuffer", copy5),
+                                              ("score_kernel<64, 1, false, false, true, 0>", 4000.0)])
+    assert bench.write_traffic(str(tmp_path / "f5.csv"), str(tmp_path / "w5.csv"), "large_5kx256_f700_1M",
+                               str(out)) == 0
+    rec = json.loads(out.read_text())
+    assert set(rec["workloads"]) == {"rank_1kx32", "large_5kx256_f700_1M"}
+    assert bench.load_traffic("large_5kx256_f700_1M") == round(1e6 * 1024 * 2) + round(4000.0 * 1024)
     rec["kernel_hash"] = "0" * 16
     out.write_text(json.dumps(rec))
     assert bench.load_traffic("rank_1kx32") is None
