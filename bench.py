@@ -580,7 +580,7 @@ def main() -> int:
                                f"{cfg.max_depth}), {cfg.n_features} features, {cfg.n_docs} docs",
                    "n_trees": cfg.n_trees, "n_docs": cfg.n_docs, "n_features": cfg.n_features,
                    "docs_per_block": rec["model"]["docs_per_block"]},
-        "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"],
+        "ns_per_doc": rec["ns_per_doc"], "kernel_ms": rec["kernel_ms"], "step_stats": rec["step_stats"],
         "latency_100doc_us": lat, "rerank": rr, "feature_usage": fu,
         "multi_output": mo, "codegen": cg, "visits": rec["visits"],
         "roofline": rec["roofline"], "roofline_hbm": rec["roofline_hbm"],

@@ -46,7 +46,11 @@ typedef struct tree_ens tree_ens_t;
  * runs it. Other entry points keep the generic kernels. Models of at most 65,536 nodes and
  * depth 64, one value per leaf (else TREE_ENS_E_MODEL / TREE_ENS_E_ARG); a compiler failure is
  * TREE_ENS_E_DEVICE with the compiler log in the message. Compiling takes about 6 s per
- * 15,000 nodes (this call returns when it is done). */
+ * 15,000 nodes (this call returns when it is done). This is the paper's comparison form, kept
+ * for that comparison: on MI355X it only ties the generic kernel on tiny models (10 trees of 8
+ * leaves, where both are bound by the launch) and is 15x slower at 200 trees of 32 leaves and
+ * 55x slower at 1,000 trees of depth 3 (one document per thread follows the union of its
+ * wave's branch paths and reads features from global memory); do not use it for throughput. */
 #define TREE_ENS_CODEGEN 2u
 
 /*
