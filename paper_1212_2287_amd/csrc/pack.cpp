@@ -691,6 +691,161 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         }
     }
 
+    // ---- compact packets (coded plans of 64-document blocks; see kCompactWindowBytes) ------------
+    {
+        constexpr int32_t W = kPacketWalkers;
+        constexpr int32_t kWords = kCompactPacketBytes / 4;
+        int64_t max_nodes = 0;
+        for (int32_t t = 0; t < n_small; t++)
+            max_nodes = std::max<int64_t>(max_nodes, p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
+        size_t max_thr = 0;
+        if (plan.coded)
+            for (const auto &tv : thr_of)
+                max_thr = std::max(max_thr, tv.size());
+        const int64_t cw = compact_window_base(plan.xs_bytes);
+        // bytes of tree t's children pairs (a lone leaf: one pair of itself)
+        auto body = [&](int32_t t) {
+            const int64_t n = int64_t(p.tree_node_off[size_t(t) + 1]) - int64_t(p.tree_node_off[size_t(t)]);
+            return int32_t(4 * std::max<int64_t>(2, n - 1));
+        };
+        constexpr int32_t K = kCompactTrees;
+        const int32_t win = kCompactWindowBytes / K, cap = win - 8;
+        const int32_t n_groups = (n_trees + K - 1) / K;
+        const int32_t max_ng = (kCompactHeaderBytes / 4 - kCompactHeaderWords) / K;
+        bool ok = plan.coded && plan.docs_per_block == 64 && plan.lds_bytes == kLdsPerCu && n_trees > 0 &&
+                  n_small == n_trees && n_cols + 1 <= kCompactMaxColumns && max_thr < kCompactNeverRight &&
+                  max_nodes <= kCompactMaxTreeNodes && cw + int64_t(W) * kCompactPacketBytes <= kLdsPerCu;
+        // per wave: runs (first round, groups) of consecutive rounds whose trees fit every window
+        std::vector<std::vector<std::pair<int32_t, int32_t>>> runs(static_cast<size_t>(W));
+        for (int32_t v = 0; v < W && ok; v++) {
+            int32_t first = -1, count = 0;
+            std::vector<int32_t> used(static_cast<size_t>(K), 0);
+            for (int32_t r = 0; v + r * W < n_groups; r++) {
+                const int32_t g = v + r * W;
+                bool more = first >= 0 && count < max_ng;
+                for (int32_t i = 0; i < K && more; i++) {
+                    const int32_t t = g * K + i;
+                    more = t >= n_trees || used[size_t(i)] + body(t) <= cap;
+                }
+                if (!more) {
+                    if (first >= 0)
+                        runs[size_t(v)].push_back({first, count});
+                    first = r;
+                    count = 0;
+                    std::fill(used.begin(), used.end(), 0);
+                }
+                count++;
+                for (int32_t i = 0; i < K; i++)
+                    if (g * K + i < n_trees)
+                        used[size_t(i)] += body(g * K + i);
+            }
+            if (first >= 0)
+                runs[size_t(v)].push_back({first, count});
+        }
+        int32_t per = 0;
+        for (const auto &r : runs)
+            per = std::max(per, int32_t(r.size()));
+        // the kernel addresses packets (and their payloads) with 32-bit byte offsets
+        if (int64_t(W) * per * kCompactPacketBytes >= (int64_t(1) << 31))
+            ok = false;
+        if (ok) {
+            const int shift_c = plan.narrow ? 16 : kWideChildShift;
+            const uint32_t cmask = plan.narrow ? kNarrowColMask : kWideColMask;
+            const uint32_t col_bytes = uint32_t(plan.docs_per_block * plan.elem_bytes);
+            p.cp_k = K;
+            p.cp_per_walker = per;
+            const size_t total = size_t(W) * size_t(per) * size_t(kWords);
+            p.cp_packets.assign(total, 0u);
+            p.cp_leaf.assign(total, 0u);
+            p.cp_leaf_id.assign(total, -1);
+            std::vector<int32_t> most(static_cast<size_t>(per), 0);
+            for (int32_t v = 0; v < W; v++) {
+                for (size_t q = 0; q < runs[size_t(v)].size(); q++) {
+                    const int32_t r0 = runs[size_t(v)][q].first, ng = runs[size_t(v)][q].second;
+                    const size_t at = (size_t(v) * size_t(per) + q) * size_t(kWords);
+                    uint32_t *img = p.cp_packets.data() + at;
+                    uint32_t *pay = p.cp_leaf.data() + at;
+                    int32_t *ids = p.cp_leaf_id.data() + at;
+                    uint32_t *hdr = img + kCompactWindowBytes / 4;
+                    p.cp_max_groups = std::max(p.cp_max_groups, ng);
+                    most[q] = std::max(most[q], ng);
+                    // the zero pair at the end of each window: a left-side leaf of payload 0
+                    const uint32_t zero = (kCompactNeverRight << kCompactThrShift) | uint32_t(cap);
+                    for (int32_t i = 0; i < K; i++) {
+                        const size_t zw = size_t(i * win + cap) / 4;
+                        img[zw] = img[zw + 1] = zero;
+                        pay[zw] = pay[zw + 1] = vec ? 1u : 0u;
+                    }
+                    // the common complete depth of every tree of the packet, else -1
+                    int32_t complete = -2;
+                    for (int32_t j = 0; j < ng; j++)
+                        for (int32_t i = 0; i < K; i++) {
+                            const int32_t t = (v + (r0 + j) * W) * K + i;
+                            if (t >= n_trees) {
+                                complete = -1; // an idle slot
+                                continue;
+                            }
+                            const int32_t d = int32_t(p.tree_depth[size_t(t)]);
+                            const int64_t nn = int64_t(p.tree_node_off[size_t(t) + 1] - p.tree_node_off[size_t(t)]);
+                            complete = (complete == -2 || complete == d) && is_complete(nn, d) ? d : -1;
+                        }
+                    hdr[0] = uint32_t(ng);
+                    hdr[1] = uint32_t(complete);
+                    hdr[2] = uint32_t(v + r0 * W);
+                    hdr[3] = 0u;
+                    std::vector<uint32_t> off(static_cast<size_t>(K), 0u);
+                    for (int32_t j = 0; j < ng; j++) {
+                        for (int32_t i = 0; i < K; i++) {
+                            const int32_t t = (v + (r0 + j) * W) * K + i;
+                            uint32_t &root = hdr[kCompactHeaderWords + j * K + i];
+                            if (t >= n_trees) {
+                                root = zero;
+                                continue;
+                            }
+                            const uint32_t first = p.tree_node_off[size_t(t)];
+                            const uint32_t nn = p.tree_node_off[size_t(t) + 1] - first;
+                            const uint32_t o = off[size_t(i)];
+                            // window byte offset of node k (k >= 1: its slot among the pairs; a
+                            // lone root leaf: the first slot of its own pair)
+                            auto pos_of = [&](uint32_t k) { return k == 0 ? o : o + (k - 1) * 4u; };
+                            auto enc = [&](uint32_t k) {
+                                const NodeRec &r = p.nodes[first + k];
+                                const uint32_t colb = r.w & cmask;
+                                if (colb != 0) {
+                                    const uint32_t lc = r.w >> shift_c; // left child (tree-relative)
+                                    const uint32_t thr = r.thr_bits > kMaxCode ? kCompactNeverRight : r.thr_bits;
+                                    return (thr << kCompactThrShift) | ((colb / col_bytes) << kCompactColShift) |
+                                           (o + (lc - 1) * 4u);
+                                }
+                                const uint32_t pos = pos_of(k);
+                                return (((pos >> 2) & 1u) ? 0u : kCompactNeverRight << kCompactThrShift) | pos;
+                            };
+                            auto put = [&](uint32_t k) {
+                                const size_t w = size_t(uint32_t(i * win) + pos_of(k)) / 4;
+                                img[w] = enc(k);
+                                if ((p.nodes[first + k].w & cmask) == 0) {
+                                    pay[w] = p.nodes[first + k].thr_bits;
+                                    ids[w] = p.orig_id[first + k];
+                                }
+                            };
+                            root = enc(0);
+                            if (nn == 1) {
+                                put(0);
+                                img[size_t(uint32_t(i * win) + o) / 4 + 1] = root;
+                            } else {
+                                for (uint32_t k = 1; k < nn; k++)
+                                    put(k);
+                            }
+                            off[size_t(i)] += uint32_t(body(t));
+                        }
+                    }
+                }
+            }
+            for (int32_t m : most)
+                p.cp_total_rounds += m;
+        }
+    }
+
     if (plan.lds_bytes == kLdsPerCu / 2) {
         const int64_t used = p.pk_recs > 0 ? int64_t(kPacketWalkers) * p.pk_recs : int64_t(p.level_slot_recs[0]);
         const int64_t off = (int64_t(plan.xs_bytes) + used * 8 + 15) & ~int64_t(15);

@@ -96,6 +96,41 @@ constexpr int kHeaderFixedWords = 4;
 constexpr int kPacketHeaderRecs = 2;
 constexpr int kPacketWalkers = 16;
 
+// Compact packets: coded plans of 64-document blocks with one workgroup per CU, whose trees have
+// at most 511 nodes. A node is one 32-bit record
+//   bits 21..31  threshold code k + 1 (2047 for a NaN threshold, which never sends right; a
+//                leaf: 2047 if it is the left child of its pair, 0 if the right one)
+//   bits 11..20  column index f + 1 (0 for a leaf)
+//   bits  3..10  byte offset of the node's children pair in its window (a leaf: its own pair)
+//   bit   2      a leaf's side in its pair (0 for an internal node)
+// and a tree is its root record plus its children pairs (breadth-first, as in `nodes`), the
+// pairs 8-byte aligned. A step reads the document's staged value and the whole children pair
+// together (one dependent LDS round trip per step, not two) and keeps the side the comparison
+// picks. Documents are staged as code << kCompactCodeShift | 31, so that the unsigned compare of
+// that 16-bit value with the record's upper half is code >= threshold (the column bits below
+// the threshold are absorbed by the 31). Leaf values stay in device memory: each packet has a
+// payload array of the same shape holding, at a leaf's position, its value's bits (the
+// leaf-vector row + 1 for vector-valued leaves) and, in a second array, its input node id.
+// Each wave's LDS holds K = 2 windows of 2 KiB (window i takes slot i of
+// every group of the packet; its last 8 bytes are a pair of zero records, {2047 << 21 | own
+// offset}, for idle slots, payload 0), then, in a separate region, a header:
+//   word 0 groups n, word 1 complete depth d (or -1), word 2 the wave's first group in the packet
+//   (later ones follow at stride 16), word 3 zero, words 4.. the K root records of each group.
+// In device memory a packet is its windows then its header (kCompactPacketBytes).
+constexpr int kCompactTrees = 2;          // K: trees per lane, one window each
+constexpr int kCompactWindowBytes = 4096; // all windows of one wave
+constexpr int kCompactHeaderBytes = 512;
+constexpr int kCompactPacketBytes = kCompactWindowBytes + kCompactHeaderBytes;
+constexpr int kCompactHeaderWords = 4;
+constexpr int kCompactThrShift = 21;
+constexpr int kCompactColShift = 11;
+constexpr uint32_t kCompactNeverRight = 2047u;
+constexpr int kCompactMaxColumns = 1023;  // column index field
+constexpr int kCompactMaxTreeNodes = 511; // root + 255 pairs: 2,040 bytes, one 2 KiB window
+constexpr int kCompactCodeShift = 5;
+// LDS byte address of the first window (windows are aligned to their size, at most 2 KiB)
+inline int32_t compact_window_base(int32_t xs_bytes) { return (xs_bytes + 2047) & ~2047; }
+
 // Launch plan fixed at create time from the model's feature range.
 struct LdsPlan {
     int32_t docs_per_block; // documents a workgroup stages (power of two, 8..64)
@@ -179,6 +214,17 @@ struct Packed {
     int32_t pk_max_groups = 0;   // groups in the fullest packet
     int64_t pk_total_rounds = 0; // sum over packet indices of the most groups any walker has there
     std::vector<NodeRec> packets;
+    // Compact packets (see kCompactWindowBytes), used in place of the packets above when
+    // cp_k > 0: trees per lane, packets per wave, groups in the fullest packet, the planner's
+    // rounds, wave v's packet q at cp_packets[(v * cp_per_walker + q) * kCompactPacketBytes / 4],
+    // and the leaf payloads and input node ids at the same positions.
+    int32_t cp_k = 0;
+    int32_t cp_per_walker = 0;
+    int32_t cp_max_groups = 0;
+    int64_t cp_total_rounds = 0;
+    std::vector<uint32_t> cp_packets;
+    std::vector<uint32_t> cp_leaf;
+    std::vector<int32_t> cp_leaf_id;
     // vector-valued leaves (n_outputs > 1): a leaf's threshold slot holds 2 + its packed node
     // index instead of a value, and row (thr - 1) of leaf_vec holds its n_outputs values,
     // padded to vec_stride (a multiple of 4) floats; row 0 is zero (the all-zero record's row)

@@ -124,7 +124,22 @@ __device__ __forceinline__ uint32_t narrow_child_coded(uint32_t w, uint32_t code
     return r;
 }
 
-template <int DL, int K, bool HALF, bool NARROW, bool CODED, int MODE>
+// Compact records: the side of the children pair {lo, hi} that a 4-byte record r sends a
+// document to, whose staged value is x = code << 5 | 31: x >= the record's upper half is
+// code >= threshold. An SDWA compare reads the upper half in place; the s_nop covers the
+// VALU-writes-VCC / VALU-reads-VCC hazard as in narrow_child.
+__device__ __forceinline__ uint32_t compact_child(uint32_t x, uint32_t r, uint32_t lo, uint32_t hi) {
+    uint32_t out;
+    asm("v_cmp_ge_u32_sdwa vcc, %1, %2 src0_sel:DWORD src1_sel:WORD_1\n\t"
+        "s_nop 1\n\t"
+        "v_cndmask_b32 %0, %3, %4, vcc"
+        : "=v"(out)
+        : "v"(x), "v"(r), "v"(lo), "v"(hi)
+        : "vcc");
+    return out;
+}
+
+template <int DL, int K, bool HALF, bool NARROW, bool CODED, int MODE, bool COMPACT>
 // min waves per SIMD: 2 or 1 workgroups per CU (a feature trace holds a CU alone)
 __global__ void __launch_bounds__(kThreads, HALF && MODE != kModeUsage ? 8 : 4)
 score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, int32_t n_cols,
@@ -138,7 +153,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
              uint32_t *__restrict__ masks, int32_t mask_words, int32_t usage_off,
              const float4 *__restrict__ leaf_vec, int32_t vec_stride4, int32_t n_out,
              int32_t chunk, double out_scale, int32_t pk_recs, const uint2 *__restrict__ big,
-             int32_t n_small, uint32_t big_off0) {
+             int32_t n_small, uint32_t big_off0, const uint32_t *__restrict__ cleaf,
+             const int32_t *__restrict__ cleaf_id) {
     // Static allocation: the LDS base is address 0, so feature and node addresses need no add.
     // HALF = half a CU's LDS, so that two workgroups share a CU. CODED = documents arrive as
     // 16-bit threshold codes (rows of n_features codes) instead of floats. Layout:
@@ -265,7 +281,21 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             }
         }
     };
-    if constexpr (HALF) {
+    // Compact packets: kCompactPacketBytes per packet, one 8-byte row of 64 lanes per 512 bytes,
+    // read with raw buffer loads as above.
+    constexpr int kCpRows = treeens::kCompactPacketBytes / 512;
+    auto fetch_compact = [&](int q) {
+        const int soff = (wave * n_tiles + q) * treeens::kCompactPacketBytes;
+#pragma unroll
+        for (int j = 0; j < kCpRows; ++j) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(pk_rsrc, pk_lane_off + j * 512, soff, 0);
+            pa[j] = make_uint2(v[0], v[1]);
+        }
+    };
+    if constexpr (COMPACT) {
+        if (t_lo < t_hi)
+            fetch_compact(t_lo);
+    } else if constexpr (HALF) {
         if (pk_recs > 0) {
             if (t_lo < t_hi)
                 fetch_packet(t_lo);
@@ -302,7 +332,8 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         const int64_t doc = doc0 + dl;
         const bool live = doc < n_docs;
         const Elem *row = X + (live ? doc : n_docs - 1) * int64_t(n_features);
-        const Elem leaf_col = CODED ? Elem(0) : Elem(__builtin_nanf(""));
+        // (compact packets: code 0 staged as 0 << 5 | 31)
+        const Elem leaf_col = COMPACT ? Elem(31) : CODED ? Elem(0) : Elem(__builtin_nanf(""));
         if (tid < DL)
             xs[dl] = leaf_col;
         const bool vec = (n_features % kVec) == 0 && (reinterpret_cast<uintptr_t>(X) & 15u) == 0;
@@ -346,7 +377,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             }
         }
     }
-    if (tid == 0) {
+    if (!COMPACT && tid == 0) {
         // value 0 (as -0.0 for codes, whose leaves never hold zero bits; the all-zero row 0 of
         // the leaf-vector table for vector-valued leaves), column 0, self link
         const uint32_t thr = VEC ? 1u : CODED ? 0x80000000u : 0u;
@@ -583,7 +614,170 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             walk_packet(part_base);
         }
     };
-    if constexpr (HALF) {
+    // Compact packets (4-byte records): wave v owns K windows of kCompactWindowBytes / K bytes past
+    // the document tile and a header past all windows. A step reads the lane's staged value and
+    // the current record's whole children pair together (one dependent LDS round trip) and keeps
+    // the side the comparison picks. Leaves hold no value: the leaf's position in its window
+    // locates its payload (value bits, leaf-vector row + 1 or input node id) in arrays shaped
+    // like the packets in device memory. Scores add each group's payloads after the next group
+    // is walked, so their loads have a whole walk to land (the sum keeps tree order).
+    auto walk_compact = [&]() {
+        if constexpr (COMPACT) {
+            constexpr uint32_t kCpWin = treeens::kCompactWindowBytes / K;
+            static_assert(K == treeens::kCompactTrees && kCpWin == 2048, "compact windows of 2 KiB");
+            const uint32_t cw = (uint32_t(xs_bytes) + 2047u) & ~2047u;
+            const uint32_t my_win = cw + uint32_t(wave) * treeens::kCompactWindowBytes;
+            const uint32_t my_hdr =
+                cw + treeens::kPacketWalkers * treeens::kCompactWindowBytes + uint32_t(wave) * treeens::kCompactHeaderBytes;
+            const __amdgpu_buffer_rsrc_t leaf_rsrc =
+                __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(cleaf), 0, 0x7fffffff, 0x00020000);
+            const __amdgpu_buffer_rsrc_t id_rsrc =
+                __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(cleaf_id), 0, 0x7fffffff, 0x00020000);
+            // the column field moved to a feature address (column * DL * 2 bytes), the pair offset
+            const uint32_t col_sel = __builtin_amdgcn_readfirstlane(0x1FF80u);
+            const uint32_t pair_sel = __builtin_amdgcn_readfirstlane(0x7F8u);
+            // window bases (aligned to the window size: OR adds the pair offset), held in vector
+            // registers for the whole walk (opaque to the compiler, which would otherwise copy
+            // one from a scalar register at every step)
+            uint32_t tb[K];
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                asm volatile("v_mov_b32 %0, %1" : "=v"(tb[i]) : "s"(my_win + uint32_t(i) * kCpWin));
+            uint32_t pend[K]; // leaf payloads of the last group walked (scores)
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                pend[i] = 0u;
+            if constexpr (MODE == kModeScore) {
+                // Loads of the zero pairs' payloads (0.0) before the first packet, so that every
+                // packet's copy finds K payload loads issued after its rows, as on later packets.
+                if (t_lo < t_hi) {
+                    const int soff = (wave * n_tiles + t_lo) * treeens::kCompactPacketBytes;
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        pend[i] = __builtin_amdgcn_raw_buffer_load_b32(leaf_rsrc, i * kCpWin + kCpWin - 8, soff, 0);
+                }
+            }
+            __syncthreads(); // the document tile is written
+            for (int q = t_lo; q < t_hi; ++q) {
+                const int soff = (wave * n_tiles + q) * treeens::kCompactPacketBytes;
+                // this packet's rows have landed (the last group's payload loads may not have)
+                __builtin_amdgcn_s_waitcnt(MODE == kModeScore ? kWaitVmcnt0 | K : kWaitVmcnt0);
+#pragma unroll
+                for (int j = 0; j < kCpRows; ++j) {
+                    const uint32_t at = j < kCpRows - 1 ? my_win + uint32_t(j) * 512u : my_hdr;
+                    *reinterpret_cast<uint2 *>(lds + at + uint32_t(pk_lane_off)) = pa[j];
+                }
+                // the wave's own writes complete before it reads the packet back
+                __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
+                // the next packet (the last one again after the last: the loads stay
+                // unconditional, so the compiler counts them exactly when it waits for payloads)
+                fetch_compact(min(q + 1, t_hi - 1));
+                const uint32_t *hw = reinterpret_cast<const uint32_t *>(lds + my_hdr);
+                const int ng = __builtin_amdgcn_readfirstlane(int(hw[0]));
+                const int complete_depth = __builtin_amdgcn_readfirstlane(int(hw[1]));
+                const int first_group = __builtin_amdgcn_readfirstlane(int(hw[2]));
+                auto walk_groups = [&](auto complete_tag) {
+                    constexpr bool kComplete = decltype(complete_tag)::value;
+                    for (int j = 0; j < ng; ++j) {
+                        uint32_t r[K];
+                        {
+                            const uint2 rr = *reinterpret_cast<const uint2 *>(
+                                lds + my_hdr + 4u * uint32_t(treeens::kCompactHeaderWords + j * K));
+                            r[0] = rr.x;
+                            r[1] = rr.y;
+                        }
+                        uint32_t fa[K], xv[K], lo[K], hi[K];
+                        auto issue = [&]() {
+#pragma unroll
+                            for (int i = 0; i < K; ++i) {
+                                fa[i] = and_or(r[i] >> 4, col_sel, lane_off);
+                                const uint32_t pa_i = and_or(r[i], pair_sel, tb[i]);
+                                xv[i] = *reinterpret_cast<const uint16_t *>(lds + fa[i]);
+                                const uint64_t pr = read_record(lds + pa_i);
+                                lo[i] = uint32_t(pr);
+                                hi[i] = uint32_t(pr >> 32);
+                            }
+                        };
+                        auto select = [&]() {
+#pragma unroll
+                            for (int i = 0; i < K; ++i)
+                                r[i] = compact_child(xv[i], r[i], lo[i], hi[i]);
+                        };
+                        if constexpr (kComplete) {
+                            for (int s = 0; s < complete_depth; ++s) {
+                                issue();
+                                select();
+                            }
+                        } else {
+                            // as in walk_group: the first step untested, then step until the lead
+                            // tree's lanes, then all K trees' lanes, sit on leaves (column 0); the
+                            // next reads are issued before the test
+                            issue();
+                            for (;;) {
+                                select();
+                                issue();
+                                if (__builtin_amdgcn_ballot_w64(fa[0] >= kLeafCol) == 0) {
+                                    bool internal = false;
+#pragma unroll
+                                    for (int i = 1; i < K; ++i)
+                                        internal |= fa[i] >= kLeafCol;
+                                    if (__builtin_amdgcn_ballot_w64(internal) == 0)
+                                        break;
+                                }
+                            }
+#pragma unroll
+                            for (int i = 0; i < K; ++i)
+                                asm volatile("" ::"v"(xv[i]), "v"(lo[i]), "v"(hi[i]));
+                        }
+                        // byte offset of each leaf's payload in the packet
+                        uint32_t voff[K];
+#pragma unroll
+                        for (int i = 0; i < K; ++i)
+                            voff[i] = (r[i] & 0x7FCu) + uint32_t(i) * kCpWin;
+                        if constexpr (MODE == kModeScore) {
+#pragma unroll
+                            for (int i = 0; i < K; ++i)
+                                acc += double(__uint_as_float(pend[i]));
+#pragma unroll
+                            for (int i = 0; i < K; ++i)
+                                pend[i] = __builtin_amdgcn_raw_buffer_load_b32(leaf_rsrc, voff[i], soff, 0);
+                        } else if constexpr (LEAVES) {
+                            const int64_t doc = doc0 + dl;
+#pragma unroll
+                            for (int i = 0; i < K; ++i) {
+                                const int gt = (first_group + j * treeens::kPacketWalkers) * K + i;
+                                if (gt < n_trees && doc < n_docs)
+                                    leaf_ids[doc * n_trees + tree_orig[gt]] =
+                                        __builtin_amdgcn_raw_buffer_load_b32(id_rsrc, voff[i], soff, 0);
+                            }
+                        } else if constexpr (VEC) {
+#pragma unroll
+                            for (int i = 0; i < K; ++i) {
+                                const uint32_t row = __builtin_amdgcn_raw_buffer_load_b32(leaf_rsrc, voff[i], soff, 0);
+                                const float4 v = leaf_vec[int64_t(row - 1u) * vec_stride4 + chunk];
+                                accv[0] += double(v.x);
+                                accv[1] += double(v.y);
+                                accv[2] += double(v.z);
+                                accv[3] += double(v.w);
+                            }
+                        }
+                    }
+                };
+                if (complete_depth >= 0)
+                    walk_groups(std::true_type{});
+                else
+                    walk_groups(std::false_type{});
+            }
+            if constexpr (MODE == kModeScore) {
+#pragma unroll
+                for (int i = 0; i < K; ++i)
+                    acc += double(__uint_as_float(pend[i]));
+            }
+        }
+    };
+    if constexpr (COMPACT) {
+        walk_compact();
+    } else if constexpr (HALF) {
         if (pk_recs > 0)
             walk_packets();
         else
@@ -635,7 +829,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
     // w = (tree-relative left child << 16) | column index; the features come from the LDS
     // document tile as for every other tree, and leaves absorb further steps (column 0). Big
     // tree b goes to split b % n_splits and, within it, to walker (b / n_splits) % n_walkers.
-    if (n_small < n_trees) {
+    if (!COMPACT && n_small < n_trees) {
         __syncthreads(); // the document tile is written (no tile may have been walked)
         const int n_big = n_trees - n_small;
         for (int b = split + n_splits * walker; b < n_big; b += n_splits * n_walkers) {
@@ -805,13 +999,15 @@ __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
 // of the chunk's fixed number of steps (2^steps exceeds every list of the chunk), the same for
 // every lane. Thread e takes elements e, e + 1,024, ... of the block's [doc][feature] order,
 // stepping its (document, feature) pair without a division. Output rows hold n_cols 16-bit
-// codes.
+// codes, each stored as code << code_shift with the shifted-out bits set (code_shift 5 for the
+// compact records' comparison, else 0).
 constexpr int kCodeThreads = 1024;
 __global__ void __launch_bounds__(kCodeThreads)
 code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
             int32_t docs_per_wg,
             const float *__restrict__ table, const uint32_t *__restrict__ table_off,
-            const treeens::CodeChunk *__restrict__ chunks, uint16_t *__restrict__ codes) {
+            const treeens::CodeChunk *__restrict__ chunks, int32_t code_shift,
+            uint16_t *__restrict__ codes) {
     __shared__ float tab[treeens::kCodeTableFloats];
     __shared__ uint32_t toff[treeens::kCodeChunkFeatures + 1];
     const treeens::CodeChunk ch = chunks[blockIdx.y];
@@ -836,7 +1032,7 @@ code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int
             if (probe <= len && x >= tab[first + probe - 1])
                 pos = probe;
         }
-        codes[doc * n_cols + ch.f_begin + j] = uint16_t(pos);
+        codes[doc * n_cols + ch.f_begin + j] = uint16_t((pos << code_shift) | ((1u << code_shift) - 1u));
         d += step_d;
         j += step_j;
         if (j >= nf) {
@@ -850,14 +1046,15 @@ using ScoreFn = void (*)(const void *, int64_t, int32_t, int32_t, const uint2 *,
                          const uint32_t *, int32_t, int32_t, int32_t, int32_t, int32_t, double *,
                          float *, int32_t *, const int32_t *, const uint32_t *, const int32_t *,
                          int32_t, uint32_t *, int32_t, int32_t, const float4 *, int32_t,
-                         int32_t, int32_t, double, int32_t, const uint2 *, int32_t, uint32_t);
+                         int32_t, int32_t, double, int32_t, const uint2 *, int32_t, uint32_t,
+                         const uint32_t *, const int32_t *);
 
 template <int DL, bool HALF, bool NARROW, bool CODED, int MODE>
 ScoreFn pick_k(int k) {
     switch (k) {
-    case 1: return score_kernel<DL, 1, HALF, NARROW, CODED, MODE>;
-    case 2: return score_kernel<DL, 2, HALF, NARROW, CODED, MODE>;
-    case 4: return score_kernel<DL, 4, HALF, NARROW, CODED, MODE>;
+    case 1: return score_kernel<DL, 1, HALF, NARROW, CODED, MODE, false>;
+    case 2: return score_kernel<DL, 2, HALF, NARROW, CODED, MODE, false>;
+    case 4: return score_kernel<DL, 4, HALF, NARROW, CODED, MODE, false>;
     default: return nullptr;
     }
 }
@@ -884,7 +1081,16 @@ ScoreFn pick_dl(const treeens::LdsPlan &p) {
 }
 
 template <int MODE>
-ScoreFn pick_kernel(const treeens::LdsPlan &p) {
+ScoreFn pick_kernel(const treeens::LdsPlan &p, bool compact) {
+    if (compact) {
+        // compact packets: coded 64-document blocks, one workgroup per CU (not the trace)
+        if constexpr (MODE == kModeScore || MODE == kModeLeaves || MODE == kModeVector)
+            return p.coded && p.docs_per_block == 64 && p.lds_bytes == treeens::kLdsPerCu
+                       ? score_kernel<64, treeens::kCompactTrees, false, false, true, MODE, true>
+                       : nullptr;
+        else
+            return nullptr;
+    }
     if (p.lds_bytes != treeens::kLdsPerCu / 2 && p.lds_bytes != treeens::kLdsPerCu)
         return nullptr;
     if (p.coded)
@@ -929,6 +1135,16 @@ struct tree_ens {
     int32_t pk_max_groups = 0;
     int64_t pk_total_rounds = 0;
     uint2 *d_packets = nullptr;
+    // compact packets (coded 64-document plans; in place of the packets above for scores, leaf
+    // ids and vector-valued leaves): trees per lane (0: none), packets per wave, the planner's
+    // figures, the packets, and the leaf payloads and input node ids at the leaves' positions
+    int32_t cp_k = 0;
+    int32_t cp_per_walker = 0;
+    int32_t cp_max_groups = 0;
+    int64_t cp_total_rounds = 0;
+    uint32_t *d_cpackets = nullptr;
+    uint32_t *d_cleaf = nullptr;
+    int32_t *d_cleaf_id = nullptr;
     // big trees (packed indices [n_small, n_trees)): their records in the big-tree format, the
     // first at packed node offset big_off0
     int32_t n_small = 0;
@@ -1010,6 +1226,9 @@ namespace {
 void free_device(tree_ens *h) {
     (void)hipFree(h->d_images);
     (void)hipFree(h->d_packets);
+    (void)hipFree(h->d_cpackets);
+    (void)hipFree(h->d_cleaf);
+    (void)hipFree(h->d_cleaf_id);
     (void)hipFree(h->d_big);
     (void)hipFree(h->d_tile_recs);
     (void)hipFree(h->d_tree_node_off);
@@ -1110,16 +1329,21 @@ LaunchShape choose_launch(const tree_ens *h, int64_t n_blocks) {
     constexpr double kPacketRounds = 0.1;  // switching packets (no barrier), in walker rounds
     const int wg_per_cu = h->plan.lds_bytes <= treeens::kLdsPerCu / 2 ? 2 : 1;
     const int64_t slots = int64_t(kNumCus) * wg_per_cu;
-    // walker packets: one level, each walker's packets in place of the tiles
-    const bool pk = h->pk_recs > 0;
+    // walker packets (8-byte or compact records): one level, each walker's packets in place of
+    // the tiles
+    const bool cp = h->cp_k > 0;
+    const bool pk = cp || h->pk_recs > 0;
     const int n_levels = pk ? 1 : treeens::kTileLevels;
     auto tiles_at = [&](int level) {
-        return pk ? h->pk_per_walker : h->level_begin[level + 1] - h->level_begin[level];
+        return cp ? h->cp_per_walker : pk ? h->pk_per_walker : h->level_begin[level + 1] - h->level_begin[level];
     };
-    auto rounds_at = [&](int level) { return pk ? h->pk_max_groups : h->level_max_rounds[level]; };
+    auto rounds_at = [&](int level) {
+        return cp ? h->cp_max_groups : pk ? h->pk_max_groups : h->level_max_rounds[level];
+    };
     const double switch_rounds = pk ? kPacketRounds : kTileRounds;
-    const double total = double(std::max<int64_t>(pk ? h->pk_total_rounds : h->total_rounds, 1)) +
-                         switch_rounds * double(tiles_at(0));
+    const double total =
+        double(std::max<int64_t>(cp ? h->cp_total_rounds : pk ? h->pk_total_rounds : h->total_rounds, 1)) +
+        switch_rounds * double(tiles_at(0));
     double best = 1e300;
     LaunchShape pick;
     auto consider = [&](int level, int64_t head, int sp) {
@@ -1248,7 +1472,9 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         if (shape.head + tail_slots * shape.splits > 0x7fffffff)
             return fail(TREE_ENS_E_ARG, "too many documents for one launch");
     }
-    ScoreFn fn = pick_kernel<MODE>(h->plan);
+    // compact packets, where the model has them, for every mode but the feature trace
+    const bool cp = h->cp_k > 0 && (MODE == kModeScore || MODE == kModeLeaves || MODE == kModeVector);
+    ScoreFn fn = pick_kernel<MODE>(h->plan, cp);
     if (!fn)
         return fail(TREE_ENS_E_ARG, "unsupported document block size");
     hipError_t e = hipSuccess;
@@ -1340,10 +1566,14 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     // The feature trace of one-workgroup plans keeps the shared tiles: its bitmasks sit past
     // their zero record, where the packets' sub-slots reach.
     const bool pk = h->pk_recs > 0 && !(MODE == kModeUsage && h->plan.lds_bytes == treeens::kLdsPerCu);
-    const uint2 *images = pk ? h->d_packets : h->d_images + h->level_image_off[level];
-    const uint32_t *tile_recs = h->d_tile_recs + (pk ? 0 : h->level_begin[level]);
-    const int n_tiles = pk ? h->pk_per_walker : h->level_begin[level + 1] - h->level_begin[level];
-    const int32_t slot_recs = pk ? h->pk_recs : h->level_slot_recs[level];
+    const uint2 *images = cp   ? reinterpret_cast<const uint2 *>(h->d_cpackets)
+                          : pk ? h->d_packets
+                               : h->d_images + h->level_image_off[level];
+    const uint32_t *tile_recs = h->d_tile_recs + (pk || cp ? 0 : h->level_begin[level]);
+    const int n_tiles = cp   ? h->cp_per_walker
+                        : pk ? h->pk_per_walker
+                             : h->level_begin[level + 1] - h->level_begin[level];
+    const int32_t slot_recs = cp ? treeens::kCompactPacketBytes / 8 : pk ? h->pk_recs : h->level_slot_recs[level];
     (void)hipGetLastError();
     // coded models: one pass turns the float features into 16-bit threshold codes
     const void *docs = X;
@@ -1358,7 +1588,7 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                                              unsigned(h->n_code_chunks)),
                            dim3(kCodeThreads), 0, stream, X, n_docs, n_features, h->n_cols,
                            int32_t(per_wg), h->d_code_table, h->d_code_table_off,
-                           h->d_code_chunks, codes);
+                           h->d_code_chunks, cp ? treeens::kCompactCodeShift : 0, codes);
         docs = codes;
         row_stride = h->n_cols;
     }
@@ -1372,8 +1602,8 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                            partials, scores, leaf_ids, h->d_orig_id, h->d_tree_node_off,
                            h->d_tree_orig, h->n_trees, masks, mask_words, usage_off,
                            reinterpret_cast<const float4 *>(h->d_leaf_vec), h->vec_stride / 4, n_out,
-                           chunk, scale, pk ? h->pk_recs : 0, h->d_big, h->n_small,
-                           h->big_off0);
+                           chunk, scale, cp ? treeens::kCompactPacketBytes / 8 : pk ? h->pk_recs : 0,
+                           h->d_big, h->n_small, h->big_off0, h->d_cleaf, h->d_cleaf_id);
         e = hipGetLastError();
         if (e == hipSuccess && partials) {
             // the tail blocks' entries, in [doc][component] order
@@ -1486,7 +1716,19 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
         e = upload(&h->d_images, images);
     if (e == hipSuccess)
         e = upload(&h->d_tile_recs, p.tile_recs);
-    if (e == hipSuccess && p.pk_recs > 0) {
+    h->cp_k = p.cp_k;
+    h->cp_per_walker = p.cp_per_walker;
+    h->cp_max_groups = p.cp_max_groups;
+    h->cp_total_rounds = p.cp_total_rounds;
+    if (e == hipSuccess && p.cp_k > 0) {
+        // the compact packets replace the 8-byte ones (the feature trace walks the shared tiles)
+        h->pk_recs = 0;
+        e = upload(&h->d_cpackets, p.cp_packets);
+        if (e == hipSuccess)
+            e = upload(&h->d_cleaf, p.cp_leaf);
+        if (e == hipSuccess)
+            e = upload(&h->d_cleaf_id, p.cp_leaf_id);
+    } else if (e == hipSuccess && p.pk_recs > 0) {
         std::vector<uint2> packets(p.packets.size());
         std::memcpy(packets.data(), p.packets.data(), p.packets.size() * sizeof(NodeRec));
         e = upload(&h->d_packets, packets);

@@ -476,6 +476,164 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
     return 0;
 }
 
+// Walk all documents through the compact packets (4-byte records, pair reads, leaf payloads in
+// their own arrays) the way the kernel addresses them: documents staged as code << 5 | 31,
+// per wave K windows of 4096 / K bytes after the document tile (aligned to their size), the
+// headers after all windows. Every feature read must stay in the document tile and every pair
+// read in the window of its slot. Outputs as emu_walk; returns 2 when the model has no compact
+// packets, else 0 or 1 with a message, or a negative packer status. *k_out: trees per lane.
+int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                     const float *threshold, const int32_t *left, const int32_t *right,
+                     const float *value, int32_t n_outputs, uint32_t flags, const float *X,
+                     int64_t n_docs, int32_t n_features, int32_t *leaf_ids, double *scores,
+                     int32_t *k_out) {
+    treeens::Packed p;
+    std::string err;
+    const int rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value,
+                                       n_outputs, flags, p, err);
+    if (rc != treeens::kOk) {
+        g_msg = err;
+        return rc;
+    }
+    if (k_out)
+        *k_out = p.cp_k;
+    if (p.cp_k == 0) {
+        g_msg = "no compact packets";
+        return 2;
+    }
+    const treeens::LdsPlan &pl = p.plan;
+    constexpr int32_t W = treeens::kPacketWalkers;
+    constexpr int32_t kWords = treeens::kCompactPacketBytes / 4;
+    const int DL = pl.docs_per_block, K = p.cp_k;
+    if (DL != 64 || !pl.coded || pl.elem_bytes != 2 || (K != 2 && K != 4) || p.n_small != n_trees)
+        return bad("compact packets on a plan they do not support");
+    const uint32_t xs = uint32_t(pl.xs_bytes);
+    const uint32_t cw = uint32_t(treeens::compact_window_base(pl.xs_bytes));
+    const uint32_t ch = cw + uint32_t(W) * treeens::kCompactWindowBytes;
+    const uint32_t win = uint32_t(treeens::kCompactWindowBytes / K);
+    if (cw % win || ch + uint32_t(W) * treeens::kCompactHeaderBytes > uint32_t(treeens::kLdsPerCu))
+        return bad("compact windows and headers do not fit the LDS");
+    const size_t total = size_t(W) * size_t(p.cp_per_walker) * size_t(kWords);
+    if (p.cp_packets.size() != total || p.cp_leaf.size() != total || p.cp_leaf_id.size() != total)
+        return bad("compact packet arrays have the wrong size");
+    std::vector<uint8_t> lds(size_t(treeens::kLdsPerCu), 0);
+    auto u32_at = [&](uint32_t a) {
+        uint32_t v;
+        std::memcpy(&v, lds.data() + a, 4);
+        return v;
+    };
+    const bool vec = n_outputs > 1;
+    std::vector<int32_t> seen(size_t(n_trees), 0);
+    for (int64_t i = 0; i < n_docs * n_trees; i++)
+        leaf_ids[i] = -1;
+    for (int64_t d = 0; d < n_docs * n_outputs; d++)
+        scores[d] = 0.0;
+    for (int64_t doc0 = 0; doc0 < n_docs; doc0 += DL) {
+        for (int c = 0; c <= p.n_cols; c++) {
+            for (int dl = 0; dl < DL; dl++) {
+                const int64_t doc = doc0 + dl;
+                const uint32_t code = c == 0 || doc >= n_docs ? 0u : code_of(p, c - 1, X[doc * n_features + c - 1]);
+                if (code >= treeens::kCompactNeverRight)
+                    return bad("a code reaches the never-right threshold");
+                const uint16_t v = uint16_t((code << treeens::kCompactCodeShift) | 31u);
+                std::memcpy(lds.data() + (size_t(c) * DL + dl) * 2, &v, 2);
+            }
+        }
+        for (int32_t v = 0; v < W; v++) {
+            for (int32_t q = 0; q < p.cp_per_walker; q++) {
+                const size_t at = (size_t(v) * size_t(p.cp_per_walker) + size_t(q)) * size_t(kWords);
+                const uint32_t my_win = cw + uint32_t(v) * treeens::kCompactWindowBytes;
+                const uint32_t my_hdr = ch + uint32_t(v) * treeens::kCompactHeaderBytes;
+                std::memcpy(lds.data() + my_win, p.cp_packets.data() + at, treeens::kCompactWindowBytes);
+                std::memcpy(lds.data() + my_hdr, p.cp_packets.data() + at + treeens::kCompactWindowBytes / 4,
+                            treeens::kCompactHeaderBytes);
+                const int ng = int(u32_at(my_hdr)), complete = int32_t(u32_at(my_hdr + 4));
+                const int g0 = int(u32_at(my_hdr + 8));
+                if (ng < 0 || treeens::kCompactHeaderWords + ng * K > treeens::kCompactHeaderBytes / 4)
+                    return bad("compact header out of range");
+                for (int j = 0; j < ng; j++) {
+                    const int g = g0 + j * W;
+                    if (g % W != v)
+                        return bad("a compact packet holds a group of another wave");
+                    const uint32_t roots = my_hdr + 4u * uint32_t(treeens::kCompactHeaderWords + j * K);
+                    if (roots % uint32_t(4 * K) != 0)
+                        return bad("a group's root records are not aligned for one read");
+                    for (int i = 0; i < K; i++) {
+                        const int gt = g * K + i;
+                        const uint32_t tb = my_win + uint32_t(i) * win;
+                        if (gt >= n_trees && complete >= 0)
+                            return bad("compact: a complete packet has an idle slot");
+                        for (int dl = 0; dl < DL && doc0 + dl < n_docs; dl++) {
+                            const int64_t doc = doc0 + dl;
+                            uint32_t r = u32_at(roots + 4u * uint32_t(i));
+                            int steps = 0;
+                            auto step = [&](uint32_t cur, uint32_t *next) -> int {
+                                const uint32_t fa = ((cur >> 4) & 0x1FF80u) | uint32_t(dl * 2);
+                                if (fa + 2 > xs)
+                                    return bad("compact: feature address outside the document tile");
+                                const uint32_t pa = (cur & 0x7F8u) | tb;
+                                if (pa != (cur & 0x7F8u) + tb || pa < tb || pa + 8 > tb + win)
+                                    return bad("compact: pair read outside the slot's window");
+                                uint16_t x;
+                                std::memcpy(&x, lds.data() + fa, 2);
+                                const bool right_side = uint32_t(x) >= (cur >> 16);
+                                *next = u32_at(pa + (right_side ? 4u : 0u));
+                                return 0;
+                            };
+                            for (;;) {
+                                if (complete >= 0 ? steps == complete : ((r >> 4) & 0x1FF80u) == 0u)
+                                    break;
+                                uint32_t nxt;
+                                if (const int e = step(r, &nxt))
+                                    return e;
+                                r = nxt;
+                                if (++steps > p.max_depth + 1)
+                                    return bad("compact: walk longer than the deepest tree");
+                            }
+                            if (((r >> 4) & 0x1FF80u) != 0u)
+                                return bad("compact: walk ended on an internal node");
+                            uint32_t again;
+                            if (const int e = step(r, &again))
+                                return e;
+                            if (again != r)
+                                return bad("compact: a leaf does not absorb a further step");
+                            const size_t w = at + size_t((r & 0x7FCu) + uint32_t(i) * win) / 4;
+                            if (gt >= n_trees) {
+                                if (p.cp_leaf[w] != (vec ? 1u : 0u))
+                                    return bad("compact: an idle slot's payload is not zero");
+                                continue;
+                            }
+                            const int32_t id = p.cp_leaf_id[w];
+                            const int32_t orig_tree = p.tree_orig[size_t(gt)];
+                            const int64_t tn = tree_offsets[orig_tree + 1] - tree_offsets[orig_tree];
+                            if (id < 0 || id >= tn || feature[tree_offsets[orig_tree] + id] >= 0)
+                                return bad("compact: the payload's node id is not a leaf of the tree");
+                            leaf_ids[doc * n_trees + orig_tree] = id;
+                            if (vec) {
+                                const int64_t row = int64_t(p.cp_leaf[w]) - 1;
+                                if (row < 1 || row > int64_t(p.nodes.size()))
+                                    return bad("compact: leaf names a row outside the leaf-vector table");
+                                for (int c = 0; c < n_outputs; c++)
+                                    scores[doc * n_outputs + c] +=
+                                        double(p.leaf_vec[size_t(row) * size_t(p.vec_stride) + size_t(c)]);
+                            } else {
+                                scores[doc] += double(as_float(p.cp_leaf[w]));
+                            }
+                        }
+                        if (gt < n_trees)
+                            seen[size_t(p.tree_orig[size_t(gt)])]++;
+                    }
+                }
+            }
+        }
+    }
+    const int64_t blocks = (n_docs + DL - 1) / DL;
+    for (int32_t t = 0; t < n_trees; t++)
+        if (seen[size_t(t)] != blocks)
+            return bad("compact: tree " + std::to_string(t) + " is not walked exactly once per block");
+    return 0;
+}
+
 // The packer's tree order (order[i] = input index of the i-th packed tree) and, per tile of
 // tiling 0, its complete depth (-1: not all trees complete of one depth). Returns the number
 // of tiles (at most max_tiles are written), or a negative packer status.

@@ -31,6 +31,9 @@ def emu(tmp_path_factory):
     lib.emu_walk.restype = ctypes.c_int
     lib.emu_walk.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_uint32, P,
                              ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P, P]
+    lib.emu_walk_compact.restype = ctypes.c_int
+    lib.emu_walk_compact.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_uint32, P,
+                                     ctypes.c_int64, ctypes.c_int32, P, P, P]
     lib.emu_message.restype = ctypes.c_char_p
     lib.emu_tree_order.restype = ctypes.c_int
     lib.emu_tree_order.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_uint32, P, P, ctypes.c_int32]
@@ -53,6 +56,26 @@ def _walk(lib, ens, X, level, flags=0, leaf_values=None):
     return leaves, (scores[:, 0] if leaf_values is None else scores), plan
 
 
+def _walk_compact(lib, ens, X, flags=0, leaf_values=None):
+    """Leaf ids, scores and trees per lane of the compact packets, or None when the model has
+    none."""
+    vals = ens.value if leaf_values is None else leaf_values
+    n_out = 1 if leaf_values is None else leaf_values.shape[1]
+    arrs = [np.ascontiguousarray(ens.tree_offsets, np.int64), np.ascontiguousarray(ens.feature, np.int32),
+            np.ascontiguousarray(ens.threshold, np.float32), np.ascontiguousarray(ens.left, np.int32),
+            np.ascontiguousarray(ens.right, np.int32), np.ascontiguousarray(vals, np.float32)]
+    X = np.ascontiguousarray(X, np.float32)
+    leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
+    scores = np.empty((X.shape[0], n_out), np.float64)
+    k = np.zeros(1, np.int32)
+    rc = lib.emu_walk_compact(ens.n_trees, *[a.ctypes.data for a in arrs], n_out, flags, X.ctypes.data,
+                              X.shape[0], X.shape[1], leaves.ctypes.data, scores.ctypes.data, k.ctypes.data)
+    if rc == 2:
+        return None
+    assert rc == 0, lib.emu_message().decode()
+    return leaves, (scores[:, 0] if leaf_values is None else scores), int(k[0])
+
+
 def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
     ref_scores, ref_leaves, _ = oracle.score(ens, X, rule=flags)
     plans = []
@@ -61,6 +84,12 @@ def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
         np.testing.assert_array_equal(leaves, ref_leaves, err_msg=f"tiling {lv}")
         np.testing.assert_allclose(scores, ref_scores, rtol=1e-12, atol=1e-12, err_msg=f"tiling {lv}")
         plans.append(plan)
+    # the compact packets, where the model has them, reach the same leaves
+    compact = _walk_compact(lib, ens, X, flags)
+    if compact is not None:
+        leaves, scores, _ = compact
+        np.testing.assert_array_equal(leaves, ref_leaves, err_msg="compact packets")
+        np.testing.assert_allclose(scores, ref_scores, rtol=1e-12, atol=1e-12, err_msg="compact packets")
     return plans[0]
 
 
@@ -130,6 +159,11 @@ def test_vector_valued_leaves(emu, wl, n_trees, n_out, kind):
         leaves, scores, _ = _walk(emu, ens, X, lv, leaf_values=vals)
         np.testing.assert_array_equal(leaves, ref_leaves, err_msg=f"tiling {lv}")
         np.testing.assert_allclose(scores, ref, rtol=1e-12, atol=1e-12, err_msg=f"tiling {lv}")
+    compact = _walk_compact(emu, ens, X, leaf_values=vals)
+    assert (compact is not None) == (wl == "large_5kx256_f700_1M")
+    if compact is not None:
+        np.testing.assert_array_equal(compact[0], ref_leaves, err_msg="compact packets")
+        np.testing.assert_allclose(compact[1], ref, rtol=1e-12, atol=1e-12, err_msg="compact packets")
 
 
 def test_coded_documents_with_corner_values(emu):
@@ -394,3 +428,66 @@ def test_tree_size_limit(emu):
     rc = emu.emu_walk(1, *[a.ctypes.data for a in arrs], 1, 0, X.ctypes.data, 10, 5, 0,
                       leaves.ctypes.data, scores.ctypes.data, plan.ctypes.data)
     assert rc == -2 and b"65535" in emu.emu_message()
+
+
+def _compact_k(lib, ens, X, flags=0):
+    got = _walk_compact(lib, ens, X, flags)
+    return None if got is None else got[2]
+
+
+def test_compact_packets_of_the_large_workload(emu):
+    """The 700-feature coded workload's 511-node trees take the compact packets with two trees
+    per lane (a 2,040-byte tree fills a 2 KiB window but its zero pair); its leaves and scores
+    through them equal the oracle's (checked inside _check), under both rules."""
+    cfg = W.WORKLOADS["large_5kx256_f700_1M"]
+    ens = W.make_ensemble(cfg, n_trees=150)
+    X = W.make_docs(cfg, n_docs=130)
+    for flags in (0, 1):
+        _check(emu, ens, X, flags=flags, levels=(0,))
+        assert _compact_k(emu, ens, X, flags) == 2
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_compact_packets_random_coded_models(emu, seed):
+    """Random coded models (700 features and trees of a few hundred nodes: float documents would
+    not fit 64 per block) mixed with small and single-leaf trees, so that groups, windows and
+    idle slots of a last partial group vary; +-inf and special thresholds under both rules, and
+    documents with NaN, +-inf and exact ties, all reach the oracle's leaves."""
+    rng = np.random.default_rng(900 + seed)
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf], np.float32)
+    big = W.random_ensemble(900 + seed, n_trees=int(rng.integers(3, 70)), n_features=700, min_leaves=150,
+                            max_leaves=256, thr_values=pool if seed % 3 == 0 else None)
+    small = W.random_ensemble(950 + seed, n_trees=int(rng.integers(1, 8)), n_features=700, min_leaves=1,
+                              max_leaves=int(rng.choice([1, 2, 9])))
+    trees = [big.tree(t) for t in range(big.n_trees)] + [small.tree(t) for t in range(small.n_trees)]
+    ens = _stack([trees[i] for i in rng.permutation(len(trees))], 700)
+    X = W.random_docs(900 + seed, n_docs=int(rng.integers(1, 140)), n_features=700, zero_frac=0.3)
+    X[:3, :50] = np.array([np.nan, np.inf, -np.inf], np.float32)[:X.shape[0], None][:3]
+    internal = np.nonzero(ens.feature >= 0)[0]
+    for _ in range(200):
+        n = internal[rng.integers(0, internal.size)]
+        X[rng.integers(0, X.shape[0]), ens.feature[n]] = ens.threshold[n]
+    for flags in (0, 1):
+        plan = _check(emu, ens, X, flags=flags, levels=(0,))
+        assert plan[3] == 1, plan
+        assert _compact_k(emu, ens, X, flags) == 2
+
+
+def test_compact_packets_not_built_where_they_do_not_apply(emu):
+    """Float documents, trees over 511 nodes, and coded models with more distinct thresholds
+    per feature than the 11-bit field holds keep the 8-byte packets only."""
+    cfg = W.WORKLOADS["rank_1kx32"]
+    ens = W.make_ensemble(cfg, n_trees=50)
+    assert _compact_k(emu, ens, W.make_docs(cfg, n_docs=10)) is None
+    big = W.random_ensemble(4, n_trees=20, n_features=700, min_leaves=257, max_leaves=300)
+    X = W.random_docs(4, 10, 700)
+    _check(emu, big, X, levels=(0,))
+    assert _compact_k(emu, big, X) is None
+    # 2,100 distinct thresholds on feature 0 (codes beyond 2,046)
+    many = W.random_ensemble(5, n_trees=20, n_features=700, min_leaves=200, max_leaves=256)
+    internal = np.nonzero(many.feature >= 0)[0]
+    many.feature[internal[:2100]] = 0
+    many.threshold[internal[:2100]] = np.arange(2100, dtype=np.float32) / 2100.0
+    Xm = W.random_docs(5, 10, 700)
+    _check(emu, many, Xm, levels=(0,))
+    assert _compact_k(emu, many, Xm) is None
