@@ -226,7 +226,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             for (auto &tv : thr_of) {
                 std::sort(tv.begin(), tv.end());
                 tv.erase(std::unique(tv.begin(), tv.end()), tv.end());
-                if (tv.size() > kMaxCode || tv.size() > size_t(kCodeTableFloats))
+                if (tv.size() > kMaxCode || tv.size() >= size_t(kCodeTableFloats))
                     code_ok = 0;
             }
         }
@@ -866,18 +866,51 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
             p.code_table.insert(p.code_table.end(), thr_of[size_t(f)].begin(), thr_of[size_t(f)].end());
         }
         p.code_table_off[size_t(n_cols)] = uint32_t(p.code_table.size());
+        // bits of a feature's search: the least s with 2^s - 1 >= |T_f|
+        auto bits = [&](int32_t f) {
+            int32_t s = 0;
+            while ((uint32_t(1) << s) - 1u < p.code_table_off[size_t(f) + 1] - p.code_table_off[size_t(f)])
+                s++;
+            return s;
+        };
+        std::vector<float> sorted;
         int32_t fb = 0;
         while (fb < n_cols) {
-            int32_t fe = fb;
-            while (fe < n_cols && fe - fb < kCodeChunkFeatures &&
-                   p.code_table_off[size_t(fe) + 1] - p.code_table_off[size_t(fb)] <= uint32_t(kCodeTableFloats))
+            int32_t fe = fb + 1, steps = bits(fb);
+            while (fe < n_cols && fe - fb < kCodeChunkFeatures) {
+                const int32_t s = std::max(steps, bits(fe));
+                if (int64_t(fe + 1 - fb) * ((int64_t(1) << s) - 1) > kCodeTableFloats)
+                    break;
+                steps = s;
                 fe++;
-            int32_t steps = 0;
-            for (int32_t f = fb; f < fe; f++)
-                while ((p.code_table_off[size_t(f) + 1] - p.code_table_off[size_t(f)]) >> steps)
-                    steps++;
-            p.code_chunks.push_back(CodeChunk{fb, fe, int32_t(p.code_table_off[size_t(fb)]),
-                                              int32_t(p.code_table_off[size_t(fe)]), steps});
+            }
+            const int32_t slots = 1 << steps;
+            const int32_t begin = int32_t(p.code_search.size());
+            p.code_search.resize(p.code_search.size() + size_t(fe - fb) * size_t(slots - 1), std::nanf(""));
+            for (int32_t f = fb; f < fe; f++) {
+                // in-order walk of the complete tree of slots 1 .. slots - 1 takes the sorted list
+                sorted.assign(p.code_table.begin() + p.code_table_off[size_t(f)],
+                              p.code_table.begin() + p.code_table_off[size_t(f) + 1]);
+                sorted.resize(size_t(slots - 1), std::nanf(""));
+                float *dst = p.code_search.data() + begin + size_t(f - fb) * size_t(slots - 1) - 1; // slot i
+                size_t next = 0;
+                std::vector<std::pair<int32_t, bool>> stack; // (slot, children done)
+                stack.push_back({1, false});
+                while (!stack.empty()) {
+                    auto [i, done] = stack.back();
+                    stack.pop_back();
+                    if (i >= slots)
+                        continue;
+                    if (done) {
+                        dst[i] = sorted[next++];
+                        stack.push_back({2 * i + 1, false});
+                    } else {
+                        stack.push_back({i, true});
+                        stack.push_back({2 * i, false});
+                    }
+                }
+            }
+            p.code_chunks.push_back(CodeChunk{fb, fe, begin, int32_t(p.code_search.size()), steps});
             fb = fe;
         }
     }

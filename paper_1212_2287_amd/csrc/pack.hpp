@@ -158,12 +158,19 @@ struct LdsPlan {
 // leaves' code column holds 0, and 0 >= bits is false, so leaves still go "left" to themselves.
 // Coding halves the staged bytes per document; it is used when float features would not fit
 // 64 documents in the LDS document tile.
+// The coding kernel takes the features in chunks. A chunk of s search steps gives each of its
+// features 2^s - 1 table entries, slots 1 .. 2^s - 1 of a complete search tree in breadth-first
+// order (slot i has children 2i and 2i + 1; slot i is entry i - 1): the feature's sorted list
+// padded with NaN. Descending i = 2i + (x >= slot i) for s steps from i = 1 ends at
+// 2^s + code_f(x): NaN entries never compare true (and sort after every threshold), so they
+// count nothing, and a NaN x never goes right. The odd stride puts the same slot of successive
+// features in different LDS banks.
 struct CodeChunk {
     int32_t f_begin, f_end;         // features [f_begin, f_end)
-    int32_t table_begin, table_end; // their thresholds in the concatenated table
-    int32_t search_steps;           // bits of the longest threshold list of the chunk
+    int32_t table_begin, table_end; // their (f_end - f_begin) * (2^s - 1) entries in code_search
+    int32_t search_steps;           // s: bits of the longest threshold list of the chunk
 };
-constexpr int kCodeTableFloats = 16384;  // LDS thresholds per coding workgroup (64 KiB)
+constexpr int kCodeTableFloats = 16384;  // LDS table slots per coding workgroup (64 KiB)
 constexpr int kCodeChunkFeatures = 256;  // features per coding workgroup at most
 constexpr uint32_t kMaxCode = 0xFFFEu;    // codes are 16-bit; 0xFFFF = "never right"
 
@@ -235,6 +242,7 @@ struct Packed {
     std::vector<float> code_table;         // T_0, T_1, ... concatenated
     std::vector<uint32_t> code_table_off;  // [n_cols + 1] start of T_f in code_table
     std::vector<CodeChunk> code_chunks;    // features grouped for the coding kernel
+    std::vector<float> code_search;        // the chunks' search tables (see CodeChunk)
 };
 
 // Outputs per leaf at most (vector-valued leaves).

@@ -126,17 +126,11 @@ __device__ __forceinline__ uint32_t narrow_child_coded(uint32_t w, uint32_t code
 
 // Compact records: the side of the children pair {lo, hi} that a 4-byte record r sends a
 // document to, whose staged value is x = code << 5 | 31: x >= the record's upper half is
-// code >= threshold. An SDWA compare reads the upper half in place; the s_nop covers the
-// VALU-writes-VCC / VALU-reads-VCC hazard as in narrow_child.
+// code >= threshold. Plain code: the compiler reads the upper half in place with an SDWA
+// compare and places the compare-to-select wait states itself (filling them with the other
+// trees' work).
 __device__ __forceinline__ uint32_t compact_child(uint32_t x, uint32_t r, uint32_t lo, uint32_t hi) {
-    uint32_t out;
-    asm("v_cmp_ge_u32_sdwa vcc, %1, %2 src0_sel:DWORD src1_sel:WORD_1\n\t"
-        "s_nop 1\n\t"
-        "v_cndmask_b32 %0, %3, %4, vcc"
-        : "=v"(out)
-        : "v"(x), "v"(r), "v"(lo), "v"(hi)
-        : "vcc");
-    return out;
+    return x >= (r >> 16) ? hi : lo;
 }
 
 template <int DL, int K, bool HALF, bool NARROW, bool CODED, int MODE, bool COMPACT>
@@ -995,49 +989,87 @@ __global__ void fill_zero_kernel(float *__restrict__ scores, int64_t n) {
 
 // Threshold codes of a block of documents for a chunk of features: code_f(x) is the number of
 // f's sorted distinct thresholds t with x >= t (a NaN x compares false everywhere and gets 0).
-// The chunk's thresholds are staged in LDS; the count is found by a branch-free binary descent
-// of the chunk's fixed number of steps (2^steps exceeds every list of the chunk), the same for
-// every lane. Thread e takes elements e, e + 1,024, ... of the block's [doc][feature] order,
+// The chunk's search tables are staged in LDS: feature j's 2^s - 1 entries hold its list as a
+// complete search tree in breadth-first order (slot i at entry i - 1), padded with NaN (which
+// never compares true), so the count is s steps of i = 2i + (x >= slot i) from i = 1, the same
+// for every lane, and code = i - 2^s. Thread e takes elements e, e + 1,024, ... of the block's [doc][feature] order,
 // stepping its (document, feature) pair without a division. Output rows hold n_cols 16-bit
 // codes, each stored as code << code_shift with the shifted-out bits set (code_shift 5 for the
 // compact records' comparison, else 0).
 constexpr int kCodeThreads = 1024;
+// One step of the search: 2i + (x >= t) as a compare into VCC and an add-with-carry of i to
+// itself (two VALU ops; the s_nop as in narrow_child).
+__device__ __forceinline__ uint32_t search_step(uint32_t i, float x, float t) {
+    uint32_t r;
+    asm("v_cmp_ge_f32 vcc, %1, %2\n\t"
+        "s_nop 1\n\t"
+        "v_addc_co_u32 %0, vcc, %3, %3, vcc"
+        : "=v"(r)
+        : "v"(x), "v"(t), "v"(i)
+        : "vcc");
+    return r;
+}
 __global__ void __launch_bounds__(kCodeThreads)
 code_kernel(const float *__restrict__ X, int64_t n_docs, int32_t n_features, int32_t n_cols,
-            int32_t docs_per_wg,
-            const float *__restrict__ table, const uint32_t *__restrict__ table_off,
-            const treeens::CodeChunk *__restrict__ chunks, int32_t code_shift,
+            int32_t docs_per_wg, const float *__restrict__ table,
+            const treeens::CodeChunk *__restrict__ chunks, int32_t n_chunks, int32_t code_shift,
             uint16_t *__restrict__ codes) {
     __shared__ float tab[treeens::kCodeTableFloats];
-    __shared__ uint32_t toff[treeens::kCodeChunkFeatures + 1];
-    const treeens::CodeChunk ch = chunks[blockIdx.y];
+    // Workgroups are dealt to the XCDs in index order: index L runs chunk (L % (8C)) / 8 of
+    // document block (L / (8C)) * 8 + L % 8, so all C chunks of a block share one XCD and run
+    // one after another there, and the cache lines of a row that two neighbouring chunks
+    // share come from HBM once.
+    const int64_t L = blockIdx.x;
+    const int64_t per = int64_t(kXcds) * n_chunks;
+    const int chunk = int((L % per) / kXcds);
+    const int64_t block = (L / per) * kXcds + L % kXcds;
+    if (block * docs_per_wg >= n_docs)
+        return;
+    const treeens::CodeChunk ch = chunks[chunk];
     const int nf = ch.f_end - ch.f_begin;
+    const int steps = ch.search_steps;
     for (int i = threadIdx.x; i < ch.table_end - ch.table_begin; i += kCodeThreads)
         tab[i] = table[ch.table_begin + i];
-    for (int j = threadIdx.x; j <= nf; j += kCodeThreads)
-        toff[j] = table_off[ch.f_begin + j] - uint32_t(ch.table_begin);
     __syncthreads();
-    const int64_t d0 = int64_t(blockIdx.x) * docs_per_wg;
+    const int64_t d0 = block * docs_per_wg;
     const int n = int(min<int64_t>(docs_per_wg, n_docs - d0)) * nf;
     // nf <= 256: every step moves at least 4 documents on
     const int step_d = kCodeThreads / nf, step_j = kCodeThreads - step_d * nf;
     int d = int(threadIdx.x) / nf, j = int(threadIdx.x) - d * nf;
-    for (int e = threadIdx.x; e < n; e += kCodeThreads) {
-        const int64_t doc = d0 + d;
-        const float x = X[doc * n_features + ch.f_begin + j];
-        const uint32_t first = toff[j], len = toff[j + 1] - first;
-        uint32_t pos = 0; // thresholds known to be <= x
-        for (int s = ch.search_steps - 1; s >= 0; --s) {
-            const uint32_t probe = pos + (1u << s);
-            if (probe <= len && x >= tab[first + probe - 1])
-                pos = probe;
+    const uint32_t leaf0 = 1u << steps;
+    // kCodeBatch elements per thread at a time: their feature values load together, then their
+    // searches interleave (independent LDS round trips in flight)
+    constexpr int kCodeBatch = 4;
+    for (int e0 = threadIdx.x; e0 < n; e0 += kCodeBatch * kCodeThreads) {
+        float x[kCodeBatch];
+        int64_t at[kCodeBatch];
+        int t0[kCodeBatch];
+        uint32_t i[kCodeBatch];
+#pragma unroll
+        for (int u = 0; u < kCodeBatch; ++u) {
+            const bool live = e0 + u * kCodeThreads < n;
+            const int64_t doc = d0 + d;
+            at[u] = live ? doc * n_cols + ch.f_begin + j : -1;
+            x[u] = live ? X[doc * n_features + ch.f_begin + j] : 0.0f;
+            t0[u] = j * int(leaf0 - 1u) - 1; // slot i of feature j is tab[t0 + i]
+            i[u] = 1u;
+            d += step_d;
+            j += step_j;
+            if (j >= nf) {
+                j -= nf;
+                ++d;
+            }
         }
-        codes[doc * n_cols + ch.f_begin + j] = uint16_t((pos << code_shift) | ((1u << code_shift) - 1u));
-        d += step_d;
-        j += step_j;
-        if (j >= nf) {
-            j -= nf;
-            ++d;
+        for (int s = 0; s < steps; ++s) {
+#pragma unroll
+            for (int u = 0; u < kCodeBatch; ++u)
+                i[u] = search_step(i[u], x[u], tab[t0[u] + int(i[u])]);
+        }
+#pragma unroll
+        for (int u = 0; u < kCodeBatch; ++u) {
+            const uint32_t code = i[u] - leaf0;
+            if (at[u] >= 0)
+                codes[at[u]] = uint16_t((code << code_shift) | ((1u << code_shift) - 1u));
         }
     }
 }
@@ -1161,8 +1193,7 @@ struct tree_ens {
     int32_t vec_stride = 0;
     float *d_leaf_vec = nullptr;
     // coded models
-    float *d_code_table = nullptr;
-    uint32_t *d_code_table_off = nullptr;
+    float *d_code_search = nullptr; // the coding chunks' search tables
     treeens::CodeChunk *d_code_chunks = nullptr;
     int32_t n_code_chunks = 0;
     // kernel specialised for the model (TREE_ENS_CODEGEN), used by tree_ens_predict
@@ -1235,8 +1266,7 @@ void free_device(tree_ens *h) {
     (void)hipFree(h->d_tree_orig);
     (void)hipFree(h->d_orig_id);
     (void)hipFree(h->d_leaf_vec);
-    (void)hipFree(h->d_code_table);
-    (void)hipFree(h->d_code_table_off);
+    (void)hipFree(h->d_code_search);
     (void)hipFree(h->d_code_chunks);
     (void)hipFree(h->d_scratch);
     if (h->scratch_done)
@@ -1584,11 +1614,12 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
         int64_t per_wg = 256;
         while (per_wg < 4096 && ((n_docs + per_wg - 1) / per_wg) * h->n_code_chunks > 4 * kNumCus)
             per_wg *= 2;
-        hipLaunchKernelGGL(code_kernel, dim3(unsigned((n_docs + per_wg - 1) / per_wg),
-                                             unsigned(h->n_code_chunks)),
+        const int64_t code_blocks = (n_docs + per_wg - 1) / per_wg;
+        hipLaunchKernelGGL(code_kernel,
+                           dim3(unsigned((code_blocks + kXcds - 1) / kXcds * kXcds * h->n_code_chunks)),
                            dim3(kCodeThreads), 0, stream, X, n_docs, n_features, h->n_cols,
-                           int32_t(per_wg), h->d_code_table, h->d_code_table_off,
-                           h->d_code_chunks, cp ? treeens::kCompactCodeShift : 0, codes);
+                           int32_t(per_wg), h->d_code_search, h->d_code_chunks, h->n_code_chunks,
+                           cp ? treeens::kCompactCodeShift : 0, codes);
         docs = codes;
         row_stride = h->n_cols;
     }
@@ -1758,9 +1789,7 @@ int tree_ens_create_multi(tree_ens_t **out, int32_t n_trees, const int64_t *tree
             e = hipModuleGetFunction(&h->cg_fn, h->cg_module, "tree_ens_cg");
     }
     if (e == hipSuccess && p.plan.coded) {
-        e = upload(&h->d_code_table, p.code_table);
-        if (e == hipSuccess)
-            e = upload(&h->d_code_table_off, p.code_table_off);
+        e = upload(&h->d_code_search, p.code_search);
         if (e == hipSuccess)
             e = upload(&h->d_code_chunks, p.code_chunks);
         h->n_code_chunks = int32_t(p.code_chunks.size());

@@ -43,27 +43,26 @@ uint16_t code_of(const treeens::Packed &p, int f, float x) {
     return c;
 }
 
-// code_f(x) by the coding kernel's branch-free descent over its chunk's table: the largest pos
-// with x >= t[pos - 1], found in the chunk's fixed number of halving steps. Returns -1 when the
-// chunk layout cannot hold feature f's list.
+// code_f(x) by the coding kernel's descent over its chunk's search table: s steps of
+// i = 2i + (x >= slot i) from i = 1, code = i - 2^s. Returns -1 when the chunk layout cannot
+// hold feature f's search (sizes, slot count, the LDS table).
 int32_t code_by_descent(const treeens::Packed &p, int f, float x) {
     for (const treeens::CodeChunk &ch : p.code_chunks) {
         if (f < ch.f_begin || f >= ch.f_end)
             continue;
-        const uint32_t first = p.code_table_off[size_t(f)];
-        const uint32_t len = p.code_table_off[size_t(f) + 1] - first;
-        if (ch.search_steps < 0 || ch.search_steps > 16 || (uint64_t(1) << ch.search_steps) <= len ||
-            int64_t(first) < ch.table_begin || int64_t(first + len) > ch.table_end ||
-            ch.table_end - ch.table_begin > treeens::kCodeTableFloats ||
-            ch.f_end - ch.f_begin > treeens::kCodeChunkFeatures)
+        const uint32_t len = p.code_table_off[size_t(f) + 1] - p.code_table_off[size_t(f)];
+        const int s = ch.search_steps;
+        if (s < 0 || s > 14 || (uint64_t(1) << s) - 1 < len || ch.f_end - ch.f_begin > treeens::kCodeChunkFeatures ||
+            int64_t(ch.table_end - ch.table_begin) != int64_t(ch.f_end - ch.f_begin) * ((int64_t(1) << s) - 1) ||
+            ch.table_end - ch.table_begin > treeens::kCodeTableFloats || ch.table_begin < 0 ||
+            size_t(ch.table_end) > p.code_search.size())
             return -1;
-        uint32_t pos = 0;
-        for (int s = ch.search_steps - 1; s >= 0; --s) {
-            const uint32_t probe = pos + (1u << s);
-            if (probe <= len && x >= p.code_table[first + probe - 1])
-                pos = probe;
-        }
-        return int32_t(pos);
+        // entry i - 1 of feature f's 2^s - 1 entries holds slot i
+        const size_t t0 = size_t(ch.table_begin) + size_t(f - ch.f_begin) * ((size_t(1) << s) - 1);
+        uint32_t i = 1;
+        for (int k = 0; k < s; ++k)
+            i = 2u * i + (x >= p.code_search[t0 + i - 1] ? 1u : 0u);
+        return int32_t(i - (1u << s));
     }
     return -1;
 }
@@ -631,6 +630,46 @@ int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t
     for (int32_t t = 0; t < n_trees; t++)
         if (seen[size_t(t)] != blocks)
             return bad("compact: tree " + std::to_string(t) + " is not walked exactly once per block");
+    return 0;
+}
+
+// Every coded feature's search table against a plain count: at each of its thresholds, just
+// below each, at +-inf, +-0 and NaN, the descent must give |{t : x >= t}|. Returns 2 when the
+// model is not coded, else 0 or 1 with a message.
+int emu_code_check(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
+                   const float *threshold, const int32_t *left, const int32_t *right,
+                   const float *value, uint32_t flags, int64_t *checked) {
+    treeens::Packed p;
+    std::string err;
+    const int rc = treeens::pack_model(n_trees, tree_offsets, feature, threshold, left, right, value, 1,
+                                       flags, p, err);
+    if (rc != treeens::kOk) {
+        g_msg = err;
+        return rc;
+    }
+    if (!p.plan.coded) {
+        g_msg = "model is not coded";
+        return 2;
+    }
+    int64_t n = 0;
+    for (int f = 0; f < p.n_cols; f++) {
+        std::vector<float> xs = {INFINITY, -INFINITY, 0.0f, -0.0f, NAN};
+        for (uint32_t k = p.code_table_off[size_t(f)]; k < p.code_table_off[size_t(f) + 1]; k++) {
+            xs.push_back(p.code_table[k]);
+            xs.push_back(std::nextafter(p.code_table[k], -INFINITY));
+        }
+        for (float x : xs) {
+            const int32_t got = code_by_descent(p, f, x);
+            if (got < 0)
+                return bad("feature " + std::to_string(f) + ": the coding chunks do not hold its search");
+            if (got != int32_t(code_of(p, f, x)))
+                return bad("feature " + std::to_string(f) + ": the search gives " + std::to_string(got) +
+                           " where the count is " + std::to_string(code_of(p, f, x)));
+            n++;
+        }
+    }
+    if (checked)
+        *checked = n;
     return 0;
 }
 

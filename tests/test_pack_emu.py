@@ -34,6 +34,8 @@ def emu(tmp_path_factory):
     lib.emu_walk_compact.restype = ctypes.c_int
     lib.emu_walk_compact.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_uint32, P,
                                      ctypes.c_int64, ctypes.c_int32, P, P, P]
+    lib.emu_code_check.restype = ctypes.c_int
+    lib.emu_code_check.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_uint32, P]
     lib.emu_message.restype = ctypes.c_char_p
     lib.emu_tree_order.restype = ctypes.c_int
     lib.emu_tree_order.argtypes = [ctypes.c_int32, P, P, P, P, P, P, ctypes.c_uint32, P, P, ctypes.c_int32]
@@ -491,3 +493,51 @@ def test_compact_packets_not_built_where_they_do_not_apply(emu):
     Xm = W.random_docs(5, 10, 700)
     _check(emu, many, Xm, levels=(0,))
     assert _compact_k(emu, many, Xm) is None
+
+
+def test_coding_search_tables_long_lists(emu):
+    """The coding kernel's breadth-first search tables hold a feature's list padded with NaN to
+    2^s - 1 entries: lists of 5,000 and 16,383 distinct thresholds (the longest that fits one
+    coding workgroup's 16,384 slots) code exactly (the emulator checks every staged code of the
+    descent against a plain count), and the model's leaves match the oracle's."""
+    cfg = W.WORKLOADS["large_5kx256_f700_1M"]
+    ens = W.make_ensemble(cfg, n_trees=100)
+    internal = np.nonzero(ens.feature >= 0)[0]
+    rng = np.random.default_rng(7)
+    pick = rng.permutation(internal)
+    ens.feature[np.isin(ens.feature, (3, 10))] = 20  # features 3 and 10: only the lists below
+    ens.feature[pick[:16383]] = 10
+    ens.threshold[pick[:16383]] = (np.arange(16383, dtype=np.float32) + 0.5) / 16383
+    ens.feature[pick[16383:21383]] = 3
+    ens.threshold[pick[16383:21383]] = rng.random(5000, dtype=np.float32)
+    assert np.unique(ens.threshold[pick[:16383]]).size == 16383
+    X = W.make_docs(cfg, n_docs=150)
+    X[:, 10] = rng.random(150, dtype=np.float32)
+    X[:20, 10] = ens.threshold[pick[:20]]  # exact ties
+    X[20, [3, 10]] = np.nan
+    X[21, [3, 10]] = np.inf
+    plan = _check(emu, ens, X, levels=(0,))
+    assert plan[3] == 1, plan
+    for flags in (0, 1):
+        assert _code_check(emu, ens, flags) > 2 * (16383 + 5000)
+
+
+def _code_check(lib, ens, flags=0):
+    arrs = [np.ascontiguousarray(ens.tree_offsets, np.int64), np.ascontiguousarray(ens.feature, np.int32),
+            np.ascontiguousarray(ens.threshold, np.float32), np.ascontiguousarray(ens.left, np.int32),
+            np.ascontiguousarray(ens.right, np.int32), np.ascontiguousarray(ens.value, np.float32)]
+    n = np.zeros(1, np.int64)
+    rc = lib.emu_code_check(ens.n_trees, *[a.ctypes.data for a in arrs], flags, n.ctypes.data)
+    assert rc == 0, lib.emu_message().decode()
+    return int(n[0])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_coding_search_tables_at_every_threshold(emu, seed):
+    """Coded models with +-inf and special thresholds, both rules: the search gives the plain
+    count at every threshold, just below it, at +-inf, +-0 and NaN."""
+    pool = np.array([0.0, -0.0, 0.25, 0.5, 0.75, 1.0, np.inf, -np.inf], np.float32)
+    ens = W.random_ensemble(300 + seed, n_trees=40, n_features=700, min_leaves=200, max_leaves=256,
+                            thr_values=pool if seed % 2 else None)
+    for flags in (0, 1):
+        assert _code_check(emu, ens, flags) > 0
