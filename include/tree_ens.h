@@ -222,7 +222,10 @@ int tree_ens_predict_topk(const tree_ens_t *h, void *stream, const float *X, int
  *   max_depth      edges on the longest root-to-leaf path over all trees.
  *   packed_bytes   bytes of node records (8 per node); the device also holds the tile images
  *                  built from them (one set per tiling granularity) and, for models whose
- *                  groups of trees fit, the per-wave packets (one more copy of the records).
+ *                  groups of trees fit, the per-wave packets (one more copy of the records;
+ *                  for threshold-coded models of trees up to 511 nodes, compact packets of
+ *                  4-byte records with two 4-byte arrays of leaf values and node ids of the
+ *                  same shape).
  *   n_tiles        LDS tiles the tiled trees are streamed in for a large batch (trees too
  *                  large for one tile are walked from device memory and not counted).
  *   docs_per_block documents a workgroup stages in LDS (a power of two from 8 to 64).
