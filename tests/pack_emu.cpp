@@ -480,7 +480,8 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
 // per wave K windows of 4096 / K bytes after the document tile (aligned to their size), the
 // headers after all windows. Every feature read must stay in the document tile and every pair
 // read in the window of its slot. Outputs as emu_walk; returns 2 when the model has no compact
-// packets, else 0 or 1 with a message, or a negative packer status. *k_out: trees per lane.
+// packets, else 0 or 1 with a message, or a negative packer status. k_out[0]: trees per lane,
+// k_out[1]: groups in the fullest packet.
 int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feature,
                      const float *threshold, const int32_t *left, const int32_t *right,
                      const float *value, int32_t n_outputs, uint32_t flags, const float *X,
@@ -494,8 +495,10 @@ int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t
         g_msg = err;
         return rc;
     }
-    if (k_out)
-        *k_out = p.cp_k;
+    if (k_out) {
+        k_out[0] = p.cp_k;
+        k_out[1] = p.cp_max_groups;
+    }
     if (p.cp_k == 0) {
         g_msg = "no compact packets";
         return 2;

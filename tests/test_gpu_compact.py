@@ -98,3 +98,19 @@ def test_vector_valued_leaves(T, n_docs):
         got = got.cpu().numpy()
     ref = oracle.score_multi(ens, vals, X)
     assert_scores_close(got.ravel(), ref.ravel(), "vector-valued leaves")
+
+
+def test_packets_of_several_groups(T):
+    """Small trees share a window (several groups per packet: bodies one after another, one
+    root pair per group in the header) next to large ones that keep the plan coded."""
+    big = W.random_ensemble(41, n_trees=150, n_features=700, min_leaves=200, max_leaves=256)
+    small = W.random_ensemble(42, n_trees=130, n_features=700, min_leaves=16, max_leaves=32)
+    trees = [big.tree(t) for t in range(big.n_trees)] + [small.tree(t) for t in range(small.n_trees)]
+    offs = np.cumsum([0] + [len(t[0]) for t in trees]).astype(np.int64)
+    cat = [np.concatenate([np.asarray(t[k], dt) for t in trees]) for k, dt in
+           enumerate((np.int32, np.float32, np.int32, np.int32, np.float32))]
+    ens = W.Ensemble(offs, *cat, 700)
+    for n_docs in (100, 7000):
+        X = W.random_docs(43, n_docs, 700)
+        for flags in (0, 1):
+            _check(T, ens, X, f"several groups, {n_docs} docs, rule {flags}", flags)

@@ -69,13 +69,13 @@ def _walk_compact(lib, ens, X, flags=0, leaf_values=None):
     X = np.ascontiguousarray(X, np.float32)
     leaves = np.empty((X.shape[0], ens.n_trees), np.int32)
     scores = np.empty((X.shape[0], n_out), np.float64)
-    k = np.zeros(1, np.int32)
+    k = np.zeros(2, np.int32)
     rc = lib.emu_walk_compact(ens.n_trees, *[a.ctypes.data for a in arrs], n_out, flags, X.ctypes.data,
                               X.shape[0], X.shape[1], leaves.ctypes.data, scores.ctypes.data, k.ctypes.data)
     if rc == 2:
         return None
     assert rc == 0, lib.emu_message().decode()
-    return leaves, (scores[:, 0] if leaf_values is None else scores), int(k[0])
+    return leaves, (scores[:, 0] if leaf_values is None else scores), int(k[0]), int(k[1])
 
 
 def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
@@ -89,7 +89,7 @@ def _check(lib, ens, X, flags=0, levels=range(LEVELS)):
     # the compact packets, where the model has them, reach the same leaves
     compact = _walk_compact(lib, ens, X, flags)
     if compact is not None:
-        leaves, scores, _ = compact
+        leaves, scores = compact[:2]
         np.testing.assert_array_equal(leaves, ref_leaves, err_msg="compact packets")
         np.testing.assert_allclose(scores, ref_scores, rtol=1e-12, atol=1e-12, err_msg="compact packets")
     return plans[0]
@@ -432,9 +432,9 @@ def test_tree_size_limit(emu):
     assert rc == -2 and b"65535" in emu.emu_message()
 
 
-def _compact_k(lib, ens, X, flags=0):
+def _compact_k(lib, ens, X, flags=0, groups=False):
     got = _walk_compact(lib, ens, X, flags)
-    return None if got is None else got[2]
+    return None if got is None else (got[2:] if groups else got[2])
 
 
 def test_compact_packets_of_the_large_workload(emu):
@@ -473,6 +473,20 @@ def test_compact_packets_random_coded_models(emu, seed):
         plan = _check(emu, ens, X, flags=flags, levels=(0,))
         assert plan[3] == 1, plan
         assert _compact_k(emu, ens, X, flags) == 2
+
+
+def test_compact_packets_of_several_groups(emu):
+    """Trees small enough to share a window (here 130 trees of 16-32 leaves next to 150 of
+    200-256, which keep the plan coded) are packed several groups to a packet: the windows hold
+    one body after another and the header one root pair per group."""
+    big = W.random_ensemble(41, n_trees=150, n_features=700, min_leaves=200, max_leaves=256)
+    small = W.random_ensemble(42, n_trees=130, n_features=700, min_leaves=16, max_leaves=32)
+    ens = _stack([big.tree(t) for t in range(big.n_trees)] + [small.tree(t) for t in range(small.n_trees)], 700)
+    X = W.random_docs(43, 100, 700)
+    for flags in (0, 1):
+        _check(emu, ens, X, flags=flags, levels=(0,))
+        k, groups = _compact_k(emu, ens, X, flags, groups=True)
+        assert k == 2 and groups > 1, (k, groups)
 
 
 def test_compact_packets_not_built_where_they_do_not_apply(emu):
