@@ -252,6 +252,24 @@ int tree_ens_codegen_source(int32_t n_trees, const int64_t *tree_offsets, const 
  * NULL). */
 int tree_ens_outputs(const tree_ens_t *h, int32_t *n_outputs, int32_t *n_bags);
 
+/*
+ * tree_ens_kernel_timing -- measurement aid: time the scoring kernel of later predict calls with
+ * HIP events (the paper reports its timings as means over repeated trials, Section 4). enable !=
+ * 0 starts a new record: every later eager predict call of h (every mode; calls captured into a
+ * HIP graph are not timed) records an event on its stream right before and right after each
+ * launch of the scoring kernel, for the first 1,024 such launches; enable == 0 stops recording.
+ * The events are created on the handle's device by the first enabling call (no device memory is
+ * allocated) and live until destroy. Returns TREE_ENS_E_ARG for a NULL handle,
+ * TREE_ENS_E_DEVICE if an event cannot be created.
+ *
+ * tree_ens_kernel_time -- waits for the recorded events (a host wait on them, so the predicts
+ * must have been enqueued) and gives the sum of the timed launches' durations in milliseconds
+ * and their number (either pointer may be NULL). Neither call may run concurrently with a
+ * predict of h on another thread.
+ */
+int tree_ens_kernel_timing(const tree_ens_t *h, int32_t enable);
+int tree_ens_kernel_time(const tree_ens_t *h, double *total_ms, int32_t *launches);
+
 /* tree_ens_destroy -- free the handle and its device memory. NULL is accepted. The caller must
  * ensure no enqueued predict that uses h is still pending. */
 void tree_ens_destroy(tree_ens_t *h);

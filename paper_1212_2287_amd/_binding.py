@@ -68,6 +68,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tree_ens_codegen_source.argtypes = [i32, P, P, P, P, P, P, u32, P, i64, P]
     lib.tree_ens_outputs.restype = ctypes.c_int
     lib.tree_ens_outputs.argtypes = [P, P, P]
+    lib.tree_ens_kernel_timing.restype = ctypes.c_int
+    lib.tree_ens_kernel_timing.argtypes = [P, i32]
+    lib.tree_ens_kernel_time.restype = ctypes.c_int
+    lib.tree_ens_kernel_time.argtypes = [P, P, P]
     lib.tree_ens_predict.restype = ctypes.c_int
     lib.tree_ens_predict.argtypes = [P, P, P, i64, i32, P]
     lib.tree_ens_predict_noalloc.restype = ctypes.c_int
@@ -174,6 +178,18 @@ def tree_ens_outputs(h) -> tuple[int, int]:
     n_out, n_bags = ctypes.c_int32(), ctypes.c_int32()
     _check(load_library().tree_ens_outputs(h, ctypes.byref(n_out), ctypes.byref(n_bags)), "tree_ens_outputs")
     return n_out.value, n_bags.value
+
+
+def tree_ens_kernel_timing(h, enable: bool) -> None:
+    """Start (a new record) or stop timing the scoring launches of later predicts."""
+    _check(load_library().tree_ens_kernel_timing(h, 1 if enable else 0), "tree_ens_kernel_timing")
+
+
+def tree_ens_kernel_time(h) -> tuple[float, int]:
+    """(total milliseconds, launches) of the scoring launches timed since the last start."""
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    _check(load_library().tree_ens_kernel_time(h, ctypes.byref(ms), ctypes.byref(n)), "tree_ens_kernel_time")
+    return ms.value, n.value
 
 
 def _stream_of(t, stream) -> Optional[int]:
@@ -407,6 +423,12 @@ class TreeEnsemble:
 
     def info(self) -> dict:
         return tree_ens_info(self.handle)
+
+    def kernel_timing(self, enable: bool) -> None:
+        tree_ens_kernel_timing(self.handle, enable)
+
+    def kernel_time(self) -> tuple[float, int]:
+        return tree_ens_kernel_time(self.handle)
 
     def close(self) -> None:
         if self._h is not None:

@@ -1212,6 +1212,12 @@ struct tree_ens {
     // threshold codes, allocated when it is captured and kept until destroy.
     mutable std::mutex capture_mu;
     mutable std::vector<void *> capture_bufs;
+    // Kernel timing (tree_ens_kernel_timing): while `timing` is set, eager predicts record
+    // t_start[i] / t_stop[i] around the i-th scoring launch, i < t_used <= kMaxTimedLaunches.
+    mutable std::mutex timing_mu;
+    mutable bool timing = false;
+    mutable std::vector<hipEvent_t> t_start, t_stop;
+    mutable int32_t t_used = 0;
     // launch shape of the last batch size seen (callers usually repeat one batch size)
     mutable std::mutex shape_mu;
     mutable int64_t shape_blocks = -1;
@@ -1222,6 +1228,7 @@ struct tree_ens {
 
 namespace {
 constexpr size_t kScratchDoubles = size_t(1) << 17; // 1 MiB of split partials
+constexpr int kMaxTimedLaunches = 1024;             // event pairs of tree_ens_kernel_timing
 
 // Scratch of the allocation-free entry point (tree_ens_predict_noalloc): split partial sums and
 // threshold codes in one static array, which every device the library runs on holds until the
@@ -1273,6 +1280,10 @@ void free_device(tree_ens *h) {
         (void)hipEventDestroy(h->scratch_done);
     for (void *b : h->capture_bufs)
         (void)hipFree(b);
+    for (hipEvent_t ev : h->t_start)
+        (void)hipEventDestroy(ev);
+    for (hipEvent_t ev : h->t_stop)
+        (void)hipEventDestroy(ev);
     if (h->cg_module)
         (void)hipModuleUnload(h->cg_module);
 }
@@ -1626,6 +1637,24 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
     const double scale = 1.0 / double(h->n_bags);
     const int n_out = MODE == kModeVector ? h->n_outputs : 1;
     for (int chunk = 0; chunk < n_chunks && e == hipSuccess; ++chunk) {
+        // kernel timing: an event pair around this launch (eager calls only)
+        hipEvent_t t0 = nullptr, t1 = nullptr;
+        {
+            std::lock_guard<std::mutex> lock(h->timing_mu);
+            if (h->timing && h->t_used < int32_t(h->t_start.size())) {
+                hipStreamCaptureStatus tc = hipStreamCaptureStatusNone;
+                if (hipStreamIsCapturing(stream, &tc) != hipSuccess)
+                    tc = hipStreamCaptureStatusActive;
+                (void)hipGetLastError();
+                if (tc == hipStreamCaptureStatusNone) {
+                    t0 = h->t_start[size_t(h->t_used)];
+                    t1 = h->t_stop[size_t(h->t_used)];
+                    h->t_used++;
+                }
+            }
+        }
+        if (t0 && (e = hipEventRecord(t0, stream)) != hipSuccess)
+            break;
         hipLaunchKernelGGL(fn, dim3(unsigned(n_wgs)), dim3(kThreads), 0, stream, docs, n_docs,
                            row_stride, h->n_cols, images, slot_recs, tile_recs,
                            n_tiles, int32_t(shape.head), splits, h->plan.xs_bytes,
@@ -1636,6 +1665,8 @@ int launch_predict(const tree_ens *h, hipStream_t stream, const float *X, int64_
                            chunk, scale, cp ? treeens::kCompactPacketBytes / 8 : pk ? h->pk_recs : 0,
                            h->d_big, h->n_small, h->big_off0, h->d_cleaf, h->d_cleaf_id);
         e = hipGetLastError();
+        if (e == hipSuccess && t1)
+            e = hipEventRecord(t1, stream);
         if (e == hipSuccess && partials) {
             // the tail blocks' entries, in [doc][component] order
             const int64_t n_entries = tail_docs * comps;
@@ -1960,6 +1991,66 @@ int tree_ens_codegen_source(int32_t n_trees, const int64_t *tree_offsets, const 
         std::memcpy(buf, src.data(), n);
         buf[n] = '\0';
     }
+    return TREE_ENS_OK;
+}
+
+int tree_ens_kernel_timing(const tree_ens_t *h, int32_t enable) {
+    g_err.clear();
+    if (!h)
+        return fail(TREE_ENS_E_ARG, "handle is NULL");
+    std::lock_guard<std::mutex> lock(h->timing_mu);
+    if (!enable) {
+        h->timing = false;
+        return TREE_ENS_OK;
+    }
+    if (h->t_start.empty()) {
+        DeviceGuard g(h->device);
+        if (g.err != hipSuccess)
+            return hip_fail(g.err, "hipSetDevice");
+        for (int i = 0; i < kMaxTimedLaunches; ++i) {
+            hipEvent_t a = nullptr, b = nullptr;
+            hipError_t e = hipEventCreate(&a);
+            if (e == hipSuccess)
+                e = hipEventCreate(&b);
+            if (e != hipSuccess) {
+                if (a)
+                    (void)hipEventDestroy(a);
+                for (hipEvent_t ev : h->t_start)
+                    (void)hipEventDestroy(ev);
+                for (hipEvent_t ev : h->t_stop)
+                    (void)hipEventDestroy(ev);
+                h->t_start.clear();
+                h->t_stop.clear();
+                return hip_fail(e, "hipEventCreate");
+            }
+            h->t_start.push_back(a);
+            h->t_stop.push_back(b);
+        }
+    }
+    h->t_used = 0;
+    h->timing = true;
+    return TREE_ENS_OK;
+}
+
+int tree_ens_kernel_time(const tree_ens_t *h, double *total_ms, int32_t *launches) {
+    g_err.clear();
+    if (!h)
+        return fail(TREE_ENS_E_ARG, "handle is NULL");
+    std::lock_guard<std::mutex> lock(h->timing_mu);
+    double sum = 0.0;
+    for (int32_t i = 0; i < h->t_used; ++i) {
+        hipError_t e = hipEventSynchronize(h->t_stop[size_t(i)]);
+        float ms = 0.0f;
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&ms, h->t_start[size_t(i)], h->t_stop[size_t(i)]);
+        if (e != hipSuccess)
+            return hip_fail(e, "timing events");
+        sum += double(ms);
+    }
+    if (total_ms)
+        *total_ms = sum;
+    if (launches)
+        *launches = h->t_used;
     return TREE_ENS_OK;
 }
 

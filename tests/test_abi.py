@@ -104,6 +104,8 @@ def test_null_arguments(lib):
     assert lib.tree_ens_predict(None, None, None, 10, 4, None) == T.TREE_ENS_E_ARG
     assert lib.tree_ens_predict_leaves(None, None, None, 10, 4, None) == T.TREE_ENS_E_ARG
     assert lib.tree_ens_info(None, None, None, None, None, None, None) == T.TREE_ENS_E_ARG
+    assert lib.tree_ens_kernel_timing(None, 1) == T.TREE_ENS_E_ARG
+    assert lib.tree_ens_kernel_time(None, None, None) == T.TREE_ENS_E_ARG
     lib.tree_ens_destroy(None)  # accepted
     h = ctypes.c_void_p()
     assert lib.tree_ens_create(ctypes.byref(h), -1, None, None, None, None, None, None, 0) == T.TREE_ENS_E_ARG

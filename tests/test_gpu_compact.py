@@ -114,3 +114,27 @@ def test_packets_of_several_groups(T):
         X = W.random_docs(43, n_docs, 700)
         for flags in (0, 1):
             _check(T, ens, X, f"several groups, {n_docs} docs, rule {flags}", flags)
+
+
+def test_kernel_timing_events(T):
+    """The measurement aid times each scoring launch of later eager predicts: one launch per
+    predict (the coding pass and the split reduction are not counted), positive durations,
+    nothing after it is switched off, and a new start clears the record."""
+    import torch
+    cfg = W.WORKLOADS["large_5kx256_f700_1M"]
+    ens = W.make_ensemble(cfg, n_trees=60)
+    X = dev(W.make_docs(cfg, n_docs=3000))
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        m.kernel_timing(True)
+        for _ in range(3):
+            m.predict(X)
+        torch.cuda.synchronize()
+        ms, n = m.kernel_time()
+        assert n == 3 and ms > 0.0, (ms, n)
+        m.kernel_timing(False)
+        m.predict(X)
+        torch.cuda.synchronize()
+        assert m.kernel_time()[1] == 3
+        m.kernel_timing(True)
+        assert m.kernel_time() == (0.0, 0)
+        m.kernel_timing(False)
