@@ -138,3 +138,17 @@ def test_kernel_timing_events(T):
         m.kernel_timing(True)
         assert m.kernel_time() == (0.0, 0)
         m.kernel_timing(False)
+
+
+@pytest.mark.parametrize("n_features,min_leaves,max_leaves", [(750, 200, 256), (700, 257, 400)])
+def test_coded_models_that_keep_8_byte_packets(T, n_features, min_leaves, max_leaves):
+    """Coded 64-document models the compact packets do not take (a 751-column tile leaves no
+    room for the windows; trees over 511 nodes) walk the 8-byte records (packets or shared tiles) with threshold codes
+    staged unshifted; the emulator test pins which models take which."""
+    ens = W.random_ensemble(60 + n_features, n_trees=90, n_features=n_features, min_leaves=min_leaves,
+                            max_leaves=max_leaves)
+    X = W.random_docs(61, 3000, n_features, zero_frac=0.2)
+    with T.TreeEnsemble.from_ensemble(ens) as m:
+        assert m.info()["docs_per_block"] == 64
+    for flags in (0, 1):
+        _check(T, ens, X, f"8-byte coded packets, {n_features} features, rule {flags}", flags)

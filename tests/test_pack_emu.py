@@ -490,8 +490,14 @@ def test_compact_packets_of_several_groups(emu):
 
 
 def test_compact_packets_not_built_where_they_do_not_apply(emu):
-    """Float documents, trees over 511 nodes, and coded models with more distinct thresholds
-    per feature than the 11-bit field holds keep the 8-byte packets only."""
+    """Float documents, trees over 511 nodes, a 751-column document tile (no room for the
+    windows) and coded models with more distinct thresholds per feature than the 11-bit field
+    holds keep the 8-byte packets only."""
+    wide = W.random_ensemble(810, n_trees=90, n_features=750, min_leaves=200, max_leaves=256)
+    Xw = W.random_docs(61, 40, 750)
+    plan = _check(emu, wide, Xw, levels=(0,))
+    assert plan[0] == 64 and plan[3] == 1, plan  # coded, 64 documents
+    assert _compact_k(emu, wide, Xw) is None
     cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=50)
     assert _compact_k(emu, ens, W.make_docs(cfg, n_docs=10)) is None
