@@ -714,7 +714,7 @@ int pack_model(int32_t n_trees, const int64_t *tree_offsets, const int32_t *feat
         const int32_t max_ng = (kCompactHeaderBytes / 4 - kCompactHeaderWords) / K;
         bool ok = plan.coded && plan.docs_per_block == 64 && plan.lds_bytes == kLdsPerCu && n_trees > 0 &&
                   n_small == n_trees && n_cols + 1 <= kCompactMaxColumns && max_thr < kCompactNeverRight &&
-                  max_nodes <= kCompactMaxTreeNodes && cw + int64_t(W) * kCompactPacketBytes <= kLdsPerCu;
+                  max_nodes <= kCompactMaxTreeNodes && cw + int64_t(W) * kCompactWindowBytes <= kLdsPerCu;
         // per wave: runs (first round, groups) of consecutive rounds whose trees fit every window
         std::vector<std::vector<std::pair<int32_t, int32_t>>> runs(static_cast<size_t>(W));
         for (int32_t v = 0; v < W && ok; v++) {

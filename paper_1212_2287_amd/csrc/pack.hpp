@@ -113,10 +113,10 @@ constexpr int kPacketWalkers = 16;
 // leaf-vector row + 1 for vector-valued leaves) and, in a second array, its input node id.
 // Each wave's LDS holds K = 2 windows of 2 KiB (window i takes slot i of
 // every group of the packet; its last 8 bytes are a pair of zero records, {2047 << 21 | own
-// offset}, for idle slots, payload 0), then, in a separate region, a header:
+// offset}, for idle slots, payload 0) past the document tile. A packet is, in device memory,
+// its windows then a header of kCompactHeaderBytes, which the kernel keeps in registers:
 //   word 0 groups n, word 1 complete depth d (or -1), word 2 the wave's first group in the packet
 //   (later ones follow at stride 16), word 3 zero, words 4.. the K root records of each group.
-// In device memory a packet is its windows then its header (kCompactPacketBytes).
 constexpr int kCompactTrees = 2;          // K: trees per lane, one window each
 constexpr int kCompactWindowBytes = 4096; // all windows of one wave
 constexpr int kCompactHeaderBytes = 512;

@@ -609,7 +609,7 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
         }
     };
     // Compact packets (4-byte records): wave v owns K windows of kCompactWindowBytes / K bytes past
-    // the document tile and a header past all windows. A step reads the lane's staged value and
+    // the document tile; the packet's header row stays in registers. A step reads the lane's staged value and
     // the current record's whole children pair together (one dependent LDS round trip) and keeps
     // the side the comparison picks. Leaves hold no value: the leaf's position in its window
     // locates its payload (value bits, leaf-vector row + 1 or input node id) in arrays shaped
@@ -621,8 +621,6 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
             static_assert(K == treeens::kCompactTrees && kCpWin == 2048, "compact windows of 2 KiB");
             const uint32_t cw = (uint32_t(xs_bytes) + 2047u) & ~2047u;
             const uint32_t my_win = cw + uint32_t(wave) * treeens::kCompactWindowBytes;
-            const uint32_t my_hdr =
-                cw + treeens::kPacketWalkers * treeens::kCompactWindowBytes + uint32_t(wave) * treeens::kCompactHeaderBytes;
             const __amdgpu_buffer_rsrc_t leaf_rsrc =
                 __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(cleaf), 0, 0x7fffffff, 0x00020000);
             const __amdgpu_buffer_rsrc_t id_rsrc =
@@ -657,29 +655,27 @@ score_kernel(const void *__restrict__ Xv, int64_t n_docs, int32_t n_features, in
                 // this packet's rows have landed (the last group's payload loads may not have)
                 __builtin_amdgcn_s_waitcnt(MODE == kModeScore ? kWaitVmcnt0 | K : kWaitVmcnt0);
 #pragma unroll
-                for (int j = 0; j < kCpRows; ++j) {
-                    const uint32_t at = j < kCpRows - 1 ? my_win + uint32_t(j) * 512u : my_hdr;
-                    *reinterpret_cast<uint2 *>(lds + at + uint32_t(pk_lane_off)) = pa[j];
-                }
+                for (int j = 0; j < kCpRows - 1; ++j)
+                    *reinterpret_cast<uint2 *>(lds + my_win + uint32_t(j) * 512u + uint32_t(pk_lane_off)) = pa[j];
+                // The header row stays in registers (lane l holds header words 2l and 2l + 1):
+                // its fields and the groups' roots are read from there with v_readlane.
+                const uint2 hrow = pa[kCpRows - 1];
                 // the wave's own writes complete before it reads the packet back
                 __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
                 // the next packet (the last one again after the last: the loads stay
                 // unconditional, so the compiler counts them exactly when it waits for payloads)
                 fetch_compact(min(q + 1, t_hi - 1));
-                const uint32_t *hw = reinterpret_cast<const uint32_t *>(lds + my_hdr);
-                const int ng = __builtin_amdgcn_readfirstlane(int(hw[0]));
-                const int complete_depth = __builtin_amdgcn_readfirstlane(int(hw[1]));
-                const int first_group = __builtin_amdgcn_readfirstlane(int(hw[2]));
+                const int ng = __builtin_amdgcn_readlane(int(hrow.x), 0);
+                const int complete_depth = __builtin_amdgcn_readlane(int(hrow.y), 0);
+                const int first_group = __builtin_amdgcn_readlane(int(hrow.x), 1);
                 auto walk_groups = [&](auto complete_tag) {
                     constexpr bool kComplete = decltype(complete_tag)::value;
                     for (int j = 0; j < ng; ++j) {
+                        // group j's roots: header words 4 + 2j and 5 + 2j, lane 2 + j
+                        static_assert(treeens::kCompactHeaderWords == 4 && K == 2, "root lane");
                         uint32_t r[K];
-                        {
-                            const uint2 rr = *reinterpret_cast<const uint2 *>(
-                                lds + my_hdr + 4u * uint32_t(treeens::kCompactHeaderWords + j * K));
-                            r[0] = rr.x;
-                            r[1] = rr.y;
-                        }
+                        r[0] = uint32_t(__builtin_amdgcn_readlane(int(hrow.x), 2 + j));
+                        r[1] = uint32_t(__builtin_amdgcn_readlane(int(hrow.y), 2 + j));
                         uint32_t fa[K], xv[K], lo[K], hi[K];
                         auto issue = [&]() {
 #pragma unroll

@@ -477,8 +477,9 @@ int emu_walk(int32_t n_trees, const int64_t *tree_offsets, const int32_t *featur
 
 // Walk all documents through the compact packets (4-byte records, pair reads, leaf payloads in
 // their own arrays) the way the kernel addresses them: documents staged as code << 5 | 31,
-// per wave K windows of 4096 / K bytes after the document tile (aligned to their size), the
-// headers after all windows. Every feature read must stay in the document tile and every pair
+// per wave K windows of 4096 / K bytes after the document tile (aligned to their size), each
+// packet's header read from its image (the kernel keeps it in registers: header words 2l and
+// 2l + 1 in lane l, so every word it reads must lie in the 64 lanes' 512 bytes). Every feature read must stay in the document tile and every pair
 // read in the window of its slot. Outputs as emu_walk; returns 2 when the model has no compact
 // packets, else 0 or 1 with a message, or a negative packer status. k_out[0]: trees per lane,
 // k_out[1]: groups in the fullest packet.
@@ -511,10 +512,11 @@ int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t
         return bad("compact packets on a plan they do not support");
     const uint32_t xs = uint32_t(pl.xs_bytes);
     const uint32_t cw = uint32_t(treeens::compact_window_base(pl.xs_bytes));
-    const uint32_t ch = cw + uint32_t(W) * treeens::kCompactWindowBytes;
     const uint32_t win = uint32_t(treeens::kCompactWindowBytes / K);
-    if (cw % win || ch + uint32_t(W) * treeens::kCompactHeaderBytes > uint32_t(treeens::kLdsPerCu))
-        return bad("compact windows and headers do not fit the LDS");
+    if (cw % win || cw + uint32_t(W) * treeens::kCompactWindowBytes > uint32_t(treeens::kLdsPerCu))
+        return bad("compact windows do not fit the LDS");
+    if (treeens::kCompactHeaderBytes != 64 * 8)
+        return bad("compact header is not one 8-byte row of 64 lanes");
     const size_t total = size_t(W) * size_t(p.cp_per_walker) * size_t(kWords);
     if (p.cp_packets.size() != total || p.cp_leaf.size() != total || p.cp_leaf_id.size() != total)
         return bad("compact packet arrays have the wrong size");
@@ -545,21 +547,20 @@ int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t
             for (int32_t q = 0; q < p.cp_per_walker; q++) {
                 const size_t at = (size_t(v) * size_t(p.cp_per_walker) + size_t(q)) * size_t(kWords);
                 const uint32_t my_win = cw + uint32_t(v) * treeens::kCompactWindowBytes;
-                const uint32_t my_hdr = ch + uint32_t(v) * treeens::kCompactHeaderBytes;
                 std::memcpy(lds.data() + my_win, p.cp_packets.data() + at, treeens::kCompactWindowBytes);
-                std::memcpy(lds.data() + my_hdr, p.cp_packets.data() + at + treeens::kCompactWindowBytes / 4,
-                            treeens::kCompactHeaderBytes);
-                const int ng = int(u32_at(my_hdr)), complete = int32_t(u32_at(my_hdr + 4));
-                const int g0 = int(u32_at(my_hdr + 8));
+                const uint32_t *hdr = p.cp_packets.data() + at + treeens::kCompactWindowBytes / 4;
+                const int ng = int(hdr[0]), complete = int32_t(hdr[1]);
+                const int g0 = int(hdr[2]);
                 if (ng < 0 || treeens::kCompactHeaderWords + ng * K > treeens::kCompactHeaderBytes / 4)
                     return bad("compact header out of range");
                 for (int j = 0; j < ng; j++) {
                     const int g = g0 + j * W;
                     if (g % W != v)
                         return bad("a compact packet holds a group of another wave");
-                    const uint32_t roots = my_hdr + 4u * uint32_t(treeens::kCompactHeaderWords + j * K);
-                    if (roots % uint32_t(4 * K) != 0)
-                        return bad("a group's root records are not aligned for one read");
+                    // group j's K = 2 roots: header words 4 + 2j, 5 + 2j, i.e. lane 2 + j's pair
+                    const uint32_t root_word = uint32_t(treeens::kCompactHeaderWords + j * K);
+                    if (root_word % 2 != 0 || root_word / 2 != uint32_t(2 + j) || root_word / 2 > 63)
+                        return bad("a group's roots are not one lane's word pair of the header row");
                     for (int i = 0; i < K; i++) {
                         const int gt = g * K + i;
                         const uint32_t tb = my_win + uint32_t(i) * win;
@@ -567,7 +568,7 @@ int emu_walk_compact(int32_t n_trees, const int64_t *tree_offsets, const int32_t
                             return bad("compact: a complete packet has an idle slot");
                         for (int dl = 0; dl < DL && doc0 + dl < n_docs; dl++) {
                             const int64_t doc = doc0 + dl;
-                            uint32_t r = u32_at(roots + 4u * uint32_t(i));
+                            uint32_t r = hdr[root_word + uint32_t(i)];
                             int steps = 0;
                             auto step = [&](uint32_t cur, uint32_t *next) -> int {
                                 const uint32_t fa = ((cur >> 4) & 0x1FF80u) | uint32_t(dl * 2);

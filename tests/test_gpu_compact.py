@@ -140,11 +140,22 @@ def test_kernel_timing_events(T):
         m.kernel_timing(False)
 
 
-@pytest.mark.parametrize("n_features,min_leaves,max_leaves", [(750, 200, 256), (700, 257, 400)])
+def test_widest_coded_tile(T):
+    """767 features: the widest coded 64-document tile (98,304 bytes) next to the 32 windows,
+    the whole LDS."""
+    ens = W.random_ensemble(1577, n_trees=90, n_features=767, min_leaves=200, max_leaves=256)
+    internal = np.nonzero(ens.feature >= 0)[0]
+    ens.feature[internal[0]] = 766
+    X = W.random_docs(62, 3000, 767, zero_frac=0.2)
+    for flags in (0, 1):
+        _check(T, ens, X, f"767 features, rule {flags}", flags)
+
+
+@pytest.mark.parametrize("n_features,min_leaves,max_leaves", [(700, 257, 400)])
 def test_coded_models_that_keep_8_byte_packets(T, n_features, min_leaves, max_leaves):
-    """Coded 64-document models the compact packets do not take (a 751-column tile leaves no
-    room for the windows; trees over 511 nodes) walk the 8-byte records (packets or shared tiles) with threshold codes
-    staged unshifted; the emulator test pins which models take which."""
+    """Coded 64-document models the compact packets do not take (trees over 511 nodes) walk the
+    8-byte records with threshold codes staged unshifted; the emulator test pins which models
+    take which."""
     ens = W.random_ensemble(60 + n_features, n_trees=90, n_features=n_features, min_leaves=min_leaves,
                             max_leaves=max_leaves)
     X = W.random_docs(61, 3000, n_features, zero_frac=0.2)

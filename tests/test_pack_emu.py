@@ -489,15 +489,23 @@ def test_compact_packets_of_several_groups(emu):
         assert k == 2 and groups > 1, (k, groups)
 
 
-def test_compact_packets_not_built_where_they_do_not_apply(emu):
-    """Float documents, trees over 511 nodes, a 751-column document tile (no room for the
-    windows) and coded models with more distinct thresholds per feature than the 11-bit field
-    holds keep the 8-byte packets only."""
-    wide = W.random_ensemble(810, n_trees=90, n_features=750, min_leaves=200, max_leaves=256)
-    Xw = W.random_docs(61, 40, 750)
+@pytest.mark.parametrize("n_features", [750, 767])
+def test_compact_packets_for_the_widest_coded_tiles(emu, n_features):
+    """The windows fit next to every coded 64-document tile (up to 768 columns, 96 KiB: 98,304 +
+    16 x 4,096 bytes is the whole LDS; the packet header stays in registers)."""
+    wide = W.random_ensemble(810 + n_features, n_trees=90, n_features=n_features, min_leaves=200,
+                             max_leaves=256)
+    internal = np.nonzero(wide.feature >= 0)[0]
+    wide.feature[internal[0]] = n_features - 1  # the last column is read
+    Xw = W.random_docs(61, 70, n_features)
     plan = _check(emu, wide, Xw, levels=(0,))
     assert plan[0] == 64 and plan[3] == 1, plan  # coded, 64 documents
-    assert _compact_k(emu, wide, Xw) is None
+    assert _compact_k(emu, wide, Xw) == 2
+
+
+def test_compact_packets_not_built_where_they_do_not_apply(emu):
+    """Float documents, trees over 511 nodes, and coded models with more distinct thresholds
+    per feature than the 11-bit field holds keep the 8-byte packets only."""
     cfg = W.WORKLOADS["rank_1kx32"]
     ens = W.make_ensemble(cfg, n_trees=50)
     assert _compact_k(emu, ens, W.make_docs(cfg, n_docs=10)) is None
