@@ -3,7 +3,8 @@
 pair whole, with leaf payloads in device memory. Leaf ids bit-exact and scores within the
 tolerance against the oracle, for batch sizes that take every launch shape (a single document,
 split tails, whole-block heads), both tie rules, models mixed with small and single-leaf trees
-(idle slots in the last group), vector-valued leaves, and repeat calls bitwise equal. The CPU
+(idle slots in the last group), vector-valued leaves, repeat calls bitwise equal, and a seeded
+sweep of 24 random models of that shape with IEEE corner values and bags. The CPU
 emulator (tests/test_pack_emu.py) pins that these models get compact packets and walks them
 with the kernel's addressing."""
 from __future__ import annotations
@@ -11,6 +12,7 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
+import _compact_cases as CC
 import oracle
 import workloads as W
 from _gpu import assert_leaves_equal, assert_scores_close, dev
@@ -163,3 +165,28 @@ def test_coded_models_that_keep_8_byte_packets(T, n_features, min_leaves, max_le
         assert m.info()["docs_per_block"] == 64
     for flags in (0, 1):
         _check(T, ens, X, f"8-byte coded packets, {n_features} features, rule {flags}", flags)
+
+
+@pytest.mark.parametrize("seed", range(CC.N_CASES))
+def test_random_compact_models(T, seed):
+    """Seeded random models of the compact packets' shape (tests/_compact_cases.py: 420-767
+    features, large trees mixed with small and single-leaf ones, IEEE corner values, exact ties,
+    one to 9,000 documents, either rule, vector-valued leaves, bags): scores and leaf ids
+    against the oracle. The emulator test pins that 22 of the 24 take the compact packets."""
+    import torch
+    ens, X, rule, vals, n_bags = CC.case(seed)
+    what = f"compact case {seed}: {ens.n_trees} trees, {X.shape[1]} features, {X.shape[0]} docs, rule {rule}"
+    print(what, flush=True)
+    with T.TreeEnsemble.from_ensemble(ens, rule, leaf_values=vals, n_bags=n_bags) as m:
+        x = dev(X)
+        s = m.predict(x)
+        ids = m.predict_leaves(x)
+        torch.cuda.synchronize()
+        s, ids = s.cpu().numpy().astype(np.float64), ids.cpu().numpy()
+    _, ref_ids, _ = oracle.score(ens, X, rule=rule)
+    if vals is None:
+        ref = oracle.score(ens, X, rule=rule)[0] / n_bags
+    else:
+        ref = oracle.score_multi(ens, vals, X, n_bags=n_bags, rule=rule)
+    assert_scores_close(s.ravel(), ref.ravel(), what)
+    assert_leaves_equal(ids, ref_ids, what)

@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 import workloads as W
+import _compact_cases as _CC
 from _golden import load_hand_ensemble
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -435,6 +436,25 @@ def test_tree_size_limit(emu):
 def _compact_k(lib, ens, X, flags=0, groups=False):
     got = _walk_compact(lib, ens, X, flags)
     return None if got is None else (got[2:] if groups else got[2])
+
+
+@pytest.mark.parametrize("seed", range(_CC.N_CASES))
+def test_compact_sweep_cases(emu, seed):
+    """The GPU sweep's random models (tests/_compact_cases.py): all but two take the compact
+    packets (cases 0 and 7 keep the 8-byte records), some with several groups in a packet; the
+    compact walk of their first 200 documents reaches the oracle's leaves under the case's rule."""
+    ens, X, rule, _, _ = _CC.case(seed)
+    X = X[:200]
+    got = _walk_compact(emu, ens, X, rule)
+    if seed in (0, 7):
+        assert got is None
+        return
+    assert got is not None and got[2] == 2
+    ref_scores, ref_leaves, _ = oracle.score(ens, X, rule=rule)
+    np.testing.assert_array_equal(got[0], ref_leaves)
+    np.testing.assert_allclose(got[1], ref_scores, rtol=1e-12, atol=1e-12)
+    if seed in (4, 21):
+        assert got[3] == 3, "three groups in one packet"
 
 
 def test_compact_packets_of_the_large_workload(emu):
